@@ -1,0 +1,74 @@
+/*
+ * basp_oracle.h -- plain CPU reference for one rank's share of batch-aware
+ * Ulysses attention (BASP, "Batch-Aware Sequence Parallelism for LLM
+ * Training", Sec. II-A, Sec. II-C, Sec. IV, Alg. 1, Alg. 2).
+ *
+ * TEST INFRASTRUCTURE ONLY.  Only the test suite, the smoke check and the
+ * benchmark's CPU-baseline leg may load this library.  It shares no code,
+ * header or helper with the HIP library; the product path never calls it.
+ *
+ * Everything is fp64 (attention) or raw bytes (permutations), slow and plain.
+ * Layouts (row-major, innermost last):
+ *   sequence shard       [b, S/G, n, d]    one per group member j
+ *   head-sharded local   [b, S, n/G, d]
+ *   LSE                  [b, Hl, rows]     natural logarithm
+ * Return value of the int functions: 0 on success, a negative code on bad
+ * arguments (see basp_oracle.c).
+ */
+#ifndef BASP_ORACLE_H
+#define BASP_ORACLE_H
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Alg. 1 (group formation) and Alg. 2 (rank -> group, local rank). */
+int oracle_group_of(long world, long micro_batch, long global_rank,
+                    long *group, long *local_rank, long *group_size);
+
+/* Alg. 2: which sequence and which token range a global rank holds. */
+int oracle_seq_partition(long L, long K, long global_rank,
+                         long *seq_start, long *seq_end,
+                         long *tok_start, long *tok_end);
+
+/* Receive side of the Ulysses all-to-all, all G sources at once (Sec. II-C):
+ * dst[beta][j*S/G + t][h][e] = src_j[beta][t][rank*n/G + h][e].
+ * elem = bytes per element (2 or 4); copied as raw bytes. */
+int oracle_pack(const void *const *src, void *dst, long b, long S, long n,
+                long d, long G, long rank, long elem);
+
+/* Inverse on the rank's head slice; every other head of dst_j is untouched. */
+int oracle_unpack(const void *src, void *const *dst, long b, long S, long n,
+                  long d, long G, long rank, long elem);
+
+/* Causal scaled dot-product attention (Sec. II-A), local q head h reads local
+ * kv head h / (Hl/Hkl).  Computes rows [r0, r1) of every (beta, h):
+ *   o   [b, r1-r0, Hl, d],  lse [b, Hl, r1-r0].
+ * q [b,S,Hl,d], k/v [b,S,Hkl,d] are full tensors. */
+int oracle_attn_fwd(const double *q, const double *k, const double *v,
+                    double *o, double *lse, long b, long S, long Hl, long Hkl,
+                    long d, double scale, long r0, long r1);
+
+/* Backward of the above for the loss sum(O * dO).  o/lse are rows [r0, S)
+ * from oracle_attn_fwd(r0, S).  Produces exact gradients for query rows and
+ * key rows in [r0, S):  dq [b,S-r0,Hl,d], dk/dv [b,S-r0,Hkl,d]. */
+int oracle_attn_bwd(const double *q, const double *k, const double *v,
+                    const double *dout, const double *o, const double *lse,
+                    double *dq, double *dk, double *dv, long b, long S,
+                    long Hl, long Hkl, long d, double scale, long r0);
+
+/* Row-local results for a list of (beta, head, row) samples: O_i, LSE_i and
+ * dQ_i, each needing only keys j <= i.  o_out/dq_out [n, d], lse_out [n]. */
+int oracle_attn_rows(const double *q, const double *k, const double *v,
+                     const double *dout, long b, long S, long Hl, long Hkl,
+                     long d, double scale, long nsamp, const long *beta,
+                     const long *head, const long *row, double *o_out,
+                     double *lse_out, double *dq_out);
+
+/* Number of OpenMP threads the oracle runs with. */
+int oracle_threads(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif
