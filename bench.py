@@ -1,0 +1,172 @@
+"""Benchmark one GPU's share of batch-aware Ulysses attention on MI355X.
+
+A step is one pass of the whole share over one batch of synthetic inputs
+already resident in HBM:
+  pack(Q, K, V) -> causal GQA attention fwd -> unpack(O)
+  pack(dO) -> attention bwd -> unpack(dQ, dK, dV)
+The reported value is attention FLOPs (fwd + bwd, causal half of S^2,
+bwd = 2.5 x fwd) divided by the whole step's time, in TFLOP/s; the pack and
+unpack permutations are inside the step and also reported as GB/s.
+
+Prints one JSON line.  With --gpus N > 1 it exits: this build runs one rank's
+share on one GPU (the exchange between ranks is not part of it).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "causal attn fwd+bwd TFLOP/s + pack/unpack GB/s, one rank's share, 1 GPU"
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBPS = 8000.0
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def cpu_baseline(w, target_s: float):
+    """Time the oracle (fp64, OpenMP) on a bounded prefix of the workload.
+
+    Sample: sequence 0 of the share, every local head, the first S' tokens,
+    full forward and backward of causal attention restricted to them; S' is
+    chosen from a short calibration run so the sample takes ~target_s."""
+    import oracle
+    import torch
+    from synth_inputs import global_tensors, shards_of
+
+    q, k, v, do = global_tensors(w)
+    loc = lambda x, n: x[w.seq_offset:w.seq_offset + 1, :, w.rank * (n // w.G):(w.rank + 1) * (n // w.G)]
+    ql, kl, vl, dl = loc(q, w.H), loc(k, w.H_kv), loc(v, w.H_kv), loc(do, w.H)
+
+    def run(Sp):
+        sl = lambda x: x[:, :Sp].double().contiguous().numpy()
+        qq, kk, vv, dd = sl(ql), sl(kl), sl(vl), sl(dl)
+        t0 = time.perf_counter()
+        o, lse = oracle.attn_fwd(qq, kk, vv, w.scale)
+        oracle.attn_bwd(qq, kk, vv, dd, o, lse, w.scale)
+        return time.perf_counter() - t0
+
+    cal = min(512, w.S)
+    t_cal = run(cal)
+    Sp = int(cal * (target_s / max(t_cal, 1e-6)) ** 0.5)
+    Sp = max(cal, min(w.S, (Sp // 64) * 64))
+    secs = run(Sp)
+    flops = 3.5 * 2.0 * 1 * w.Hl * w.d * float(Sp) ** 2
+    return {"value": flops / secs / 1e12, "unit": "TFLOP/s", "cores": oracle.threads(),
+            "kind": "oracle",
+            "sample": f"fp64 oracle fwd+bwd, sequence 0, all {w.Hl} local heads, first {Sp} "
+                      f"of {w.S} tokens ({secs:.1f} s)",
+            "seconds": secs}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="llama3_8b_s32k")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py measures one rank's share on one GPU; --gpus {args.gpus} is not "
+              "supported (the inter-GPU exchange is outside this build)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2609_03151_amd as basp
+    from paper_2609_03151_amd.share import RankShare
+    from synth_inputs import WORKLOADS, global_tensors, shards_of
+
+    basp.lib()
+    w = WORKLOADS[args.workload]
+    log(f"[bench] workload {w.name}: b={w.b} S={w.S} H={w.H} H_kv={w.H_kv} d={w.d} "
+        f"G={w.G} rank={w.rank}")
+    q, k, v, do = global_tensors(w)
+    dev = lambda x: [s.cuda() for s in shards_of(x, w)]
+    sh = RankShare(dev(q), dev(k), dev(v), dev(do), G=w.G, rank=w.rank, scale=w.scale)
+    del q, k, v, do
+    log("[bench] inputs on device")
+
+    for _ in range(args.warmup):
+        sh.step()
+    torch.cuda.synchronize()
+    log("[bench] warmup done")
+
+    phases = ["pack_qkv", "attn_fwd", "unpack_o", "pack_do", "attn_bwd", "unpack_grads"]
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(phases) + 1)]
+          for _ in range(args.steps)]
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for s in range(args.steps):
+        e = ev[s]
+        e[0].record()
+        for i, ph in enumerate(phases):
+            getattr(sh, ph)()
+            e[i + 1].record()
+    stop.record()
+    torch.cuda.synchronize()
+    total_ms = start.elapsed_time(stop)
+    ms_step = total_ms / args.steps
+    phase_ms = {ph: sum(ev[s][i].elapsed_time(ev[s][i + 1]) for s in range(args.steps)) / args.steps
+                for i, ph in enumerate(phases)}
+    log(f"[bench] {args.steps} steps, {ms_step:.3f} ms/step; phases {phase_ms}")
+
+    fwd_f, bwd_f = sh.attn_fwd_flops(), sh.attn_bwd_flops()
+    value = (fwd_f + bwd_f) / (ms_step * 1e-3) / 1e12
+    nbytes = sh.pack_unpack_bytes()
+    perm_ms = sum(phase_ms[p] for p in nbytes)
+    perm_gbps = sum(nbytes.values()) / (perm_ms * 1e-3) / 1e9
+    fwd_tf = fwd_f / (phase_ms["attn_fwd"] * 1e-3) / 1e12
+    bwd_tf = bwd_f / (phase_ms["attn_bwd"] * 1e-3) / 1e12
+    dom = "attn_bwd" if phase_ms["attn_bwd"] >= phase_ms["attn_fwd"] else "attn_fwd"
+    achieved = bwd_tf if dom == "attn_bwd" else fwd_tf
+    out = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": w.name, "b": w.b, "S": w.S, "H": w.H, "H_kv": w.H_kv, "d": w.d,
+                   "G": w.G, "rank": w.rank, "causal": True, "inputs": "bf16 N(0,1), seeded"},
+        "roofline": {
+            "kernel": ("basp_attn_bwd (bwd_pre + bwd_dkdv + bwd_dq)" if dom == "attn_bwd"
+                       else "basp_attn_fwd"),
+            "bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+        },
+        "attn_fwd_tflops": round(fwd_tf, 2),
+        "attn_bwd_tflops": round(bwd_tf, 2),
+        "attn_fwd_frac": round(fwd_tf / PEAK_BF16_TFLOPS, 4),
+        "pack_unpack_gbps": round(perm_gbps, 1),
+        "pack_unpack_frac": round(perm_gbps / PEAK_HBM_GBPS, 4),
+        "pack_unpack_gbps_by_call": {p: round(nbytes[p] / (phase_ms[p] * 1e-3) / 1e9, 1)
+                                     for p in nbytes},
+        "phase_ms": {p: round(t, 4) for p, t in phase_ms.items()},
+        "cpu_baseline": None,
+    }
+    if not args.no_cpu_baseline:
+        log("[bench] timing the CPU oracle sample")
+        out["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

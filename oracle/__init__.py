@@ -144,8 +144,8 @@ def unpack(local, shards, rank: int):
     for a in shards:
         if not (isinstance(a, np.ndarray) and a.flags.c_contiguous):
             raise OracleError("unpack targets must be C-contiguous numpy arrays")
-        if a.dtype != src.dtype:
-            raise OracleError("dtype mismatch")
+        if a.dtype.itemsize != src.dtype.itemsize:
+            raise OracleError("element size mismatch")
     ptrs = (ctypes.c_void_p * G)(*[a.ctypes.data for a in shards])
     rc = lib().oracle_unpack(_ptr(src), ptrs, b, Sg * G, n, d, G, rank,
                              src.dtype.itemsize)

@@ -1,0 +1,198 @@
+"""Python binding of libbasp: one GPU's share of batch-aware Ulysses attention.
+
+Argument marshalling only: every function checks tensor devices, dtypes and
+contiguity, then passes raw device pointers, sizes and the current HIP stream
+to the C ABI of ``include/basp.h``.  All work runs in the library's HIP
+kernels; there is no fallback.  If ``libbasp.so`` has not been built, importing
+the library raises.
+
+Names follow the C ABI: ``pack``, ``unpack``, ``attn_fwd``, ``attn_bwd``,
+``attn_bwd_workspace_bytes``, ``validate``, ``group_of``, ``status_str``.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libbasp.so")
+
+BASP_BF16, BASP_F32 = 0, 1
+STATUS = {
+    0: "BASP_OK", 1: "BASP_ERR_NULL", 2: "BASP_ERR_SHAPE", 3: "BASP_ERR_RANK",
+    4: "BASP_ERR_UNSUPPORTED", 5: "BASP_ERR_ALIGN", 6: "BASP_ERR_WORKSPACE",
+    7: "BASP_ERR_HIP", 8: "BASP_ERR_DP_FALLBACK",
+}
+# Every symbol include/basp.h declares.
+EXPORTS = ("basp_status_str", "basp_group_of", "basp_validate", "basp_pack",
+           "basp_unpack", "basp_attn_fwd", "basp_attn_bwd_workspace_bytes",
+           "basp_attn_bwd")
+
+
+class BaspError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        self.status = status
+        super().__init__(f"{what}: {status_str(status)}")
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded libbasp.so; raises if it is not built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(
+            f"{LIB_PATH} is not built: run `python -c 'import __graft_entry__ as g; g.build()'` "
+            "or `python paper_2609_03151_amd/build.py`")
+    L = ctypes.CDLL(LIB_PATH)
+    i, vp, sz, f = ctypes.c_int, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_float
+    ip = ctypes.POINTER(ctypes.c_int)
+    L.basp_status_str.argtypes = [i]
+    L.basp_status_str.restype = ctypes.c_char_p
+    L.basp_group_of.argtypes = [i, i, i, ip, ip, ip]
+    L.basp_validate.argtypes = [i] * 7
+    L.basp_pack.argtypes = [ctypes.POINTER(vp), vp] + [i] * 7 + [vp]
+    L.basp_unpack.argtypes = [vp, ctypes.POINTER(vp)] + [i] * 7 + [vp]
+    L.basp_attn_fwd.argtypes = [vp] * 5 + [i] * 6 + [f, vp]
+    L.basp_attn_bwd_workspace_bytes.argtypes = [i] * 6
+    L.basp_attn_bwd_workspace_bytes.restype = sz
+    L.basp_attn_bwd.argtypes = [vp] * 10 + [sz] + [i] * 6 + [f, vp]
+    for name in ("basp_group_of", "basp_validate", "basp_pack", "basp_unpack",
+                 "basp_attn_fwd", "basp_attn_bwd"):
+        getattr(L, name).restype = i
+    _lib = L
+    return L
+
+
+def status_str(status: int) -> str:
+    return lib().basp_status_str(int(status)).decode()
+
+
+def _check(rc: int, what: str):
+    if rc != 0:
+        raise BaspError(rc, what)
+
+
+def _stream(t: torch.Tensor):
+    return ctypes.c_void_p(torch.cuda.current_stream(t.device).cuda_stream)
+
+
+def _dev(t: torch.Tensor, name: str, dtype=None):
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError(f"{name} must be a CUDA (HIP) tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return BASP_BF16
+    if t.dtype == torch.float32:
+        return BASP_F32
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+# ------------------------------------------------------------ host helpers
+def group_of(world: int, micro_batch: int, global_rank: int):
+    """(group, local_rank, group_size) of a global rank (Alg. 1 / Alg. 2)."""
+    g, l, k = ctypes.c_int(), ctypes.c_int(), ctypes.c_int()
+    _check(lib().basp_group_of(world, micro_batch, global_rank, ctypes.byref(g),
+                               ctypes.byref(l), ctypes.byref(k)), "basp_group_of")
+    return g.value, l.value, k.value
+
+
+def validate(b, S, H, H_kv, d, G, rank) -> int:
+    """Status code of a share's parameters (0 = valid); no GPU needed."""
+    return lib().basp_validate(b, S, H, H_kv, d, G, rank)
+
+
+# ------------------------------------------------------------ permutations
+def pack(shards, rank: int, out: torch.Tensor | None = None) -> torch.Tensor:
+    """G shards [b, S/G, n, d] -> the rank's head-sharded [b, S, n/G, d]."""
+    G = len(shards)
+    b, Sg, n, d = shards[0].shape
+    ptrs = (ctypes.c_void_p * G)(*[_dev(s, f"shards[{j}]", shards[0].dtype).value
+                                   for j, s in enumerate(shards)])
+    for s in shards:
+        if s.shape != shards[0].shape or s.device != shards[0].device:
+            raise ValueError("shards differ in shape or device")
+    if out is None:
+        out = torch.empty((b, Sg * G, max(n // G, 0), d), dtype=shards[0].dtype,
+                          device=shards[0].device)
+    _check(lib().basp_pack(ptrs, _dev(out, "out", shards[0].dtype), b, Sg * G, n, d, G, rank,
+                           _dtype_code(out), _stream(out)), "basp_pack")
+    return out
+
+
+def unpack(local: torch.Tensor, shards, rank: int):
+    """Write local [b, S, n/G, d] into the rank's head slice of every shard."""
+    G = len(shards)
+    b, Sg, n, d = shards[0].shape
+    ptrs = (ctypes.c_void_p * G)(*[_dev(s, f"shards[{j}]", local.dtype).value
+                                   for j, s in enumerate(shards)])
+    _check(lib().basp_unpack(_dev(local, "local"), ptrs, b, Sg * G, n, d, G, rank,
+                             _dtype_code(local), _stream(local)), "basp_unpack")
+    return shards
+
+
+# -------------------------------------------------------------- attention
+def _attn_dims(q, k, G):
+    b, S, Hl, d = q.shape
+    Hkl = k.shape[2]
+    if k.shape[:2] != (b, S) or k.shape[3] != d:
+        raise ValueError("q and k/v disagree in shape")
+    return b, S, Hl * G, Hkl * G, d
+
+
+def attn_fwd(q, k, v, G: int = 1, scale: float | None = None, out=None, lse=None):
+    """Causal GQA attention of the local heads: returns (o bf16, lse fp32 [b,Hl,S])."""
+    b, S, H, H_kv, d = _attn_dims(q, k, G)
+    scale = d ** -0.5 if scale is None else scale
+    if v.shape != k.shape:
+        raise ValueError("v must have k's shape")
+    if out is None:
+        out = torch.empty_like(q)
+    if lse is None:
+        lse = torch.empty((b, q.shape[2], S), dtype=torch.float32, device=q.device)
+    _check(lib().basp_attn_fwd(_dev(q, "q", torch.bfloat16), _dev(k, "k", torch.bfloat16),
+                               _dev(v, "v", torch.bfloat16), _dev(out, "o", torch.bfloat16),
+                               _dev(lse, "lse", torch.float32), b, S, H, H_kv, d, G,
+                               float(scale), _stream(q)), "basp_attn_fwd")
+    return out, lse
+
+
+def attn_bwd_workspace_bytes(b, S, H, H_kv, d, G) -> int:
+    return int(lib().basp_attn_bwd_workspace_bytes(b, S, H, H_kv, d, G))
+
+
+def attn_bwd(q, k, v, o, lse, do, G: int = 1, scale: float | None = None,
+             dq=None, dk=None, dv=None, workspace=None):
+    """Backward of attn_fwd: returns (dq, dk, dv) in fp32."""
+    b, S, H, H_kv, d = _attn_dims(q, k, G)
+    scale = d ** -0.5 if scale is None else scale
+    if dq is None:
+        dq = torch.empty(q.shape, dtype=torch.float32, device=q.device)
+    if dk is None:
+        dk = torch.empty(k.shape, dtype=torch.float32, device=q.device)
+    if dv is None:
+        dv = torch.empty(v.shape, dtype=torch.float32, device=q.device)
+    need = attn_bwd_workspace_bytes(b, S, H, H_kv, d, G)
+    if workspace is None:
+        workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=q.device)
+    _check(lib().basp_attn_bwd(
+        _dev(q, "q", torch.bfloat16), _dev(k, "k", torch.bfloat16),
+        _dev(v, "v", torch.bfloat16), _dev(o, "o", torch.bfloat16),
+        _dev(lse, "lse", torch.float32), _dev(do, "do", torch.bfloat16),
+        _dev(dq, "dq", torch.float32), _dev(dk, "dk", torch.float32),
+        _dev(dv, "dv", torch.float32), _dev(workspace, "workspace"),
+        workspace.numel() * workspace.element_size(), b, S, H, H_kv, d, G, float(scale),
+        _stream(q)), "basp_attn_bwd")
+    return dq, dk, dv

@@ -1,0 +1,109 @@
+"""One rank's share of a batch-aware Ulysses attention layer, on one GPU.
+
+A rank of a BASP group (G members, Sec. IV of the paper) receives G sequence
+shards of Q, K, V, runs attention on its H/G query heads over the full
+sequence, and returns the output to the G shard owners; the backward mirrors
+this with dO in and dQ, dK, dV out (the transposed exchanges of Ulysses,
+Sec. II-C).  `RankShare` holds every device buffer of that share, allocated
+once, and chains the library calls:
+
+  forward:  pack(Q), pack(K), pack(V) -> attn_fwd -> unpack(O)
+  backward: pack(dO) -> attn_bwd -> unpack(dQ), unpack(dK), unpack(dV)
+
+The exchange itself (RCCL all-to-all) is outside this share: the shard
+buffers stand for the receive and send buffers of that exchange.
+"""
+from __future__ import annotations
+
+import torch
+
+from . import attn_bwd, attn_bwd_workspace_bytes, attn_fwd, pack, unpack
+
+
+class RankShare:
+    def __init__(self, q_shards, k_shards, v_shards, do_shards, G: int, rank: int,
+                 scale: float | None = None):
+        self.G, self.rank = G, rank
+        self.q_shards, self.k_shards, self.v_shards = q_shards, k_shards, v_shards
+        self.do_shards = do_shards
+        b, Sg, H, d = q_shards[0].shape
+        H_kv = k_shards[0].shape[2]
+        self.b, self.S, self.H, self.H_kv, self.d = b, Sg * G, H, H_kv, d
+        self.Hl, self.Hkl = H // G, H_kv // G
+        self.scale = d ** -0.5 if scale is None else scale
+        dev = q_shards[0].device
+        bf, f32 = torch.bfloat16, torch.float32
+        S = self.S
+        # head-sharded local tensors
+        self.q = torch.empty((b, S, self.Hl, d), dtype=bf, device=dev)
+        self.k = torch.empty((b, S, self.Hkl, d), dtype=bf, device=dev)
+        self.v = torch.empty_like(self.k)
+        self.o = torch.empty_like(self.q)
+        self.lse = torch.empty((b, self.Hl, S), dtype=f32, device=dev)
+        self.do = torch.empty_like(self.q)
+        self.dq = torch.empty((b, S, self.Hl, d), dtype=f32, device=dev)
+        self.dk = torch.empty((b, S, self.Hkl, d), dtype=f32, device=dev)
+        self.dv = torch.empty_like(self.dk)
+        # send buffers of the output exchanges (shard layout)
+        self.o_shards = [torch.zeros((b, Sg, H, d), dtype=bf, device=dev) for _ in range(G)]
+        self.dq_shards = [torch.zeros((b, Sg, H, d), dtype=f32, device=dev) for _ in range(G)]
+        self.dk_shards = [torch.zeros((b, Sg, H_kv, d), dtype=f32, device=dev) for _ in range(G)]
+        self.dv_shards = [torch.zeros((b, Sg, H_kv, d), dtype=f32, device=dev) for _ in range(G)]
+        ws = attn_bwd_workspace_bytes(b, S, H, H_kv, d, G)
+        self.workspace = torch.empty(max(ws, 16), dtype=torch.uint8, device=dev)
+
+    # individual steps, so that callers can time them
+    def pack_qkv(self):
+        pack(self.q_shards, self.rank, out=self.q)
+        pack(self.k_shards, self.rank, out=self.k)
+        pack(self.v_shards, self.rank, out=self.v)
+
+    def attn_fwd(self):
+        attn_fwd(self.q, self.k, self.v, G=self.G, scale=self.scale, out=self.o, lse=self.lse)
+
+    def unpack_o(self):
+        unpack(self.o, self.o_shards, self.rank)
+
+    def pack_do(self):
+        pack(self.do_shards, self.rank, out=self.do)
+
+    def attn_bwd(self):
+        attn_bwd(self.q, self.k, self.v, self.o, self.lse, self.do, G=self.G, scale=self.scale,
+                 dq=self.dq, dk=self.dk, dv=self.dv, workspace=self.workspace)
+
+    def unpack_grads(self):
+        unpack(self.dq, self.dq_shards, self.rank)
+        unpack(self.dk, self.dk_shards, self.rank)
+        unpack(self.dv, self.dv_shards, self.rank)
+
+    def forward(self):
+        self.pack_qkv()
+        self.attn_fwd()
+        self.unpack_o()
+
+    def backward(self):
+        self.pack_do()
+        self.attn_bwd()
+        self.unpack_grads()
+
+    def step(self):
+        self.forward()
+        self.backward()
+
+    # work counts (FlashAttention convention: causal half of S^2)
+    def attn_fwd_flops(self) -> float:
+        return 2.0 * self.b * self.Hl * self.d * float(self.S) ** 2
+
+    def attn_bwd_flops(self) -> float:
+        return 2.5 * self.attn_fwd_flops()
+
+    def pack_unpack_bytes(self) -> dict:
+        """Bytes read + written by each permutation (each moved element twice)."""
+        bq = self.q.numel() * 2
+        bkv = self.k.numel() * 2
+        return {
+            "pack_qkv": 2 * (bq + 2 * bkv),
+            "unpack_o": 2 * bq,
+            "pack_do": 2 * bq,
+            "unpack_grads": 2 * (self.dq.numel() + 2 * self.dk.numel()) * 4,
+        }

@@ -1,0 +1,131 @@
+"""The C ABI of libbasp on a host without a GPU: the library loads, exports
+every function include/basp.h declares, and rejects each host-detectable
+misuse with its status code before making any HIP call."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2609_03151_amd as basp
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+GOLDEN = os.path.join(ROOT, "tests", "golden")
+
+OK, NULL, SHAPE, RANK, UNSUP, ALIGN, WS, HIP, DP = range(9)
+
+
+def _declared():
+    with open(os.path.join(ROOT, "include", "basp.h")) as f:
+        text = f.read()
+    return sorted(set(re.findall(r"\b(basp_[a-z_]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol():
+    L = basp.lib()
+    names = _declared()
+    assert set(names) == set(basp.EXPORTS)
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def test_status_strings():
+    for code, name in basp.STATUS.items():
+        assert basp.status_str(code).startswith(name)
+    assert "unknown" in basp.status_str(99)
+
+
+def test_group_of_matches_paper_example_and_errors():
+    with open(os.path.join(GOLDEN, "group_formation_n4_b2.txt")) as f:
+        rows = [list(map(int, ln.split())) for ln in f if ln.strip() and not ln.startswith("#")]
+    for rank, g, l, K, _seq, _chunk in rows:
+        assert basp.group_of(4, 2, rank) == (g, l, K)
+    for (N, B, r), code in {(6, 4, 0): SHAPE, (4, 8, 0): DP, (4, 2, 4): RANK,
+                            (0, 1, 0): SHAPE, (4, 2, -1): RANK}.items():
+        with pytest.raises(basp.BaspError) as e:
+            basp.group_of(N, B, r)
+        assert e.value.status == code
+    g = ctypes.c_int()
+    assert basp.lib().basp_group_of(4, 2, 0, None, ctypes.byref(g), ctypes.byref(g)) == NULL
+
+
+@pytest.mark.parametrize("args,code", [
+    ((1, 32768, 32, 8, 128, 4, 1), OK),
+    ((1, 65536, 28, 4, 128, 4, 3), OK),
+    ((2, 512, 8, 8, 64, 2, 0), OK),
+    ((0, 512, 8, 8, 64, 2, 0), OK),          # empty batch is valid
+    ((1, 0, 8, 8, 64, 2, 0), OK),            # empty sequence is valid
+    ((-1, 512, 8, 8, 64, 2, 0), SHAPE),
+    ((1, 510, 8, 8, 64, 4, 0), SHAPE),       # S % G
+    ((1, 512, 6, 2, 64, 4, 0), SHAPE),       # H % G
+    ((1, 512, 8, 2, 64, 4, 0), SHAPE),       # H_kv % G
+    ((1, 512, 12, 8, 64, 4, 0), SHAPE),      # H % H_kv
+    ((1, 512, 8, 8, 64, 2, 2), RANK),
+    ((1, 512, 8, 8, 64, 2, -1), RANK),
+    ((1, 512, 8, 8, 96, 2, 0), UNSUP),       # head dim
+])
+def test_validate(args, code):
+    assert basp.validate(*args) == code
+
+
+def _fake(addr):
+    return ctypes.c_void_p(addr)
+
+
+def test_pack_rejects_before_any_hip_call():
+    """Only invalid (or empty) calls here: the pointers are fake host values,
+    so a call that passed validation would launch on them."""
+    L = basp.lib()
+    vp = ctypes.c_void_p
+    good = (vp * 2)(0x1000, 0x2000)
+    dst = _fake(0x3000)
+    cases = [
+        ((good, dst, 1, 63, 8, 64, 2, 0, 0), SHAPE),
+        ((good, dst, 1, 64, 7, 64, 2, 0, 0), SHAPE),
+        ((good, dst, 1, 64, 8, 64, 2, 2, 0), RANK),
+        ((good, dst, 1, 64, 8, 64, 2, 0, 5), UNSUP),
+        ((None, dst, 1, 64, 8, 64, 2, 0, 0), NULL),
+        (((vp * 2)(0x1000, 0), dst, 1, 64, 8, 64, 2, 0, 0), NULL),
+        (((vp * 2)(0x1001, 0x2000), dst, 1, 64, 8, 64, 2, 0, 0), ALIGN),
+        (((vp * 2)(0x1002, 0x2000), dst, 1, 64, 8, 64, 2, 0, 1), ALIGN),
+        ((good, dst, 0, 64, 8, 64, 2, 0, 0), OK),      # empty: nothing enqueued
+    ]
+    for args, code in cases:
+        assert L.basp_pack(*args, None) == code, args
+        src = args[1]
+        assert L.basp_unpack(src, args[0], *args[2:], None) == code, args
+
+
+def test_pack_rejects_group_beyond_maximum():
+    L = basp.lib()
+    G = 256
+    ptrs = (ctypes.c_void_p * G)(*[0x1000 * (j + 1) for j in range(G)])
+    assert L.basp_pack(ptrs, _fake(0x100000), 1, G, G, 8, G, 0, 0, None) == UNSUP
+
+
+def test_attn_rejects_before_any_hip_call():
+    L = basp.lib()
+    p = [_fake(0x10000 * (i + 1)) for i in range(10)]
+    fwd = lambda *a, ptrs=p[:5], scale=0.125: L.basp_attn_fwd(*ptrs, *a, ctypes.c_float(scale), None)
+    assert fwd(1, 128, 8, 2, 96, 2) == UNSUP
+    assert fwd(1, 128, 8, 2, 128, 2, scale=0.0) == UNSUP
+    assert fwd(1, 128, 8, 2, 128, 2, scale=float("nan")) == UNSUP
+    assert fwd(1, 127, 8, 2, 128, 2) == SHAPE
+    assert fwd(1, 128, 8, 2, 128, 2, ptrs=[None] + p[1:5]) == NULL
+    assert fwd(1, 128, 8, 2, 128, 2, ptrs=[_fake(0x10008)] + p[1:5]) == ALIGN
+    assert fwd(0, 128, 8, 2, 128, 2) == OK
+
+    need = L.basp_attn_bwd_workspace_bytes(1, 128, 8, 2, 128, 2)
+    assert need >= 1 * 4 * 128 * 4 and need % 256 == 0
+    bwd = lambda ws, n, *a: L.basp_attn_bwd(*p[:9], ws, n, *a, ctypes.c_float(0.125), None)
+    assert bwd(p[9], need - 1, 1, 128, 8, 2, 128, 2) == WS
+    assert bwd(None, need, 1, 128, 8, 2, 128, 2) == NULL
+    assert bwd(p[9], need, 1, 128, 8, 2, 64, 3) == SHAPE
+    assert bwd(p[9], 0, 0, 128, 8, 2, 128, 2) == OK
+
+
+def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
+    monkeypatch.setattr(basp, "_lib", None)
+    monkeypatch.setattr(basp, "LIB_PATH", str(tmp_path / "missing.so"))
+    with pytest.raises(ImportError):
+        basp.lib()

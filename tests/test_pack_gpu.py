@@ -1,0 +1,142 @@
+"""GPU parity of basp_pack / basp_unpack: bit-exact against the oracle at
+small sizes (every rank, both element sizes, every vector width), with
+sentinel guard bands; at the full workload sizes bit-exact against the head
+slice of the global tensor and against the oracle on sampled token windows."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2609_03151_amd as basp
+from synth_inputs import WORKLOADS, random_shards
+from parity import device_shards, log, workload_inputs
+
+pytestmark = pytest.mark.gpu
+
+SENT16 = 0x7F7B  # a bf16 NaN pattern no input contains
+
+
+def _bits(t: torch.Tensor) -> np.ndarray:
+    t = t.detach().cpu().contiguous()
+    if t.dtype == torch.bfloat16:
+        return t.view(torch.int16).numpy()
+    return t.view(torch.int32).numpy()
+
+
+def _guarded(shape, dtype, pad=64, dev="cuda"):
+    """A tensor of `shape` inside a sentinel-filled buffer with `pad` guard
+    elements on each side; returns (view, whole buffer)."""
+    n = int(np.prod(shape))
+    itype = torch.int16 if dtype == torch.bfloat16 else torch.int32
+    sent = SENT16 if dtype == torch.bfloat16 else 0x7FBADBAD
+    buf = torch.full((pad + n + pad,), sent, dtype=itype, device=dev)
+    return buf[pad:pad + n].view(dtype).view(shape), buf, sent
+
+
+CASES = [  # b, S, n, d, G
+    (2, 512, 8, 64, 2),
+    (1, 256, 32, 128, 4),
+    (1, 96, 28, 128, 4),      # 7 heads per rank
+    (3, 40, 8, 5, 8),         # odd head dim: narrow accesses
+    (1, 64, 4, 128, 1),       # G = 1: a copy
+    (1, 24, 6, 6, 3),
+    (2, 130, 2, 64, 2),       # one head per rank, odd token count per shard
+]
+
+
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
+@pytest.mark.parametrize("b,S,n,d,G", CASES)
+def test_pack_unpack_small_bitexact(b, S, n, d, G, dtype):
+    host = random_shards(b, S, n, d, G, seed=S * 31 + n + d, dtype=dtype)
+    dev = [s.cuda() for s in host]
+    nl = n // G
+    for r in range(G):
+        out, buf, sent = _guarded((b, S, nl, d), dtype)
+        basp.pack(dev, r, out=out)
+        torch.cuda.synchronize()
+        ref = oracle.pack(host, r)
+        assert np.array_equal(_bits(out), ref.view(_bits(out).dtype)), f"pack rank {r}"
+        whole = buf.cpu().numpy()
+        assert np.all(whole[:64] == np.array(sent).astype(whole.dtype))
+        assert np.all(whole[-64:] == np.array(sent).astype(whole.dtype))
+        # unpack into sentinel-filled shards: only the rank's slice changes
+        tgt = []
+        bufs = []
+        for _ in range(G):
+            t, bb, _ = _guarded((b, S // G, n, d), dtype)
+            tgt.append(t)
+            bufs.append(bb)
+        basp.unpack(out, tgt, r)
+        torch.cuda.synchronize()
+        ref_t = [np.full((b, S // G, n, d), sent, dtype=_bits(out).dtype) for _ in range(G)]
+        oracle.unpack(ref, ref_t, r)
+        for j in range(G):
+            assert np.array_equal(_bits(tgt[j]), ref_t[j]), f"unpack rank {r} shard {j}"
+            whole = bufs[j].cpu().numpy()
+            assert np.all(whole[:64] == np.array(sent).astype(whole.dtype))
+            assert np.all(whole[-64:] == np.array(sent).astype(whole.dtype))
+
+
+def test_pack_misaligned_pointers_take_narrow_path():
+    """Shard pointers offset by one element still pack exactly."""
+    b, S, n, d, G = 1, 64, 8, 64, 2
+    host = random_shards(b, S, n, d, G, seed=5)
+    flat = [torch.empty(s.numel() + 1, dtype=torch.bfloat16, device="cuda") for s in host]
+    dev = []
+    for f, s in zip(flat, host):
+        f[1:].copy_(s.reshape(-1).cuda())
+        dev.append(f[1:].view(s.shape))
+    for r in range(G):
+        out = basp.pack(dev, r)
+        torch.cuda.synchronize()
+        assert np.array_equal(_bits(out), oracle.pack(host, r))
+
+
+def test_empty_is_a_noop():
+    host = random_shards(0, 8, 4, 8, 2, seed=1)
+    dev = [s.cuda() for s in host]
+    out = basp.pack(dev, 1)
+    basp.unpack(out, dev, 1)
+    torch.cuda.synchronize()
+    assert out.shape == (0, 8, 2, 8)
+
+
+FULL = ["llama3_8b_s32k", "qwen25_7b_s64k", "ulysses_g8_b2_s64k", "basp_g4_b1_s64k",
+        "llama3_70b_s128k"]
+
+
+@pytest.mark.parametrize("name", FULL)
+def test_pack_unpack_full_size(name):
+    """Full-size shards: every rank's pack equals the head slice of the
+    concatenated shards (bit for bit, compared on the GPU); sampled token
+    windows equal the oracle; unpack of the packed result restores the shards."""
+    w = WORKLOADS[name]
+    log(f"[pack full] {name}")
+    q, k, v, _ = workload_inputs(name)
+    for x, n in ((q, w.H), (k, w.H_kv)):
+        shards = device_shards(x, w)
+        glob = torch.cat(shards, dim=1)
+        nl = n // w.G
+        ranks = sorted({0, w.rank, w.G - 1})
+        for r in ranks:
+            out = basp.pack(shards, r)
+            torch.cuda.synchronize()
+            assert torch.equal(out.view(torch.int16),
+                               glob[:, :, r * nl:(r + 1) * nl].contiguous().view(torch.int16)), r
+        # sampled token windows of every shard against the oracle
+        r = w.rank
+        out = basp.pack(shards, r).cpu()
+        Sg = w.S // w.G
+        for t0 in (0, Sg // 2 + 3, Sg - 17):
+            win = [s[:, t0:t0 + 16].cpu().contiguous() for s in shards]
+            ref = oracle.pack(win, r)               # [b, 16*G, nl, d]
+            got = torch.cat([out[:, j * Sg + t0:j * Sg + t0 + 16] for j in range(w.G)], dim=1)
+            assert np.array_equal(_bits(got), ref)
+        # unpack restores the shards exactly (its slice rewritten, rest untouched)
+        before = [s.clone() for s in shards]
+        basp.unpack(basp.pack(shards, r), shards, r)
+        torch.cuda.synchronize()
+        assert all(torch.equal(a.view(torch.int16), b_.view(torch.int16))
+                   for a, b_ in zip(shards, before))
+        del shards, glob, out
+    torch.cuda.empty_cache()
