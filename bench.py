@@ -53,11 +53,13 @@ def cpu_baseline(w, target_s: float):
         oracle.attn_bwd(qq, kk, vv, dd, o, lse, w.scale)
         return time.perf_counter() - t0
 
-    cal = min(512, w.S)
+    # Work grows with S'^2: calibrate on a prefix large enough for the
+    # quadratic term to dominate, then size the sample to the target time.
+    cal = min(2048, w.S)
     t_cal = run(cal)
     Sp = int(cal * (target_s / max(t_cal, 1e-6)) ** 0.5)
     Sp = max(cal, min(w.S, (Sp // 64) * 64))
-    secs = run(Sp)
+    secs = run(Sp) if Sp != cal else t_cal
     flops = 3.5 * 2.0 * 1 * w.Hl * w.d * float(Sp) ** 2
     return {"value": flops / secs / 1e12, "unit": "TFLOP/s", "cores": oracle.threads(),
             "kind": "oracle",
