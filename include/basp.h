@@ -113,7 +113,8 @@ int basp_unpack(const void *src, void *const *dst_shards, int b, int S,
  * lse [b,H/G,S] fp32 out (kept for the backward).  bf16 MFMA products with
  * fp32 accumulation and an fp32 online softmax.
  * Alignment: q, k, v, o 16 bytes; lse 4 bytes.
- * Errors: NULL, SHAPE, UNSUPPORTED (d not 64 or 128), ALIGN, HIP. */
+ * Errors: NULL, SHAPE, UNSUPPORTED (d not 64 or 128, scale not finite and
+ * positive, or S*(H/G)*d*2 >= 2^31 bytes), ALIGN, HIP. */
 int basp_attn_fwd(const void *q, const void *k, const void *v, void *o,
                   float *lse, int b, int S, int H, int H_kv, int d, int G,
                   float scale, void *stream);

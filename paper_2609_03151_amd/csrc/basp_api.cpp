@@ -30,8 +30,10 @@ int check_attn(int b, int S, int H, int H_kv, int d, int G, float scale) {
   if (rc) return rc;
   if (d != 64 && d != 128) return BASP_ERR_UNSUPPORTED;
   if (!(scale > 0.f) || !isfinite(scale)) return BASP_ERR_UNSUPPORTED;
-  // Row indices inside the kernels are 32-bit: b*S must fit.
+  // Row indices inside the kernels are 32-bit: b*S must fit, and one head's
+  // span of a tensor (S rows of H/G heads) is addressed with 31-bit offsets.
   if ((long long)b * S >= (long long)INT_MAX) return BASP_ERR_UNSUPPORTED;
+  if ((long long)S * (H / G) * d * 2 >= (1LL << 31)) return BASP_ERR_UNSUPPORTED;
   return BASP_OK;
 }
 

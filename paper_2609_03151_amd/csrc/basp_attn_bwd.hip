@@ -18,9 +18,11 @@
 // On gfx950 both main kernels use v_mfma_f32_32x32x16_bf16 with fp32
 // accumulation.  Which operand order is used is chosen so that every
 // elementwise step (P, dS) happens in the accumulator layout and feeds the
-// next product without a round trip through LDS; the operands that must be
-// read along the sequence are kept in transposed LDS copies whose order
-// inside each 16-block matches the accumulator (mfma_pos16).
+// next product without a round trip through LDS.  Operands that must be read
+// along the sequence (Q^T, dO^T, K^T) come from the same row-major LDS tiles
+// through ds_read_b64_tr_b16, in the order the accumulator holds P and dS.
+// Tiles are filled with 16-byte buffer loads (rows past S read as zero),
+// double-buffered, and each 64-wide tile is processed in two 32-wide halves.
 #include <math.h>
 
 #include "basp_device.hpp"
@@ -70,16 +72,13 @@ constexpr int kQM = 64;   // query rows per step
 
 template <int D>
 struct DkdvCfg {
-  static constexpr int RS = D + 8;    // row-major tile stride (elements)
-  static constexpr int TS = kQM + 8;  // transposed tile stride
-  static constexpr int ROW_ELEMS = kQM * RS;
-  static constexpr int T_ELEMS = D * TS;
-  // Q, dO row-major; Q^T, dO^T transposed; then 2 x kQM floats (LSE2, D).
-  static constexpr int STAGE_BYTES = (2 * ROW_ELEMS + 2 * T_ELEMS) * 2 + 2 * kQM * 4;
+  static constexpr int TILE_BYTES = kQM * D * 2;
+  // Q tile, dO tile, then 2 x kQM floats (LSE in log2 units, D).
+  static constexpr int STAGE_BYTES = 2 * TILE_BYTES + 2 * kQM * 4;
   static constexpr int NS = D / 16;
   static constexpr int NE = D / 32;
-  static constexpr int UNITS = (kQM / 8) * (D / 2) / kThreads;  // 8 rows x 2 cols per unit
-  static_assert(UNITS >= 1, "tile too small");
+  static constexpr int CPR = D / 8;
+  static constexpr int CHUNKS = kQM * CPR / kThreads;
 };
 
 template <int D>
@@ -90,6 +89,7 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_dkdv_kernel(
     float *__restrict__ dk, float *__restrict__ dv, int S, int Hl, int Hkl,
     int n_rep, int kvheads_total, float c /* scale*log2e */, float scale) {
   using C = DkdvCfg<D>;
+  using T = LdsTile<D>;
   __shared__ __attribute__((aligned(16))) unsigned char smem[2 * C::STAGE_BYTES];
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -102,21 +102,16 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_dkdv_kernel(
   const int wk0 = k0 + 32 * w;
   const int key = wk0 + l32;
 
-  const size_t qstride = (size_t)Hl * D, kvstride = (size_t)Hkl * D;
-  const uint16_t *kb = k + ((size_t)beta * S * Hkl + kvh) * D;
-  const uint16_t *vb = v + ((size_t)beta * S * Hkl + kvh) * D;
+  const uint32_t q_row_bytes = (uint32_t)Hl * D * 2, kv_row_bytes = (uint32_t)Hkl * D * 2;
+  const rsrc_t rk = make_rsrc(k + ((size_t)beta * S * Hkl + kvh) * D, (uint32_t)S * kv_row_bytes);
+  const rsrc_t rv = make_rsrc(v + ((size_t)beta * S * Hkl + kvh) * D, (uint32_t)S * kv_row_bytes);
 
   // K and V of this lane's key as B operands (B[e][j] = K[j][e]).
   bf16x8 kf[C::NS], vf[C::NS];
-  {
-    const u32x4 zero = {0u, 0u, 0u, 0u};
-    const u32x4 *ks = reinterpret_cast<const u32x4 *>(kb + (size_t)key * kvstride);
-    const u32x4 *vs = reinterpret_cast<const u32x4 *>(vb + (size_t)key * kvstride);
 #pragma unroll
-    for (int s = 0; s < C::NS; ++s) {
-      kf[s] = as_bf16x8(key < S ? ks[2 * s + hh] : zero);
-      vf[s] = as_bf16x8(key < S ? vs[2 * s + hh] : zero);
-    }
+  for (int s = 0; s < C::NS; ++s) {
+    kf[s] = as_bf16x8(buf_load16(rk, (uint32_t)key * kv_row_bytes + (2 * s + hh) * 16));
+    vf[s] = as_bf16x8(buf_load16(rv, (uint32_t)key * kv_row_bytes + (2 * s + hh) * 16));
   }
 
   f32x16 dkacc[C::NE], dvacc[C::NE];
@@ -130,7 +125,31 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_dkdv_kernel(
   const int steps_per_head = qtn - qt0;
   const int nsteps = steps_per_head * n_rep;
 
-  uint32_t qreg[C::UNITS][8], doreg[C::UNITS][8];
+  uint32_t g_off[C::CHUNKS];
+  int s_off[C::CHUNKS];
+#pragma unroll
+  for (int r = 0; r < C::CHUNKS; ++r) {
+    const int cidx = tid + r * kThreads;
+    const int ir = cidx / C::CPR, cc = cidx % C::CPR;
+    g_off[r] = (uint32_t)ir * q_row_bytes + cc * 16;
+    s_off[r] = T::off(ir, cc);
+  }
+  // LDS offsets of the operand reads (fixed across steps).
+  // A of S and dP: row 32m + l32, chunk 2s + hh.  The swizzle depends on
+  // the row modulo 16 only, so row 32 + r sits 32 rows further on.
+  int a_off[C::NS];
+#pragma unroll
+  for (int s = 0; s < C::NS; ++s) a_off[s] = T::off(l32, 2 * s + hh);
+  // Transposed A operand: rows 16*s2 + 4hh (+8), columns 32n + 16*((lane/16)&1);
+  // row block s2 sits 16*s2 rows further on (same swizzle).
+  int t_off[C::NE][2];
+#pragma unroll
+  for (int n = 0; n < C::NE; ++n)
+#pragma unroll
+    for (int x = 0; x < 2; ++x)
+      t_off[n][x] = tr_piece_off<D>(4 * hh + 8 * x, 32 * n + 16 * ((lane >> 4) & 1), lane);
+
+  u32x4 qreg[C::CHUNKS], doreg[C::CHUNKS];
   float aux = 0.f;  // LSE2 (tid < 64) or D (64 <= tid < 128) of one row
 
   auto step_coords = [&](int st, int &h, int &i0) {
@@ -142,20 +161,14 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_dkdv_kernel(
   auto load_step = [&](int st) {
     int h, i0;
     step_coords(st, h, i0);
-    const uint16_t *qb = q + ((size_t)beta * S * Hl + h) * D;
-    const uint16_t *db = d_o + ((size_t)beta * S * Hl + h) * D;
+    const size_t hoff = ((size_t)beta * S * Hl + h) * D;
+    const rsrc_t rq = make_rsrc(q + hoff, (uint32_t)S * q_row_bytes);
+    const rsrc_t rd = make_rsrc(d_o + hoff, (uint32_t)S * q_row_bytes);
+    const uint32_t base = (uint32_t)i0 * q_row_bytes;
 #pragma unroll
-    for (int u = 0; u < C::UNITS; ++u) {
-      const int uidx = tid + u * kThreads;
-      const int ep = uidx % (D / 2), ig = uidx / (D / 2);
-      const int blk = ig >> 1, half = ig & 1;
-#pragma unroll
-      for (int r = 0; r < 8; ++r) {
-        const int i = i0 + blk * 16 + half * 4 + (r & 3) + (r >> 2) * 8;
-        const bool ok = i < S;
-        qreg[u][r] = ok ? reinterpret_cast<const uint32_t *>(qb + (size_t)i * qstride)[ep] : 0u;
-        doreg[u][r] = ok ? reinterpret_cast<const uint32_t *>(db + (size_t)i * qstride)[ep] : 0u;
-      }
+    for (int r = 0; r < C::CHUNKS; ++r) {
+      qreg[r] = buf_load16(rq, base + g_off[r]);
+      doreg[r] = buf_load16(rd, base + g_off[r]);
     }
     if (tid < 2 * kQM) {
       const int i = i0 + (tid & (kQM - 1));
@@ -168,38 +181,13 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_dkdv_kernel(
   };
 
   auto store_step = [&](int buf) {
-    unsigned char *base = smem + buf * C::STAGE_BYTES;
-    uint16_t *Qs = reinterpret_cast<uint16_t *>(base);
-    uint16_t *dOs = Qs + C::ROW_ELEMS;
-    uint16_t *Qt = dOs + C::ROW_ELEMS;
-    uint16_t *dOt = Qt + C::T_ELEMS;
-    float *aux_s = reinterpret_cast<float *>(dOt + C::T_ELEMS);
+    unsigned char *Qs = smem + buf * C::STAGE_BYTES;
+    unsigned char *dOs = Qs + C::TILE_BYTES;
+    float *aux_s = reinterpret_cast<float *>(dOs + C::TILE_BYTES);
 #pragma unroll
-    for (int u = 0; u < C::UNITS; ++u) {
-      const int uidx = tid + u * kThreads;
-      const int ep = uidx % (D / 2), ig = uidx / (D / 2);
-      const int blk = ig >> 1, half = ig & 1;
-      const int pos = blk * 16 + half * 8;
-#pragma unroll
-      for (int r = 0; r < 8; ++r) {
-        const int il = blk * 16 + half * 4 + (r & 3) + (r >> 2) * 8;
-        *reinterpret_cast<uint32_t *>(Qs + il * C::RS + 2 * ep) = qreg[u][r];
-        *reinterpret_cast<uint32_t *>(dOs + il * C::RS + 2 * ep) = doreg[u][r];
-      }
-      const uint32_t *x = qreg[u];
-      const uint32_t *y = doreg[u];
-      u32x4 qlo = {lo_halves(x[0], x[1]), lo_halves(x[2], x[3]), lo_halves(x[4], x[5]),
-                   lo_halves(x[6], x[7])};
-      u32x4 qhi = {hi_halves(x[0], x[1]), hi_halves(x[2], x[3]), hi_halves(x[4], x[5]),
-                   hi_halves(x[6], x[7])};
-      u32x4 dlo = {lo_halves(y[0], y[1]), lo_halves(y[2], y[3]), lo_halves(y[4], y[5]),
-                   lo_halves(y[6], y[7])};
-      u32x4 dhi = {hi_halves(y[0], y[1]), hi_halves(y[2], y[3]), hi_halves(y[4], y[5]),
-                   hi_halves(y[6], y[7])};
-      *reinterpret_cast<u32x4 *>(Qt + (2 * ep) * C::TS + pos) = qlo;
-      *reinterpret_cast<u32x4 *>(Qt + (2 * ep + 1) * C::TS + pos) = qhi;
-      *reinterpret_cast<u32x4 *>(dOt + (2 * ep) * C::TS + pos) = dlo;
-      *reinterpret_cast<u32x4 *>(dOt + (2 * ep + 1) * C::TS + pos) = dhi;
+    for (int r = 0; r < C::CHUNKS; ++r) {
+      *reinterpret_cast<u32x4 *>(Qs + s_off[r]) = qreg[r];
+      *reinterpret_cast<u32x4 *>(dOs + s_off[r]) = doreg[r];
     }
     if (tid < 2 * kQM) aux_s[tid] = aux;
   };
@@ -215,35 +203,30 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_dkdv_kernel(
     int h_unused, i0;
     step_coords(st, h_unused, i0);
     if (i0 + kQM - 1 >= wk0) {  // wave-uniform: some row of the step sees a key of this wave
-      const unsigned char *base = smem + (st & 1) * C::STAGE_BYTES;
-      const uint16_t *Qs = reinterpret_cast<const uint16_t *>(base);
-      const uint16_t *dOs = Qs + C::ROW_ELEMS;
-      const uint16_t *Qt = dOs + C::ROW_ELEMS;
-      const uint16_t *dOt = Qt + C::T_ELEMS;
-      const float *lse_s = reinterpret_cast<const float *>(dOt + C::T_ELEMS);
+      const unsigned char *Qs = smem + (st & 1) * C::STAGE_BYTES;
+      const unsigned char *dOs = Qs + C::TILE_BYTES;
+      const float *lse_s = reinterpret_cast<const float *>(dOs + C::TILE_BYTES);
       const float *D_s = lse_s + kQM;
 
-      // S = Q K^T and dP = dO V^T: M = query rows (2 x 32), N = the wave's keys.
-      f32x16 sacc[2], pacc[2];
+      // Two halves of 32 rows each (keeps the score state at 2 x 16 registers).
+      // S = Q K^T and dP = dO V^T: M = 32 query rows, N = the wave's keys;
+      // acc[r] holds row i0 + 32m + 8(r/4) + 4hh + r%4, key `key`.
 #pragma unroll
-      for (int m = 0; m < 2; ++m)
+      for (int m = 0; m < 2; ++m) {
+        if (i0 + 32 * m + 31 < wk0) continue;  // wave-uniform: half entirely above the keys
+        f32x16 sacc, pacc;
 #pragma unroll
-        for (int r = 0; r < 16; ++r) sacc[m][r] = pacc[m][r] = 0.f;
+        for (int r = 0; r < 16; ++r) sacc[r] = pacc[r] = 0.f;
 #pragma unroll
-      for (int s = 0; s < C::NS; ++s)
-#pragma unroll
-        for (int m = 0; m < 2; ++m) {
+        for (int s = 0; s < C::NS; ++s) {
           const bf16x8 aq =
-              *reinterpret_cast<const bf16x8 *>(Qs + (32 * m + l32) * C::RS + 16 * s + 8 * hh);
+              *reinterpret_cast<const bf16x8 *>(Qs + a_off[s] + m * 32 * T::ROW_BYTES);
           const bf16x8 ad =
-              *reinterpret_cast<const bf16x8 *>(dOs + (32 * m + l32) * C::RS + 16 * s + 8 * hh);
-          sacc[m] = mfma32x32x16(aq, kf[s], sacc[m]);
-          pacc[m] = mfma32x32x16(ad, vf[s], pacc[m]);
+              *reinterpret_cast<const bf16x8 *>(dOs + a_off[s] + m * 32 * T::ROW_BYTES);
+          sacc = mfma32x32x16(aq, kf[s], sacc);
+          pacc = mfma32x32x16(ad, vf[s], pacc);
         }
-      // acc[m][r] holds row i0 + 32m + 8(r/4) + 4hh + r%4, key `key`.
-      const bool diag = i0 < wk0 + 31;
-#pragma unroll
-      for (int m = 0; m < 2; ++m)
+        const bool diag = i0 + 32 * m < wk0 + 31;
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
           const int il = 32 * m + 8 * g + 4 * hh;
@@ -252,41 +235,42 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_dkdv_kernel(
 #pragma unroll
           for (int x = 0; x < 4; ++x) {
             const int r = 4 * g + x;
-            float p = fast_exp2(fmaf(sacc[m][r], c, -l4[x]));
+            float p = fast_exp2(fmaf(sacc[r], c, -l4[x]));
             if (diag && key > i0 + il + x) p = 0.f;
-            sacc[m][r] = p;
-            pacc[m][r] = p * (pacc[m][r] - d4[x]);
+            sacc[r] = p;
+            pacc[r] = p * (pacc[r] - d4[x]);
           }
         }
-      // P and dS as B operands along the query rows: step s covers rows
-      // 16s .. 16s+15 of the 64, slot t <-> accumulator register (s&1)*8 + t.
-      bf16x8 pb[kQM / 16], sb[kQM / 16];
+        // P and dS as B operands along the rows: block s2 covers rows
+        // 32m + 16*s2 .. +15, slot t <-> accumulator register 8*s2 + t.
+        bf16x8 pb[2], sb[2];
 #pragma unroll
-      for (int s2 = 0; s2 < kQM / 16; ++s2) {
-        const int m = s2 >> 1, b8 = (s2 & 1) * 8;
-        u32x4 tp = {pack_bf16x2(sacc[m][b8 + 0], sacc[m][b8 + 1]),
-                    pack_bf16x2(sacc[m][b8 + 2], sacc[m][b8 + 3]),
-                    pack_bf16x2(sacc[m][b8 + 4], sacc[m][b8 + 5]),
-                    pack_bf16x2(sacc[m][b8 + 6], sacc[m][b8 + 7])};
-        u32x4 ts = {pack_bf16x2(pacc[m][b8 + 0], pacc[m][b8 + 1]),
-                    pack_bf16x2(pacc[m][b8 + 2], pacc[m][b8 + 3]),
-                    pack_bf16x2(pacc[m][b8 + 4], pacc[m][b8 + 5]),
-                    pack_bf16x2(pacc[m][b8 + 6], pacc[m][b8 + 7])};
-        pb[s2] = as_bf16x8(tp);
-        sb[s2] = as_bf16x8(ts);
-      }
-      // dV^T += dO^T P,  dK^T += Q^T dS:  M = head dim, N = keys, K = rows.
-#pragma unroll
-      for (int n = 0; n < C::NE; ++n)
-#pragma unroll
-        for (int s2 = 0; s2 < kQM / 16; ++s2) {
-          const bf16x8 ad =
-              *reinterpret_cast<const bf16x8 *>(dOt + (32 * n + l32) * C::TS + 16 * s2 + 8 * hh);
-          const bf16x8 aq =
-              *reinterpret_cast<const bf16x8 *>(Qt + (32 * n + l32) * C::TS + 16 * s2 + 8 * hh);
-          dvacc[n] = mfma32x32x16(ad, pb[s2], dvacc[n]);
-          dkacc[n] = mfma32x32x16(aq, sb[s2], dkacc[n]);
+        for (int s2 = 0; s2 < 2; ++s2) {
+          const int b8 = 8 * s2;
+          u32x4 tp = {pack_bf16x2(sacc[b8 + 0], sacc[b8 + 1]), pack_bf16x2(sacc[b8 + 2], sacc[b8 + 3]),
+                      pack_bf16x2(sacc[b8 + 4], sacc[b8 + 5]), pack_bf16x2(sacc[b8 + 6], sacc[b8 + 7])};
+          u32x4 ts = {pack_bf16x2(pacc[b8 + 0], pacc[b8 + 1]), pack_bf16x2(pacc[b8 + 2], pacc[b8 + 3]),
+                      pack_bf16x2(pacc[b8 + 4], pacc[b8 + 5]), pack_bf16x2(pacc[b8 + 6], pacc[b8 + 7])};
+          pb[s2] = as_bf16x8(tp);
+          sb[s2] = as_bf16x8(ts);
         }
+        // dV^T += dO^T P,  dK^T += Q^T dS:  M = head dim, N = keys, K = rows.
+        // The transposed A operands come straight from the row-major tiles.
+#pragma unroll
+        for (int n = 0; n < C::NE; ++n)
+#pragma unroll
+          for (int s2 = 0; s2 < 2; ++s2) {
+            const int ro = (2 * m + s2) * 16 * T::ROW_BYTES;
+            const uint2 dlo = lds_read_tr4(dOs, t_off[n][0] + ro);
+            const uint2 dhi = lds_read_tr4(dOs, t_off[n][1] + ro);
+            const uint2 qlo = lds_read_tr4(Qs, t_off[n][0] + ro);
+            const uint2 qhi = lds_read_tr4(Qs, t_off[n][1] + ro);
+            const u32x4 ad = {dlo.x, dlo.y, dhi.x, dhi.y};
+            const u32x4 aq = {qlo.x, qlo.y, qhi.x, qhi.y};
+            dvacc[n] = mfma32x32x16(as_bf16x8(ad), pb[s2], dvacc[n]);
+            dkacc[n] = mfma32x32x16(as_bf16x8(aq), sb[s2], dkacc[n]);
+          }
+      }
     }
     if (st + 1 < nsteps) store_step((st + 1) & 1);
     __syncthreads();
@@ -316,27 +300,24 @@ constexpr int kDQN = 64;   // keys per tile
 
 template <int D>
 struct DqCfg {
-  static constexpr int RS = D + 8;     // K, V row-major stride
-  static constexpr int TS = kDQN + 8;  // K^T stride
-  static constexpr int ROW_ELEMS = kDQN * RS;
-  static constexpr int T_ELEMS = D * TS;
-  static constexpr int STAGE = 2 * ROW_ELEMS + T_ELEMS;
+  static constexpr int TILE_BYTES = kDQN * D * 2;
+  static constexpr int STAGE_BYTES = 2 * TILE_BYTES;  // K, V
   static constexpr int NS = D / 16;
   static constexpr int NE = D / 32;
-  static constexpr int CHUNKS = kDQN * D / 8 / kThreads;
-  static constexpr int UNITS = (kDQN / 8) * (D / 2) / kThreads;
-  static_assert(CHUNKS >= 1 && UNITS >= 1, "tile too small");
+  static constexpr int CPR = D / 8;
+  static constexpr int CHUNKS = kDQN * CPR / kThreads;
 };
 
 template <int D>
-__global__ __launch_bounds__(kThreads, 1) void bwd_dq_kernel(
+__global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(
     const uint16_t *__restrict__ q, const uint16_t *__restrict__ k,
     const uint16_t *__restrict__ v, const uint16_t *__restrict__ d_o,
     const float *__restrict__ lse, const float *__restrict__ Dbuf,
     float *__restrict__ dq, int S, int Hl, int Hkl, int n_rep, int heads_total,
     int qtiles, float c, float scale) {
   using C = DqCfg<D>;
-  __shared__ __attribute__((aligned(16))) uint16_t smem[2 * C::STAGE];
+  using T = LdsTile<D>;
+  __shared__ __attribute__((aligned(16))) unsigned char smem[2 * C::STAGE_BYTES];
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int l32 = lane & 31, hh = lane >> 5;
@@ -348,22 +329,18 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_dq_kernel(
   const int wrow0 = q0 + 32 * w;
   const int row = wrow0 + l32;
 
-  const size_t qstride = (size_t)Hl * D, kvstride = (size_t)Hkl * D;
-  const uint16_t *qb = q + ((size_t)beta * S * Hl + h) * D;
-  const uint16_t *db = d_o + ((size_t)beta * S * Hl + h) * D;
-  const uint16_t *kb = k + ((size_t)beta * S * Hkl + kvh) * D;
-  const uint16_t *vb = v + ((size_t)beta * S * Hkl + kvh) * D;
+  const uint32_t q_row_bytes = (uint32_t)Hl * D * 2, kv_row_bytes = (uint32_t)Hkl * D * 2;
+  const size_t hoff = ((size_t)beta * S * Hl + h) * D;
+  const rsrc_t rq = make_rsrc(q + hoff, (uint32_t)S * q_row_bytes);
+  const rsrc_t rd = make_rsrc(d_o + hoff, (uint32_t)S * q_row_bytes);
+  const rsrc_t rk = make_rsrc(k + ((size_t)beta * S * Hkl + kvh) * D, (uint32_t)S * kv_row_bytes);
+  const rsrc_t rv = make_rsrc(v + ((size_t)beta * S * Hkl + kvh) * D, (uint32_t)S * kv_row_bytes);
 
   bf16x8 qf[C::NS], df[C::NS];
-  {
-    const u32x4 zero = {0u, 0u, 0u, 0u};
-    const u32x4 *qs = reinterpret_cast<const u32x4 *>(qb + (size_t)row * qstride);
-    const u32x4 *ds = reinterpret_cast<const u32x4 *>(db + (size_t)row * qstride);
 #pragma unroll
-    for (int s = 0; s < C::NS; ++s) {
-      qf[s] = as_bf16x8(row < S ? qs[2 * s + hh] : zero);
-      df[s] = as_bf16x8(row < S ? ds[2 * s + hh] : zero);
-    }
+  for (int s = 0; s < C::NS; ++s) {
+    qf[s] = as_bf16x8(buf_load16(rq, (uint32_t)row * q_row_bytes + (2 * s + hh) * 16));
+    df[s] = as_bf16x8(buf_load16(rd, (uint32_t)row * q_row_bytes + (2 * s + hh) * 16));
   }
   const size_t lidx = ((size_t)beta * Hl + h) * S + row;
   const float lse2 = row < S ? lse[lidx] * kLog2e : INFINITY;
@@ -372,56 +349,43 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_dq_kernel(
   const int kv_end = min(S, q0 + kDQM);
   const int nt = (kv_end + kDQN - 1) / kDQN;
 
-  u32x4 kreg[C::CHUNKS], vreg[C::CHUNKS];
-  uint32_t ktreg[C::UNITS][8];
+  uint32_t g_off[C::CHUNKS];
+  int s_off[C::CHUNKS];
+#pragma unroll
+  for (int r = 0; r < C::CHUNKS; ++r) {
+    const int cidx = tid + r * kThreads;
+    const int jr = cidx / C::CPR, cc = cidx % C::CPR;
+    g_off[r] = (uint32_t)jr * kv_row_bytes + cc * 16;
+    s_off[r] = T::off(jr, cc);
+  }
+  int a_off[C::NS];  // row l32 (+32 for m = 1), chunk 2s + hh
+#pragma unroll
+  for (int s = 0; s < C::NS; ++s) a_off[s] = T::off(l32, 2 * s + hh);
+  // Transposed A operand: rows 16*s2 + 4hh (+8), columns 32n + 16*((lane/16)&1);
+  // row block s2 sits 16*s2 rows further on (same swizzle).
+  int t_off[C::NE][2];
+#pragma unroll
+  for (int n = 0; n < C::NE; ++n)
+#pragma unroll
+    for (int x = 0; x < 2; ++x)
+      t_off[n][x] = tr_piece_off<D>(4 * hh + 8 * x, 32 * n + 16 * ((lane >> 4) & 1), lane);
 
+  u32x4 kreg[C::CHUNKS], vreg[C::CHUNKS];
   auto load_tile = [&](int t) {
-    const int j0 = t * kDQN;
-    const u32x4 zero = {0u, 0u, 0u, 0u};
+    const uint32_t base = (uint32_t)(t * kDQN) * kv_row_bytes;
 #pragma unroll
     for (int r = 0; r < C::CHUNKS; ++r) {
-      const int cidx = tid + r * kThreads;
-      const int jr = cidx / (D / 8), c8 = cidx % (D / 8);
-      const int j = j0 + jr;
-      kreg[r] = j < S ? reinterpret_cast<const u32x4 *>(kb + (size_t)j * kvstride)[c8] : zero;
-      vreg[r] = j < S ? reinterpret_cast<const u32x4 *>(vb + (size_t)j * kvstride)[c8] : zero;
-    }
-#pragma unroll
-    for (int u = 0; u < C::UNITS; ++u) {
-      const int uidx = tid + u * kThreads;
-      const int ep = uidx % (D / 2), jg = uidx / (D / 2);
-      const int blk = jg >> 1, half = jg & 1;
-#pragma unroll
-      for (int r = 0; r < 8; ++r) {
-        const int j = j0 + blk * 16 + half * 4 + (r & 3) + (r >> 2) * 8;
-        ktreg[u][r] = j < S ? reinterpret_cast<const uint32_t *>(kb + (size_t)j * kvstride)[ep] : 0u;
-      }
+      kreg[r] = buf_load16(rk, base + g_off[r]);
+      vreg[r] = buf_load16(rv, base + g_off[r]);
     }
   };
-
   auto store_tile = [&](int buf) {
-    uint16_t *Ks = smem + buf * C::STAGE;
-    uint16_t *Vs = Ks + C::ROW_ELEMS;
-    uint16_t *Kt = Vs + C::ROW_ELEMS;
+    unsigned char *Ks = smem + buf * C::STAGE_BYTES;
+    unsigned char *Vs = Ks + C::TILE_BYTES;
 #pragma unroll
     for (int r = 0; r < C::CHUNKS; ++r) {
-      const int cidx = tid + r * kThreads;
-      const int jr = cidx / (D / 8), c8 = cidx % (D / 8);
-      *reinterpret_cast<u32x4 *>(Ks + jr * C::RS + c8 * 8) = kreg[r];
-      *reinterpret_cast<u32x4 *>(Vs + jr * C::RS + c8 * 8) = vreg[r];
-    }
-#pragma unroll
-    for (int u = 0; u < C::UNITS; ++u) {
-      const int uidx = tid + u * kThreads;
-      const int ep = uidx % (D / 2), jg = uidx / (D / 2);
-      const int pos = (jg >> 1) * 16 + (jg & 1) * 8;
-      const uint32_t *x = ktreg[u];
-      u32x4 lo = {lo_halves(x[0], x[1]), lo_halves(x[2], x[3]), lo_halves(x[4], x[5]),
-                  lo_halves(x[6], x[7])};
-      u32x4 hi = {hi_halves(x[0], x[1]), hi_halves(x[2], x[3]), hi_halves(x[4], x[5]),
-                  hi_halves(x[6], x[7])};
-      *reinterpret_cast<u32x4 *>(Kt + (2 * ep) * C::TS + pos) = lo;
-      *reinterpret_cast<u32x4 *>(Kt + (2 * ep + 1) * C::TS + pos) = hi;
+      *reinterpret_cast<u32x4 *>(Ks + s_off[r]) = kreg[r];
+      *reinterpret_cast<u32x4 *>(Vs + s_off[r]) = vreg[r];
     }
   };
 
@@ -439,55 +403,57 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_dq_kernel(
     if (t + 1 < nt) load_tile(t + 1);
     const int j0 = t * kDQN;
     if (j0 <= wrow0 + 31) {
-      const uint16_t *Ks = smem + (t & 1) * C::STAGE;
-      const uint16_t *Vs = Ks + C::ROW_ELEMS;
-      const uint16_t *Kt = Vs + C::ROW_ELEMS;
-      // S^T = K Q^T and dP^T = V dO^T: M = keys (2 x 32), N = this wave's rows.
-      f32x16 sacc[2], pacc[2];
+      const unsigned char *Ks = smem + (t & 1) * C::STAGE_BYTES;
+      const unsigned char *Vs = Ks + C::TILE_BYTES;
+      // Two halves of 32 keys each (keeps the score state at 2 x 16 registers).
+      // S^T = K Q^T and dP^T = V dO^T: M = 32 keys, N = this wave's rows;
+      // acc[r] holds key j0 + 32m + 8(r/4) + 4hh + r%4, query row `row`.
 #pragma unroll
-      for (int m = 0; m < 2; ++m)
+      for (int m = 0; m < 2; ++m) {
+        if (j0 + 32 * m > wrow0 + 31) continue;  // wave-uniform: half entirely masked
+        f32x16 sacc, pacc;
 #pragma unroll
-        for (int r = 0; r < 16; ++r) sacc[m][r] = pacc[m][r] = 0.f;
+        for (int r = 0; r < 16; ++r) sacc[r] = pacc[r] = 0.f;
 #pragma unroll
-      for (int s = 0; s < C::NS; ++s)
-#pragma unroll
-        for (int m = 0; m < 2; ++m) {
+        for (int s = 0; s < C::NS; ++s) {
           const bf16x8 ak =
-              *reinterpret_cast<const bf16x8 *>(Ks + (32 * m + l32) * C::RS + 16 * s + 8 * hh);
+              *reinterpret_cast<const bf16x8 *>(Ks + a_off[s] + m * 32 * T::ROW_BYTES);
           const bf16x8 av =
-              *reinterpret_cast<const bf16x8 *>(Vs + (32 * m + l32) * C::RS + 16 * s + 8 * hh);
-          sacc[m] = mfma32x32x16(ak, qf[s], sacc[m]);
-          pacc[m] = mfma32x32x16(av, df[s], pacc[m]);
+              *reinterpret_cast<const bf16x8 *>(Vs + a_off[s] + m * 32 * T::ROW_BYTES);
+          sacc = mfma32x32x16(ak, qf[s], sacc);
+          pacc = mfma32x32x16(av, df[s], pacc);
         }
-      const bool diag = j0 + kDQN - 1 > wrow0;
-#pragma unroll
-      for (int m = 0; m < 2; ++m)
+        const bool diag = j0 + 32 * m + 31 > wrow0;
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const int j = j0 + 32 * m + 8 * (r >> 2) + 4 * hh + (r & 3);
-          float p = fast_exp2(fmaf(sacc[m][r], c, -lse2));
-          if (diag && j > row) p = 0.f;
-          pacc[m][r] = p * (pacc[m][r] - Drow);
+          float p = fast_exp2(fmaf(sacc[r], c, -lse2));
+          if (diag) {
+            const int j = j0 + 32 * m + 8 * (r >> 2) + 4 * hh + (r & 3);
+            if (j > row) p = 0.f;
+          }
+          pacc[r] = p * (pacc[r] - Drow);
         }
-      bf16x8 sb[kDQN / 16];
+        bf16x8 sb[2];
 #pragma unroll
-      for (int s2 = 0; s2 < kDQN / 16; ++s2) {
-        const int m = s2 >> 1, b8 = (s2 & 1) * 8;
-        u32x4 ts = {pack_bf16x2(pacc[m][b8 + 0], pacc[m][b8 + 1]),
-                    pack_bf16x2(pacc[m][b8 + 2], pacc[m][b8 + 3]),
-                    pack_bf16x2(pacc[m][b8 + 4], pacc[m][b8 + 5]),
-                    pack_bf16x2(pacc[m][b8 + 6], pacc[m][b8 + 7])};
-        sb[s2] = as_bf16x8(ts);
+        for (int s2 = 0; s2 < 2; ++s2) {
+          const int b8 = 8 * s2;
+          u32x4 ts = {pack_bf16x2(pacc[b8 + 0], pacc[b8 + 1]), pack_bf16x2(pacc[b8 + 2], pacc[b8 + 3]),
+                      pack_bf16x2(pacc[b8 + 4], pacc[b8 + 5]), pack_bf16x2(pacc[b8 + 6], pacc[b8 + 7])};
+          sb[s2] = as_bf16x8(ts);
+        }
+        // dQ^T += K^T dS^T: M = head dim, N = rows, K = keys; K^T straight
+        // from the row-major K tile.
+#pragma unroll
+        for (int n = 0; n < C::NE; ++n)
+#pragma unroll
+          for (int s2 = 0; s2 < 2; ++s2) {
+            const int ro = (2 * m + s2) * 16 * T::ROW_BYTES;
+            const uint2 lo = lds_read_tr4(Ks, t_off[n][0] + ro);
+            const uint2 hi = lds_read_tr4(Ks, t_off[n][1] + ro);
+            const u32x4 a4 = {lo.x, lo.y, hi.x, hi.y};
+            qacc[n] = mfma32x32x16(as_bf16x8(a4), sb[s2], qacc[n]);
+          }
       }
-      // dQ^T += K^T dS^T: M = head dim, N = rows, K = keys.
-#pragma unroll
-      for (int n = 0; n < C::NE; ++n)
-#pragma unroll
-        for (int s2 = 0; s2 < kDQN / 16; ++s2) {
-          const bf16x8 a =
-              *reinterpret_cast<const bf16x8 *>(Kt + (32 * n + l32) * C::TS + 16 * s2 + 8 * hh);
-          qacc[n] = mfma32x32x16(a, sb[s2], qacc[n]);
-        }
     }
     if (t + 1 < nt) store_tile((t + 1) & 1);
     __syncthreads();

@@ -5,8 +5,8 @@
 // for each local query head h with local kv head h / n_rep:
 //   O_i = sum_j softmax_j(scale * q_i . k_j) v_j,   LSE_i = log sum_j exp(.)
 // The S x S score matrix is never stored: keys are visited in tiles with a
-// running row maximum and row sum (online softmax), the standard
-// re-association that changes only rounding.
+// running row maximum and row sum (online softmax), a re-association that
+// changes only rounding.
 //
 // gfx950 mapping
 //   * workgroup = 4 waves = 128 query rows of one (sequence, head); wave w
@@ -17,15 +17,18 @@
 //     lane one query row and 16 keys, so the softmax statistics are lane-local
 //     up to one exchange with the partner lane l^32.
 //   * O^T = V^T P^T: P goes from the score accumulator straight into the B
-//     operand (bf16, round to nearest even); V^T (A operand) is read from a
-//     transposed LDS copy whose key order inside each 16-block matches the
-//     accumulator's row order (see mfma_pos16).
-//   * K/V tiles of 64 keys are double-buffered in LDS and prefetched into
-//     registers one tile ahead; tiles past a wave's last row are skipped and
-//     only tiles crossing the diagonal are masked.
-//   * the grid is one-dimensional, heaviest query tiles first (they visit the
-//     most key tiles), heads fastest so that the heads sharing a kv head run
-//     side by side.
+//     operand (bf16, round to nearest even).  V^T (A operand) is read from the
+//     row-major V tile with ds_read_b64_tr_b16, two 4-key reads per operand,
+//     in exactly the key order the accumulator holds P in.
+//   * K/V tiles of 64 keys are loaded with 16-byte buffer loads (rows past S
+//     read as zero), stored row-major with an XOR swizzle (conflict-free for
+//     both read patterns), double-buffered and prefetched one tile ahead.
+//   * the running maximum used as the exponent reference only moves when a
+//     row's maximum grows by more than 8 (in log2 units): P <= 2^8 stays exact
+//     in bf16's relative precision and O is rescaled only on those tiles.
+//   * tiles past a wave's last row are skipped; only tiles crossing the
+//     diagonal are masked.  The grid is one-dimensional, heaviest query tiles
+//     first, heads fastest, so heads sharing a kv head run side by side.
 #include <math.h>
 
 #include "basp_device.hpp"
@@ -35,21 +38,18 @@ namespace basp {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kBM = 128;  // query rows per workgroup
-constexpr int kBN = 64;   // keys per tile
+constexpr int kBM = 128;          // query rows per workgroup
+constexpr int kBN = 64;           // keys per tile
+constexpr float kRescaleSlack = 8.f;  // log2 headroom before the reference max moves
 
 template <int D>
 struct FwdCfg {
-  static constexpr int KS = D + 8;     // K tile row stride (elements), 16B-padded
-  static constexpr int VS = kBN + 8;   // V^T row stride
-  static constexpr int K_ELEMS = kBN * KS;
-  static constexpr int V_ELEMS = D * VS;
-  static constexpr int STAGE = K_ELEMS + V_ELEMS;
-  static constexpr int NS = D / 16;    // 16-deep steps over the head dim
-  static constexpr int NE = D / 32;    // 32-wide head-dim subtiles of O
-  static constexpr int K_CHUNKS = kBN * D / 8 / kThreads;        // 16B chunks / thread
-  static constexpr int V_UNITS = (kBN / 8) * (D / 2) / kThreads;  // 8 rows x 2 cols units
-  static_assert(K_CHUNKS >= 1 && V_UNITS >= 1, "tile too small for the block");
+  static constexpr int TILE_BYTES = kBN * D * 2;
+  static constexpr int STAGE_BYTES = 2 * TILE_BYTES;  // K, V
+  static constexpr int NS = D / 16;                   // 16-deep steps over the head dim
+  static constexpr int NE = D / 32;                   // 32-wide head-dim subtiles of O
+  static constexpr int CPR = D / 8;                   // 16-byte chunks per row
+  static constexpr int CHUNKS = kBN * CPR / kThreads; // chunks per thread per tile
 };
 
 template <int D>
@@ -59,7 +59,8 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(
     float *__restrict__ lse, int S, int Hl, int Hkl, int n_rep, int heads_total,
     int qtiles, float c /* scale * log2(e) */) {
   using C = FwdCfg<D>;
-  __shared__ __attribute__((aligned(16))) uint16_t smem[2 * C::STAGE];
+  using T = LdsTile<D>;
+  __shared__ __attribute__((aligned(16))) unsigned char smem[2 * C::STAGE_BYTES];
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int l32 = lane & 31, hh = lane >> 5;
@@ -72,79 +73,71 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(
   const int wrow0 = q0 + 32 * w;
   const int row = wrow0 + l32;
 
-  const size_t qstride = (size_t)Hl * D, kvstride = (size_t)Hkl * D;
-  const uint16_t *qb = q + ((size_t)beta * S * Hl + h) * D;
-  const uint16_t *kb = k + ((size_t)beta * S * Hkl + kvh) * D;
-  const uint16_t *vb = v + ((size_t)beta * S * Hkl + kvh) * D;
+  const uint32_t q_row_bytes = (uint32_t)Hl * D * 2, kv_row_bytes = (uint32_t)Hkl * D * 2;
+  const rsrc_t rq = make_rsrc(q + ((size_t)beta * S * Hl + h) * D, (uint32_t)S * q_row_bytes);
+  const rsrc_t rk = make_rsrc(k + ((size_t)beta * S * Hkl + kvh) * D, (uint32_t)S * kv_row_bytes);
+  const rsrc_t rv = make_rsrc(v + ((size_t)beta * S * Hkl + kvh) * D, (uint32_t)S * kv_row_bytes);
 
   // Q fragments (B operand of S^T = K Q^T): row `row`, e = 16s + 8hh .. +7.
   bf16x8 qf[C::NS];
-  {
-    const u32x4 zero = {0u, 0u, 0u, 0u};
-    const u32x4 *src = reinterpret_cast<const u32x4 *>(qb + (size_t)row * qstride);
 #pragma unroll
-    for (int s = 0; s < C::NS; ++s) qf[s] = as_bf16x8(row < S ? src[2 * s + hh] : zero);
-  }
+  for (int s = 0; s < C::NS; ++s)
+    qf[s] = as_bf16x8(buf_load16(rq, (uint32_t)row * q_row_bytes + (2 * s + hh) * 16));
 
   const int kv_end = min(S, q0 + kBM);
   const int nt = (kv_end + kBN - 1) / kBN;
 
-  u32x4 kreg[C::K_CHUNKS];
-  uint32_t vreg[C::V_UNITS][8];
-
+  // Per-thread chunk coordinates of the tile loads (fixed across tiles).
+  uint32_t g_off[C::CHUNKS];
+  int s_off[C::CHUNKS];
+#pragma unroll
+  for (int r = 0; r < C::CHUNKS; ++r) {
+    const int cidx = tid + r * kThreads;
+    const int jr = cidx / C::CPR, cc = cidx % C::CPR;
+    g_off[r] = (uint32_t)jr * kv_row_bytes + cc * 16;
+    s_off[r] = T::off(jr, cc);
+  }
+  u32x4 kreg[C::CHUNKS], vreg[C::CHUNKS];
   auto load_tile = [&](int t) {
-    const int j0 = t * kBN;
+    const uint32_t base = (uint32_t)(t * kBN) * kv_row_bytes;
 #pragma unroll
-    for (int r = 0; r < C::K_CHUNKS; ++r) {
-      const int cidx = tid + r * kThreads;
-      const int jr = cidx / (D / 8), c8 = cidx % (D / 8);
-      const int j = j0 + jr;
-      const u32x4 zero = {0u, 0u, 0u, 0u};
-      kreg[r] = j < S ? reinterpret_cast<const u32x4 *>(kb + (size_t)j * kvstride)[c8] : zero;
+    for (int r = 0; r < C::CHUNKS; ++r) {
+      kreg[r] = buf_load16(rk, base + g_off[r]);
+      vreg[r] = buf_load16(rv, base + g_off[r]);
     }
+  };
+  auto store_tile = [&](int buf) {
+    unsigned char *Ks = smem + buf * C::STAGE_BYTES;
+    unsigned char *Vs = Ks + C::TILE_BYTES;
 #pragma unroll
-    for (int u = 0; u < C::V_UNITS; ++u) {
-      const int uidx = tid + u * kThreads;
-      const int ep = uidx % (D / 2), jg = uidx / (D / 2);
-      const int blk = jg >> 1, half = jg & 1;
-#pragma unroll
-      for (int r = 0; r < 8; ++r) {
-        const int j = j0 + blk * 16 + half * 4 + (r & 3) + (r >> 2) * 8;
-        vreg[u][r] = j < S ? reinterpret_cast<const uint32_t *>(vb + (size_t)j * kvstride)[ep] : 0u;
-      }
+    for (int r = 0; r < C::CHUNKS; ++r) {
+      *reinterpret_cast<u32x4 *>(Ks + s_off[r]) = kreg[r];
+      *reinterpret_cast<u32x4 *>(Vs + s_off[r]) = vreg[r];
     }
   };
 
-  auto store_tile = [&](int buf) {
-    uint16_t *Ks = smem + buf * C::STAGE;
-    uint16_t *Vt = Ks + C::K_ELEMS;
+  // LDS offsets of this lane's operand reads (fixed across tiles).
+  // A of S^T: K row 32m + l32, chunk 2s + hh.  The swizzle depends on the
+  // row modulo 16 only, so row 32 + r sits 32 rows further on.
+  int k_off[C::NS];
 #pragma unroll
-    for (int r = 0; r < C::K_CHUNKS; ++r) {
-      const int cidx = tid + r * kThreads;
-      const int jr = cidx / (D / 8), c8 = cidx % (D / 8);
-      *reinterpret_cast<u32x4 *>(Ks + jr * C::KS + c8 * 8) = kreg[r];
-    }
+  for (int s = 0; s < C::NS; ++s) k_off[s] = T::off(l32, 2 * s + hh);
+  // A of O^T: V^T rows e = 32n + l32, keys 16*s2 + 4hh + {0..3} and + 8.
+  // Transposed A operand: rows 16*s2 + 4hh (+8), columns 32n + 16*((lane/16)&1);
+  // row block s2 sits 16*s2 rows further on (same swizzle).
+  int v_off[C::NE][2];
 #pragma unroll
-    for (int u = 0; u < C::V_UNITS; ++u) {
-      const int uidx = tid + u * kThreads;
-      const int ep = uidx % (D / 2), jg = uidx / (D / 2);
-      const int pos = (jg >> 1) * 16 + (jg & 1) * 8;
-      const uint32_t *x = vreg[u];
-      u32x4 lo = {lo_halves(x[0], x[1]), lo_halves(x[2], x[3]), lo_halves(x[4], x[5]),
-                  lo_halves(x[6], x[7])};
-      u32x4 hi = {hi_halves(x[0], x[1]), hi_halves(x[2], x[3]), hi_halves(x[4], x[5]),
-                  hi_halves(x[6], x[7])};
-      *reinterpret_cast<u32x4 *>(Vt + (2 * ep) * C::VS + pos) = lo;
-      *reinterpret_cast<u32x4 *>(Vt + (2 * ep + 1) * C::VS + pos) = hi;
-    }
-  };
+  for (int n = 0; n < C::NE; ++n)
+#pragma unroll
+    for (int x = 0; x < 2; ++x)
+      v_off[n][x] = tr_piece_off<D>(4 * hh + 8 * x, 32 * n + 16 * ((lane >> 4) & 1), lane);
 
   f32x16 oacc[C::NE];
 #pragma unroll
   for (int n = 0; n < C::NE; ++n)
 #pragma unroll
     for (int r = 0; r < 16; ++r) oacc[n][r] = 0.f;
-  float m_run = -INFINITY, l_run = 0.f;
+  float m_ref = -INFINITY, l_run = 0.f;
 
   load_tile(0);
   store_tile(0);
@@ -154,8 +147,8 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(
     if (t + 1 < nt) load_tile(t + 1);
     const int j0 = t * kBN;
     if (j0 <= wrow0 + 31) {  // wave-uniform: tile has keys visible to this wave
-      const uint16_t *Ks = smem + (t & 1) * C::STAGE;
-      const uint16_t *Vt = Ks + C::K_ELEMS;
+      const unsigned char *Ks = smem + (t & 1) * C::STAGE_BYTES;
+      const unsigned char *Vs = Ks + C::TILE_BYTES;
 
       f32x16 sacc[2];
 #pragma unroll
@@ -166,8 +159,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(
       for (int s = 0; s < C::NS; ++s)
 #pragma unroll
         for (int m = 0; m < 2; ++m) {
-          const bf16x8 a =
-              *reinterpret_cast<const bf16x8 *>(Ks + (32 * m + l32) * C::KS + 16 * s + 8 * hh);
+          const bf16x8 a = *reinterpret_cast<const bf16x8 *>(Ks + k_off[s] + m * 32 * T::ROW_BYTES);
           sacc[m] = mfma32x32x16(a, qf[s], sacc[m]);
         }
 
@@ -186,24 +178,30 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(
       for (int m = 0; m < 2; ++m)
 #pragma unroll
         for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[m][r]);
-      mx = fmaxf(mx, swap_halves(mx));
-      const float m_new = fmaxf(m_run, mx * c);
-      const float alpha = fast_exp2(m_run - m_new);
-      m_run = m_new;
+      mx = fmaxf(mx, swap_halves(mx)) * c;
+      // Move the reference only when the row maximum outgrew it by the slack
+      // (always on a row's first tile, where m_ref is -inf).
+      const bool grow = mx > m_ref + kRescaleSlack;
+      if (__builtin_amdgcn_ballot_w64(grow)) {  // wave-uniform
+        const float m_new = grow ? mx : m_ref;
+        const float alpha = fast_exp2(m_ref - m_new);
+        m_ref = m_new;
+        l_run *= alpha;
+#pragma unroll
+        for (int n = 0; n < C::NE; ++n)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) oacc[n][r] *= alpha;
+      }
       float psum = 0.f;
 #pragma unroll
       for (int m = 0; m < 2; ++m)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const float p = fast_exp2(fmaf(sacc[m][r], c, -m_new));
+          const float p = fast_exp2(fmaf(sacc[m][r], c, -m_ref));
           sacc[m][r] = p;
           psum += p;
         }
-      l_run = l_run * alpha + psum;
-#pragma unroll
-      for (int n = 0; n < C::NE; ++n)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) oacc[n][r] *= alpha;
+      l_run += psum;
 
       bf16x8 pf[kBN / 16];
 #pragma unroll
@@ -219,9 +217,10 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(
       for (int n = 0; n < C::NE; ++n)
 #pragma unroll
         for (int s2 = 0; s2 < kBN / 16; ++s2) {
-          const bf16x8 a =
-              *reinterpret_cast<const bf16x8 *>(Vt + (32 * n + l32) * C::VS + 16 * s2 + 8 * hh);
-          oacc[n] = mfma32x32x16(a, pf[s2], oacc[n]);
+          const uint2 lo = lds_read_tr4(Vs, v_off[n][0] + s2 * 16 * T::ROW_BYTES);
+          const uint2 hi = lds_read_tr4(Vs, v_off[n][1] + s2 * 16 * T::ROW_BYTES);
+          const u32x4 a4 = {lo.x, lo.y, hi.x, hi.y};
+          oacc[n] = mfma32x32x16(as_bf16x8(a4), pf[s2], oacc[n]);
         }
     }
     if (t + 1 < nt) store_tile((t + 1) & 1);
@@ -242,7 +241,7 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(
         *reinterpret_cast<u32x2 *>(ob + 32 * n + 8 * g + 4 * hh) = val;
       }
     if (hh == 0)
-      lse[((size_t)beta * Hl + h) * S + row] = (m_run + fast_log2(l_tot)) * 0.69314718055994531f;
+      lse[((size_t)beta * Hl + h) * S + row] = (m_ref + fast_log2(l_tot)) * 0.69314718055994531f;
   }
 }
 

@@ -63,12 +63,76 @@ __device__ __forceinline__ uint32_t hi_halves(uint32_t a, uint32_t b) {
   return __builtin_amdgcn_perm(b, a, 0x07060302u);
 }
 
-// Position of key/row index j inside a 16-wide block when stored in the
-// MFMA-operand order: swaps bits 2 and 3, so that lane half h reads the
-// indices {4h..4h+3, 8+4h..8+4h+3} (what a 32x32 accumulator holds) as one
-// contiguous 8-element run at [8h, 8h+8).
-__device__ __forceinline__ int mfma_pos16(int j) {
-  return (j & ~12) | ((j & 4) << 1) | ((j & 8) >> 1);
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+
+// ---------------------------------------------------------------- buffers
+// Raw buffer resource over [base, base + num_bytes): loads whose offset falls
+// outside return zeros without touching memory, which handles ragged tails
+// without branches.  Offsets are 32-bit (num_bytes < 2^31, checked on the
+// host).  Word 3 selects the 32-bit data format expected by raw loads.
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+
+__device__ __forceinline__ rsrc_t make_rsrc(const void *base, uint32_t num_bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)num_bytes,
+                                           0x00020000);
+}
+__device__ __forceinline__ u32x4 buf_load16(rsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+}
+__device__ __forceinline__ float buf_load_f32(rsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
+}
+
+// ------------------------------------------------------------- LDS tiles
+// A [rows][D] bf16 tile stored row-major without padding, its 16-byte chunks
+// permuted by an XOR of the row.  The permutation makes both access patterns
+// of the attention kernels free of bank conflicts:
+//   * 16 lanes reading one chunk of 16 consecutive rows (MFMA operand rows);
+//   * ds_read_b64_tr_b16 over 4 consecutive rows starting at a multiple of 4,
+//     each lane group touching two adjacent chunks (even first) of every row.
+template <int D>
+struct LdsTile;
+
+template <>
+struct LdsTile<128> {
+  static constexpr int ROW_BYTES = 256;
+  __device__ static __forceinline__ int swz(int r) { return ((r & 7) << 1) | ((r >> 3) & 1); }
+  __device__ static __forceinline__ int off(int r, int chunk) {
+    return r * ROW_BYTES + ((chunk ^ swz(r)) << 4);
+  }
+};
+
+template <>
+struct LdsTile<64> {
+  static constexpr int ROW_BYTES = 128;
+  __device__ static __forceinline__ int swz(int r) {
+    return (((r >> 1) & 3) << 1) | ((r >> 3) & 1);
+  }
+  __device__ static __forceinline__ int off(int r, int chunk) {
+    return r * ROW_BYTES + ((chunk ^ swz(r)) << 4);
+  }
+};
+
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+
+// ds_read_b64_tr_b16: each lane passes the address of 4 consecutive bf16; in
+// every group of 16 lanes, lane i receives element i%4 of the 8-byte pieces
+// addressed by lanes i/4, i/4+4, i/4+8, i/4+12.  With lane c of the group
+// addressing row r0 + c/4, columns e0 + 4(c%4) .. +3, lane i therefore gets
+// the column e0 + i over rows r0 .. r0+3: a transposed read.
+__device__ __forceinline__ uint2 lds_read_tr4(const unsigned char *tile, int byte_off) {
+  i16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (lds_i16x4 *)(tile + byte_off));
+  return __builtin_bit_cast(uint2, v);
+}
+
+// Byte offset, inside an LdsTile<D>, of the 8-byte piece lane `lane` passes to
+// lds_read_tr4 when reading columns [e0, e0+16) over rows [r0, r0+4).
+template <int D>
+__device__ __forceinline__ int tr_piece_off(int r0, int e0, int lane) {
+  const int c = lane & 15;
+  const int col = e0 + 4 * (c & 3);
+  return LdsTile<D>::off(r0 + (c >> 2), col >> 3) + ((col & 4) << 1);
 }
 
 }  // namespace basp
