@@ -67,22 +67,38 @@ __global__ __launch_bounds__(kThreads) void bwd_pre_kernel(
 }
 
 // ---------------------------------------------------------------- bwd_dkdv
-constexpr int kKN = 128;  // keys per workgroup (32 per wave)
-constexpr int kQM = 64;   // query rows per step
+// Key-stationary.  A workgroup of 8 waves owns 128 keys of one kv head and
+// sweeps every 64-row query tile at or after them, for all query heads of the
+// GQA group.  The waves form 4 pairs, one per 32-key group; inside a pair the
+// work of a 32-row half-tile is split without recomputation:
+//   role 0 holds K, forms S = Q K^T and P = exp2(S c - LSE2) (masked);
+//   role 1 holds V, forms dP = dO V^T;
+//   the two swap P and dP (fp32) through LDS, both form dS = P (dP - D),
+//   and each accumulates dV^T += dO^T P and dK^T += Q^T dS for its half of
+//   the head dimension.
+// This keeps each wave near 190 registers, so two waves share a SIMD.
+constexpr int kKN = 128;            // keys per workgroup (32 per pair)
+constexpr int kQM = 64;             // query rows per step (two 32-row halves)
+constexpr int kDkdvThreads = 512;   // 8 waves
+constexpr int kXBytes = 64 * 16 * 4;  // one wave's 16 accumulator floats per lane
 
 template <int D>
 struct DkdvCfg {
   static constexpr int TILE_BYTES = kQM * D * 2;
   // Q tile, dO tile, then 2 x kQM floats (LSE in log2 units, D).
   static constexpr int STAGE_BYTES = 2 * TILE_BYTES + 2 * kQM * 4;
+  // exchange: [parity][pair][P | dP]
+  static constexpr int XCHG_BYTES = 2 * 4 * 2 * kXBytes;
   static constexpr int NS = D / 16;
   static constexpr int NE = D / 32;
+  static constexpr int NEH = NE / 2;  // head-dim subtiles per role
   static constexpr int CPR = D / 8;
-  static constexpr int CHUNKS = kQM * CPR / kThreads;
+  static constexpr int CHUNKS = kQM * CPR / kDkdvThreads;
+  static_assert(CHUNKS >= 1 && NEH >= 1, "tile too small");
 };
 
 template <int D>
-__global__ __launch_bounds__(kThreads, 1) void bwd_dkdv_kernel(
+__global__ __launch_bounds__(kDkdvThreads, 1) void bwd_dkdv_kernel(
     const uint16_t *__restrict__ q, const uint16_t *__restrict__ k,
     const uint16_t *__restrict__ v, const uint16_t *__restrict__ d_o,
     const float *__restrict__ lse, const float *__restrict__ Dbuf,
@@ -90,33 +106,32 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_dkdv_kernel(
     int n_rep, int kvheads_total, float c /* scale*log2e */, float scale) {
   using C = DkdvCfg<D>;
   using T = LdsTile<D>;
-  __shared__ __attribute__((aligned(16))) unsigned char smem[2 * C::STAGE_BYTES];
+  __shared__ __attribute__((aligned(16))) unsigned char smem[2 * C::STAGE_BYTES + C::XCHG_BYTES];
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  // Waves w and w + 4 form the pair of key group w % 4 (roles 0 and 1).
+  const int role = w >> 2, kg = w & 3;
   const int l32 = lane & 31, hh = lane >> 5;
   const int L = blockIdx.x;
   const int kt = L / kvheads_total;  // heaviest (earliest keys) first
   const int hb = L % kvheads_total;
   const int beta = hb / Hkl, kvh = hb % Hkl;
   const int k0 = kt * kKN;
-  const int wk0 = k0 + 32 * w;
+  const int wk0 = k0 + 32 * kg;
   const int key = wk0 + l32;
 
   const uint32_t q_row_bytes = (uint32_t)Hl * D * 2, kv_row_bytes = (uint32_t)Hkl * D * 2;
-  const rsrc_t rk = make_rsrc(k + ((size_t)beta * S * Hkl + kvh) * D, (uint32_t)S * kv_row_bytes);
-  const rsrc_t rv = make_rsrc(v + ((size_t)beta * S * Hkl + kvh) * D, (uint32_t)S * kv_row_bytes);
-
-  // K and V of this lane's key as B operands (B[e][j] = K[j][e]).
-  bf16x8 kf[C::NS], vf[C::NS];
+  // B operand of this wave's product: K (role 0) or V (role 1) of its key.
+  const rsrc_t rb = make_rsrc((role ? v : k) + ((size_t)beta * S * Hkl + kvh) * D,
+                              (uint32_t)S * kv_row_bytes);
+  bf16x8 bf[C::NS];
 #pragma unroll
-  for (int s = 0; s < C::NS; ++s) {
-    kf[s] = as_bf16x8(buf_load16(rk, (uint32_t)key * kv_row_bytes + (2 * s + hh) * 16));
-    vf[s] = as_bf16x8(buf_load16(rv, (uint32_t)key * kv_row_bytes + (2 * s + hh) * 16));
-  }
+  for (int s = 0; s < C::NS; ++s)
+    bf[s] = as_bf16x8(buf_load16(rb, (uint32_t)key * kv_row_bytes + (2 * s + hh) * 16));
 
-  f32x16 dkacc[C::NE], dvacc[C::NE];
+  f32x16 dvacc[C::NEH], dkacc[C::NEH];  // head-dim subtiles role*NEH + nn
 #pragma unroll
-  for (int n = 0; n < C::NE; ++n)
+  for (int n = 0; n < C::NEH; ++n)
 #pragma unroll
     for (int r = 0; r < 16; ++r) dkacc[n][r] = dvacc[n][r] = 0.f;
 
@@ -129,25 +144,28 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_dkdv_kernel(
   int s_off[C::CHUNKS];
 #pragma unroll
   for (int r = 0; r < C::CHUNKS; ++r) {
-    const int cidx = tid + r * kThreads;
+    const int cidx = tid + r * kDkdvThreads;
     const int ir = cidx / C::CPR, cc = cidx % C::CPR;
     g_off[r] = (uint32_t)ir * q_row_bytes + cc * 16;
     s_off[r] = T::off(ir, cc);
   }
-  // LDS offsets of the operand reads (fixed across steps).
-  // A of S and dP: row 32m + l32, chunk 2s + hh.  The swizzle depends on
-  // the row modulo 16 only, so row 32 + r sits 32 rows further on.
+  // A of S or dP: row l32 (+32 for the second half), chunk 2s + hh.
   int a_off[C::NS];
 #pragma unroll
   for (int s = 0; s < C::NS; ++s) a_off[s] = T::off(l32, 2 * s + hh);
-  // Transposed A operand: rows 16*s2 + 4hh (+8), columns 32n + 16*((lane/16)&1);
-  // row block s2 sits 16*s2 rows further on (same swizzle).
-  int t_off[C::NE][2];
+  // Transposed A of dV^T, dK^T: rows 16*s2 + 4hh (+8), columns 32n + 16*((lane/16)&1).
+  int t_off[C::NEH][2];
 #pragma unroll
-  for (int n = 0; n < C::NE; ++n)
+  for (int n = 0; n < C::NEH; ++n)
 #pragma unroll
     for (int x = 0; x < 2; ++x)
-      t_off[n][x] = tr_piece_off<D>(4 * hh + 8 * x, 32 * n + 16 * ((lane >> 4) & 1), lane);
+      t_off[n][x] = tr_piece_off<D>(4 * hh + 8 * x, 32 * (role * C::NEH + n) +
+                                    16 * ((lane >> 4) & 1), lane);
+
+  unsigned char *xchg = smem + 2 * C::STAGE_BYTES;
+  auto xslot = [&](int parity, int pair, int kind) {
+    return xchg + ((parity * 4 + pair) * 2 + kind) * kXBytes;
+  };
 
   u32x4 qreg[C::CHUNKS], doreg[C::CHUNKS];
   float aux = 0.f;  // LSE2 (tid < 64) or D (64 <= tid < 128) of one row
@@ -202,62 +220,82 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_dkdv_kernel(
     if (st + 1 < nsteps) load_step(st + 1);
     int h_unused, i0;
     step_coords(st, h_unused, i0);
-    if (i0 + kQM - 1 >= wk0) {  // wave-uniform: some row of the step sees a key of this wave
-      const unsigned char *Qs = smem + (st & 1) * C::STAGE_BYTES;
-      const unsigned char *dOs = Qs + C::TILE_BYTES;
-      const float *lse_s = reinterpret_cast<const float *>(dOs + C::TILE_BYTES);
-      const float *D_s = lse_s + kQM;
+    const unsigned char *Qs = smem + (st & 1) * C::STAGE_BYTES;
+    const unsigned char *dOs = Qs + C::TILE_BYTES;
+    const float *lse_s = reinterpret_cast<const float *>(dOs + C::TILE_BYTES);
+    const float *D_s = lse_s + kQM;
+    const unsigned char *As = role ? dOs : Qs;
 
-      // Two halves of 32 rows each (keeps the score state at 2 x 16 registers).
-      // S = Q K^T and dP = dO V^T: M = 32 query rows, N = the wave's keys;
-      // acc[r] holds row i0 + 32m + 8(r/4) + 4hh + r%4, key `key`.
 #pragma unroll
-      for (int m = 0; m < 2; ++m) {
-        if (i0 + 32 * m + 31 < wk0) continue;  // wave-uniform: half entirely above the keys
-        f32x16 sacc, pacc;
+    for (int m = 0; m < 2; ++m) {
+      // Pair-uniform: does any row of this half see a key of the pair?
+      const bool active = i0 + 32 * m + 31 >= wk0;
+      // acc[r] holds row i0 + 32m + 8(r/4) + 4hh + r%4, key `key`:
+      // P (role 0) or dP (role 1).
+      f32x16 acc;
+      if (active) {
 #pragma unroll
-        for (int r = 0; r < 16; ++r) sacc[r] = pacc[r] = 0.f;
+        for (int r = 0; r < 16; ++r) acc[r] = 0.f;
 #pragma unroll
         for (int s = 0; s < C::NS; ++s) {
-          const bf16x8 aq =
-              *reinterpret_cast<const bf16x8 *>(Qs + a_off[s] + m * 32 * T::ROW_BYTES);
-          const bf16x8 ad =
-              *reinterpret_cast<const bf16x8 *>(dOs + a_off[s] + m * 32 * T::ROW_BYTES);
-          sacc = mfma32x32x16(aq, kf[s], sacc);
-          pacc = mfma32x32x16(ad, vf[s], pacc);
+          const bf16x8 a =
+              *reinterpret_cast<const bf16x8 *>(As + a_off[s] + m * 32 * T::ROW_BYTES);
+          acc = mfma32x32x16(a, bf[s], acc);
         }
-        const bool diag = i0 + 32 * m < wk0 + 31;
+        if (role == 0) {
+          const bool diag = i0 + 32 * m < wk0 + 31;
+#pragma unroll
+          for (int g = 0; g < 4; ++g) {
+            const f32x4 l4 =
+                *reinterpret_cast<const f32x4 *>(lse_s + 32 * m + 8 * g + 4 * hh);
+#pragma unroll
+            for (int x = 0; x < 4; ++x) {
+              const int r = 4 * g + x;
+              float p = fast_exp2(fmaf(acc[r], c, -l4[x]));
+              if (diag && key > i0 + 32 * m + 8 * g + 4 * hh + x) p = 0.f;
+              acc[r] = p;
+            }
+          }
+        }
+        f32x4 *mine = reinterpret_cast<f32x4 *>(xslot(m, kg, role));
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+          mine[g * 64 + lane] = (f32x4){acc[4 * g], acc[4 * g + 1], acc[4 * g + 2], acc[4 * g + 3]};
+      }
+      __syncthreads();  // every wave, active or not: the exchange of this half
+      if (active) {
+        const f32x4 *other = reinterpret_cast<const f32x4 *>(xslot(m, kg, role ^ 1));
+        f32x16 P, dS;
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
-          const int il = 32 * m + 8 * g + 4 * hh;
-          const f32x4 l4 = *reinterpret_cast<const f32x4 *>(lse_s + il);
-          const f32x4 d4 = *reinterpret_cast<const f32x4 *>(D_s + il);
+          const f32x4 o4 = other[g * 64 + lane];
+          const f32x4 d4 = *reinterpret_cast<const f32x4 *>(D_s + 32 * m + 8 * g + 4 * hh);
 #pragma unroll
           for (int x = 0; x < 4; ++x) {
             const int r = 4 * g + x;
-            float p = fast_exp2(fmaf(sacc[r], c, -l4[x]));
-            if (diag && key > i0 + il + x) p = 0.f;
-            sacc[r] = p;
-            pacc[r] = p * (pacc[r] - d4[x]);
+            const float p = role ? o4[x] : acc[r];
+            const float dp = role ? acc[r] : o4[x];
+            P[r] = p;
+            dS[r] = p * (dp - d4[x]);
           }
         }
         // P and dS as B operands along the rows: block s2 covers rows
-        // 32m + 16*s2 .. +15, slot t <-> accumulator register 8*s2 + t.
+        // 32m + 16*s2 .. +15, slot t <-> register 8*s2 + t.
         bf16x8 pb[2], sb[2];
 #pragma unroll
         for (int s2 = 0; s2 < 2; ++s2) {
           const int b8 = 8 * s2;
-          u32x4 tp = {pack_bf16x2(sacc[b8 + 0], sacc[b8 + 1]), pack_bf16x2(sacc[b8 + 2], sacc[b8 + 3]),
-                      pack_bf16x2(sacc[b8 + 4], sacc[b8 + 5]), pack_bf16x2(sacc[b8 + 6], sacc[b8 + 7])};
-          u32x4 ts = {pack_bf16x2(pacc[b8 + 0], pacc[b8 + 1]), pack_bf16x2(pacc[b8 + 2], pacc[b8 + 3]),
-                      pack_bf16x2(pacc[b8 + 4], pacc[b8 + 5]), pack_bf16x2(pacc[b8 + 6], pacc[b8 + 7])};
+          u32x4 tp = {pack_bf16x2(P[b8 + 0], P[b8 + 1]), pack_bf16x2(P[b8 + 2], P[b8 + 3]),
+                      pack_bf16x2(P[b8 + 4], P[b8 + 5]), pack_bf16x2(P[b8 + 6], P[b8 + 7])};
+          u32x4 ts = {pack_bf16x2(dS[b8 + 0], dS[b8 + 1]), pack_bf16x2(dS[b8 + 2], dS[b8 + 3]),
+                      pack_bf16x2(dS[b8 + 4], dS[b8 + 5]), pack_bf16x2(dS[b8 + 6], dS[b8 + 7])};
           pb[s2] = as_bf16x8(tp);
           sb[s2] = as_bf16x8(ts);
         }
-        // dV^T += dO^T P,  dK^T += Q^T dS:  M = head dim, N = keys, K = rows.
-        // The transposed A operands come straight from the row-major tiles.
+        // dV^T += dO^T P,  dK^T += Q^T dS on this role's head-dim half; the
+        // transposed A operands come straight from the row-major tiles.
 #pragma unroll
-        for (int n = 0; n < C::NE; ++n)
+        for (int n = 0; n < C::NEH; ++n)
 #pragma unroll
           for (int s2 = 0; s2 < 2; ++s2) {
             const int ro = (2 * m + s2) * 16 * T::ROW_BYTES;
@@ -276,20 +314,21 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_dkdv_kernel(
     __syncthreads();
   }
 
-  // dkacc[n][r] = dK^T[e = 32n + 8(r/4) + 4hh + r%4][key]
+  // dkacc[n][r] = dK^T[e = 32(role*NEH + n) + 8(r/4) + 4hh + r%4][key]
   if (key < S) {
     float *dkr = dk + ((size_t)(beta * S + key) * Hkl + kvh) * D;
     float *dvr = dv + ((size_t)(beta * S + key) * Hkl + kvh) * D;
 #pragma unroll
-    for (int n = 0; n < C::NE; ++n)
+    for (int n = 0; n < C::NEH; ++n)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
+        const int e = 32 * (role * C::NEH + n) + 8 * g + 4 * hh;
         f32x4 a = {dkacc[n][4 * g] * scale, dkacc[n][4 * g + 1] * scale,
                    dkacc[n][4 * g + 2] * scale, dkacc[n][4 * g + 3] * scale};
         f32x4 b = {dvacc[n][4 * g], dvacc[n][4 * g + 1], dvacc[n][4 * g + 2],
                    dvacc[n][4 * g + 3]};
-        *reinterpret_cast<f32x4 *>(dkr + 32 * n + 8 * g + 4 * hh) = a;
-        *reinterpret_cast<f32x4 *>(dvr + 32 * n + 8 * g + 4 * hh) = b;
+        *reinterpret_cast<f32x4 *>(dkr + e) = a;
+        *reinterpret_cast<f32x4 *>(dvr + e) = b;
       }
   }
 }
@@ -493,7 +532,7 @@ hipError_t launch_bwd_d(const void *q, const void *k, const void *v, const void 
   const int ktiles = (s.S + kKN - 1) / kKN;
   const int kvheads_total = s.b * s.Hkl;
   hipLaunchKernelGGL(bwd_dkdv_kernel<D>, dim3((unsigned)(ktiles * kvheads_total)),
-                     dim3(kThreads), 0, stream, qp, kp, vp, dop, lse, Dbuf, dk, dv, s.S,
+                     dim3(kDkdvThreads), 0, stream, qp, kp, vp, dop, lse, Dbuf, dk, dv, s.S,
                      s.Hl, s.Hkl, n_rep, kvheads_total, c, s.scale);
 
   const int qtiles = (s.S + kDQM - 1) / kDQM;
