@@ -8,11 +8,12 @@
 //   dV_j  = sum_{h in group} sum_{i>=j} P_ij dO_i
 //   dK_j  = scale sum_{h in group} sum_{i>=j} dS_ij q_i
 //   dQ_i  = scale sum_{j<=i} dS_ij k_j
-// Three kernels, all deterministic (no atomics):
+// Four kernels, all deterministic (no atomics):
 //   bwd_pre   D for every (sequence, head, row)
-//   bwd_dkdv  key-stationary: a workgroup owns 128 keys of one kv head and
-//             sweeps every query row at or after them, for all query heads
-//             of the GQA group, accumulating dK and dV in registers
+//   bwd_kv    key-stationary, twice (dV, then dK): a workgroup owns 128
+//             keys of one kv head and sweeps every query row at or after
+//             them, for all query heads of the GQA group, accumulating in
+//             registers
 //   bwd_dq    query-stationary: like the forward, a workgroup owns 128 rows
 //             of one query head and sweeps the keys up to the diagonal
 // On gfx950 both main kernels use v_mfma_f32_32x32x16_bf16 with fp32
@@ -33,6 +34,26 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr float kLog2e = 1.4426950408889634f;
+
+// Row chunking of the key-stationary kernels: 1 chunk up to 2048 rows, 2 up
+// to 8192, else 4 (multiples of 64 rows), enough workgroups to balance the
+// causal triangle over the GPU.  Workspace: D, then (if chunked) the dV and dK
+// partial sums [chunk][b][S][H_kv/G][d].
+struct BwdChunks {
+  int n, rows;
+  size_t part_offset_floats;
+};
+
+BwdChunks bwd_chunks(const AttnShape &s) {
+  BwdChunks ck;
+  ck.n = s.S <= 2048 ? 1 : (s.S <= 8192 ? 2 : 4);
+  ck.rows = ((s.S + ck.n - 1) / ck.n + 63) / 64 * 64;
+  ck.n = (s.S + ck.rows - 1) / ck.rows;
+  if (ck.n < 1) ck.n = 1;
+  const size_t d_floats = (size_t)s.b * s.Hl * s.S;
+  ck.part_offset_floats = (d_floats + 63) & ~(size_t)63;  // 256-byte aligned
+  return ck;
+}
 
 // ---------------------------------------------------------------- bwd_pre
 // One group of D/8 lanes per (beta, row, head); 16-byte loads of O and dO.
@@ -66,114 +87,116 @@ __global__ __launch_bounds__(kThreads) void bwd_pre_kernel(
   }
 }
 
-// ---------------------------------------------------------------- bwd_dkdv
-// Key-stationary.  A workgroup of 8 waves owns 128 keys of one kv head and
-// sweeps every 64-row query tile at or after them, for all query heads of the
-// GQA group.  The waves form 4 pairs, one per 32-key group; inside a pair the
-// work of a 32-row half-tile is split without recomputation:
-//   role 0 holds K, forms S = Q K^T and P = exp2(S c - LSE2) (masked);
-//   role 1 holds V, forms dP = dO V^T;
-//   the two swap P and dP (fp32) through LDS, both form dS = P (dP - D),
-//   and each accumulates dV^T += dO^T P and dK^T += Q^T dS for its half of
-//   the head dimension.
-// This keeps each wave near 190 registers, so two waves share a SIMD.
-constexpr int kKN = 128;            // keys per workgroup (32 per pair)
-constexpr int kQM = 64;             // query rows per step (two 32-row halves)
-constexpr int kDkdvThreads = 512;   // 8 waves
-constexpr int kXBytes = 64 * 16 * 4;  // one wave's 16 accumulator floats per lane
+// ------------------------------------------------------ bwd_dv / bwd_dk
+// Key-stationary.  A workgroup of 4 waves owns 128 keys of one kv head (32
+// per wave) and sweeps every 64-row query tile at or after them, for all
+// query heads of the GQA group.  Two instances of one kernel:
+//   kDV: S = Q K^T, P = exp2(S c - LSE2),   dV^T += dO^T P
+//   kDK: S, dP = dO V^T, dS = P (dP - D),   dK^T += Q^T dS
+// Keeping dV and dK in separate launches recomputes S once more, but leaves
+// every wave independent (no exchange between waves, one barrier per step)
+// and small enough for two waves per SIMD.
+constexpr int kKN = 128;  // keys per workgroup (32 per wave)
+constexpr int kQM = 64;   // query rows per step (two 32-row halves)
+enum KvGrad { kDV = 0, kDK = 1 };
 
 template <int D>
-struct DkdvCfg {
+struct KvCfg {
   static constexpr int TILE_BYTES = kQM * D * 2;
   // Q tile, dO tile, then 2 x kQM floats (LSE in log2 units, D).
   static constexpr int STAGE_BYTES = 2 * TILE_BYTES + 2 * kQM * 4;
-  // exchange: [parity][pair][P | dP]
-  static constexpr int XCHG_BYTES = 2 * 4 * 2 * kXBytes;
   static constexpr int NS = D / 16;
   static constexpr int NE = D / 32;
-  static constexpr int NEH = NE / 2;  // head-dim subtiles per role
   static constexpr int CPR = D / 8;
-  static constexpr int CHUNKS = kQM * CPR / kDkdvThreads;
-  static_assert(CHUNKS >= 1 && NEH >= 1, "tile too small");
+  static constexpr int CHUNKS = kQM * CPR / kThreads;
 };
 
-template <int D>
-__global__ __launch_bounds__(kDkdvThreads, 1) void bwd_dkdv_kernel(
+template <int D, int G>
+__global__ __launch_bounds__(kThreads, 2) void bwd_kv_kernel(
     const uint16_t *__restrict__ q, const uint16_t *__restrict__ k,
     const uint16_t *__restrict__ v, const uint16_t *__restrict__ d_o,
     const float *__restrict__ lse, const float *__restrict__ Dbuf,
-    float *__restrict__ dk, float *__restrict__ dv, int S, int Hl, int Hkl,
-    int n_rep, int kvheads_total, float c /* scale*log2e */, float scale) {
-  using C = DkdvCfg<D>;
+    float *__restrict__ out, int S, int Hl, int Hkl, int n_rep, int kvheads_total,
+    int ktiles, int chunk_rows, float c /* scale*log2e */, float out_scale) {
+  using C = KvCfg<D>;
   using T = LdsTile<D>;
-  __shared__ __attribute__((aligned(16))) unsigned char smem[2 * C::STAGE_BYTES + C::XCHG_BYTES];
+  __shared__ __attribute__((aligned(16))) unsigned char smem[2 * C::STAGE_BYTES];
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  // Waves w and w + 4 form the pair of key group w % 4 (roles 0 and 1).
-  const int role = w >> 2, kg = w & 3;
   const int l32 = lane & 31, hh = lane >> 5;
+  // Work item: (row chunk ch, key tile kt, sequence x kv head hb).  The rows a
+  // key tile needs, [k0, S), are cut at multiples of chunk_rows; each chunk
+  // writes its own partial sum (slice ch of `out`), so long key tiles are
+  // spread over several workgroups.  Earlier key tiles come first within a
+  // chunk (they have more rows).
   const int L = blockIdx.x;
-  const int kt = L / kvheads_total;  // heaviest (earliest keys) first
   const int hb = L % kvheads_total;
+  const int kt = (L / kvheads_total) % ktiles;
+  const int ch = L / (kvheads_total * ktiles);
   const int beta = hb / Hkl, kvh = hb % Hkl;
   const int k0 = kt * kKN;
-  const int wk0 = k0 + 32 * kg;
+  const int r_lo = max(k0, ch * chunk_rows), r_hi = min(S, (ch + 1) * chunk_rows);
+  if (r_lo >= r_hi) return;  // workgroup-uniform: this chunk lies before the keys
+  const int wk0 = k0 + 32 * w;
   const int key = wk0 + l32;
 
   const uint32_t q_row_bytes = (uint32_t)Hl * D * 2, kv_row_bytes = (uint32_t)Hkl * D * 2;
-  // B operand of this wave's product: K (role 0) or V (role 1) of its key.
-  const rsrc_t rb = make_rsrc((role ? v : k) + ((size_t)beta * S * Hkl + kvh) * D,
-                              (uint32_t)S * kv_row_bytes);
-  bf16x8 bf[C::NS];
+  const size_t kvoff = ((size_t)beta * S * Hkl + kvh) * D;
+  out += (size_t)ch * ((size_t)kvheads_total * S * D);
+  // K (and V for dK) of this lane's key as B operands (B[e][j] = K[j][e]).
+  bf16x8 kf[C::NS], vf[G == kDK ? C::NS : 1];
+  {
+    const rsrc_t rk = make_rsrc(k + kvoff, (uint32_t)S * kv_row_bytes);
 #pragma unroll
-  for (int s = 0; s < C::NS; ++s)
-    bf[s] = as_bf16x8(buf_load16(rb, (uint32_t)key * kv_row_bytes + (2 * s + hh) * 16));
+    for (int s = 0; s < C::NS; ++s)
+      kf[s] = as_bf16x8(buf_load16(rk, (uint32_t)key * kv_row_bytes + (2 * s + hh) * 16));
+    if constexpr (G == kDK) {
+      const rsrc_t rv = make_rsrc(v + kvoff, (uint32_t)S * kv_row_bytes);
+#pragma unroll
+      for (int s = 0; s < C::NS; ++s)
+        vf[s] = as_bf16x8(buf_load16(rv, (uint32_t)key * kv_row_bytes + (2 * s + hh) * 16));
+    }
+  }
 
-  f32x16 dvacc[C::NEH], dkacc[C::NEH];  // head-dim subtiles role*NEH + nn
+  f32x16 acc[C::NE];
 #pragma unroll
-  for (int n = 0; n < C::NEH; ++n)
+  for (int n = 0; n < C::NE; ++n)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) dkacc[n][r] = dvacc[n][r] = 0.f;
+    for (int r = 0; r < 16; ++r) acc[n][r] = 0.f;
 
-  const int qt0 = k0 / kQM;
-  const int qtn = (S + kQM - 1) / kQM;
-  const int steps_per_head = qtn - qt0;
+  const int steps_per_head = (r_hi - r_lo + kQM - 1) / kQM;
   const int nsteps = steps_per_head * n_rep;
 
   uint32_t g_off[C::CHUNKS];
   int s_off[C::CHUNKS];
 #pragma unroll
   for (int r = 0; r < C::CHUNKS; ++r) {
-    const int cidx = tid + r * kDkdvThreads;
+    const int cidx = tid + r * kThreads;
     const int ir = cidx / C::CPR, cc = cidx % C::CPR;
     g_off[r] = (uint32_t)ir * q_row_bytes + cc * 16;
     s_off[r] = T::off(ir, cc);
   }
-  // A of S or dP: row l32 (+32 for the second half), chunk 2s + hh.
+  // A of S and dP: row l32 (+32 for the second half), chunk 2s + hh.
   int a_off[C::NS];
 #pragma unroll
   for (int s = 0; s < C::NS; ++s) a_off[s] = T::off(l32, 2 * s + hh);
-  // Transposed A of dV^T, dK^T: rows 16*s2 + 4hh (+8), columns 32n + 16*((lane/16)&1).
-  int t_off[C::NEH][2];
+  // Transposed A of dV^T / dK^T: rows 16*s2 + 4hh (+8), columns 32n + 16*((lane/16)&1).
+  int t_off[C::NE][2];
 #pragma unroll
-  for (int n = 0; n < C::NEH; ++n)
+  for (int n = 0; n < C::NE; ++n)
 #pragma unroll
     for (int x = 0; x < 2; ++x)
-      t_off[n][x] = tr_piece_off<D>(4 * hh + 8 * x, 32 * (role * C::NEH + n) +
-                                    16 * ((lane >> 4) & 1), lane);
-
-  unsigned char *xchg = smem + 2 * C::STAGE_BYTES;
-  auto xslot = [&](int parity, int pair, int kind) {
-    return xchg + ((parity * 4 + pair) * 2 + kind) * kXBytes;
-  };
+      t_off[n][x] = tr_piece_off<D>(4 * hh + 8 * x, 32 * n + 16 * ((lane >> 4) & 1), lane);
 
   u32x4 qreg[C::CHUNKS], doreg[C::CHUNKS];
   float aux = 0.f;  // LSE2 (tid < 64) or D (64 <= tid < 128) of one row
 
+  // Rows past r_hi (in the last step of a chunk that ends before S) are
+  // read as data but carry LSE = +inf, so their P is exactly zero.
   auto step_coords = [&](int st, int &h, int &i0) {
     const int hr = st / steps_per_head;
     h = kvh * n_rep + hr;
-    i0 = (qt0 + (st - hr * steps_per_head)) * kQM;
+    i0 = r_lo + (st - hr * steps_per_head) * kQM;
   };
 
   auto load_step = [&](int st) {
@@ -192,9 +215,9 @@ __global__ __launch_bounds__(kDkdvThreads, 1) void bwd_dkdv_kernel(
       const int i = i0 + (tid & (kQM - 1));
       const size_t idx = ((size_t)beta * Hl + h) * S + i;
       if (tid < kQM)
-        aux = i < S ? lse[idx] * kLog2e : INFINITY;
+        aux = i < r_hi ? lse[idx] * kLog2e : INFINITY;
       else
-        aux = i < S ? Dbuf[idx] : 0.f;
+        aux = i < r_hi ? Dbuf[idx] : 0.f;
     }
   };
 
@@ -210,10 +233,8 @@ __global__ __launch_bounds__(kDkdvThreads, 1) void bwd_dkdv_kernel(
     if (tid < 2 * kQM) aux_s[tid] = aux;
   };
 
-  if (nsteps > 0) {
-    load_step(0);
-    store_step(0);
-  }
+  load_step(0);
+  store_step(0);
   __syncthreads();
 
   for (int st = 0; st < nsteps; ++st) {
@@ -224,113 +245,119 @@ __global__ __launch_bounds__(kDkdvThreads, 1) void bwd_dkdv_kernel(
     const unsigned char *dOs = Qs + C::TILE_BYTES;
     const float *lse_s = reinterpret_cast<const float *>(dOs + C::TILE_BYTES);
     const float *D_s = lse_s + kQM;
-    const unsigned char *As = role ? dOs : Qs;
+    // The transposed operand of the accumulation: dO^T for dV, Q^T for dK.
+    const unsigned char *Ts = G == kDV ? dOs : Qs;
 
 #pragma unroll
     for (int m = 0; m < 2; ++m) {
-      // Pair-uniform: does any row of this half see a key of the pair?
-      const bool active = i0 + 32 * m + 31 >= wk0;
-      // acc[r] holds row i0 + 32m + 8(r/4) + 4hh + r%4, key `key`:
-      // P (role 0) or dP (role 1).
-      f32x16 acc;
-      if (active) {
+      if (i0 + 32 * m + 31 < wk0) continue;  // wave-uniform: half entirely above the keys
+      // sacc[r] holds row i0 + 32m + 8(r/4) + 4hh + r%4, key `key`.
+      f32x16 sacc, pacc;
 #pragma unroll
-        for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+      for (int r = 0; r < 16; ++r) sacc[r] = 0.f;
+      if constexpr (G == kDK) {
 #pragma unroll
-        for (int s = 0; s < C::NS; ++s) {
-          const bf16x8 a =
-              *reinterpret_cast<const bf16x8 *>(As + a_off[s] + m * 32 * T::ROW_BYTES);
-          acc = mfma32x32x16(a, bf[s], acc);
-        }
-        if (role == 0) {
-          const bool diag = i0 + 32 * m < wk0 + 31;
-#pragma unroll
-          for (int g = 0; g < 4; ++g) {
-            const f32x4 l4 =
-                *reinterpret_cast<const f32x4 *>(lse_s + 32 * m + 8 * g + 4 * hh);
-#pragma unroll
-            for (int x = 0; x < 4; ++x) {
-              const int r = 4 * g + x;
-              float p = fast_exp2(fmaf(acc[r], c, -l4[x]));
-              if (diag && key > i0 + 32 * m + 8 * g + 4 * hh + x) p = 0.f;
-              acc[r] = p;
-            }
-          }
-        }
-        f32x4 *mine = reinterpret_cast<f32x4 *>(xslot(m, kg, role));
-#pragma unroll
-        for (int g = 0; g < 4; ++g)
-          mine[g * 64 + lane] = (f32x4){acc[4 * g], acc[4 * g + 1], acc[4 * g + 2], acc[4 * g + 3]};
+        for (int r = 0; r < 16; ++r) pacc[r] = 0.f;
       }
-      __syncthreads();  // every wave, active or not: the exchange of this half
-      if (active) {
-        const f32x4 *other = reinterpret_cast<const f32x4 *>(xslot(m, kg, role ^ 1));
-        f32x16 P, dS;
+#pragma unroll
+      for (int s = 0; s < C::NS; ++s) {
+        const bf16x8 aq = *reinterpret_cast<const bf16x8 *>(Qs + a_off[s] + m * 32 * T::ROW_BYTES);
+        sacc = mfma32x32x16(aq, kf[s], sacc);
+        if constexpr (G == kDK) {
+          const bf16x8 ad =
+              *reinterpret_cast<const bf16x8 *>(dOs + a_off[s] + m * 32 * T::ROW_BYTES);
+          pacc = mfma32x32x16(ad, vf[s], pacc);
+        }
+      }
+      // P (masked on the diagonal), then dS for dK.
+      if (i0 + 32 * m < wk0 + 31) {
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
-          const f32x4 o4 = other[g * 64 + lane];
-          const f32x4 d4 = *reinterpret_cast<const f32x4 *>(D_s + 32 * m + 8 * g + 4 * hh);
+          const f32x4 l4 = *reinterpret_cast<const f32x4 *>(lse_s + 32 * m + 8 * g + 4 * hh);
 #pragma unroll
           for (int x = 0; x < 4; ++x) {
             const int r = 4 * g + x;
-            const float p = role ? o4[x] : acc[r];
-            const float dp = role ? acc[r] : o4[x];
-            P[r] = p;
-            dS[r] = p * (dp - d4[x]);
+            const float p = fast_exp2(fmaf(sacc[r], c, -l4[x]));
+            sacc[r] = key > i0 + 32 * m + 8 * g + 4 * hh + x ? 0.f : p;
           }
         }
-        // P and dS as B operands along the rows: block s2 covers rows
-        // 32m + 16*s2 .. +15, slot t <-> register 8*s2 + t.
-        bf16x8 pb[2], sb[2];
+      } else {
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const f32x4 l4 = *reinterpret_cast<const f32x4 *>(lse_s + 32 * m + 8 * g + 4 * hh);
+#pragma unroll
+          for (int x = 0; x < 4; ++x) sacc[4 * g + x] = fast_exp2(fmaf(sacc[4 * g + x], c, -l4[x]));
+        }
+      }
+      if constexpr (G == kDK) {
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const f32x4 d4 = *reinterpret_cast<const f32x4 *>(D_s + 32 * m + 8 * g + 4 * hh);
+#pragma unroll
+          for (int x = 0; x < 4; ++x) sacc[4 * g + x] *= pacc[4 * g + x] - d4[x];
+        }
+      }
+      // P or dS as the B operand along the rows: block s2 covers rows
+      // 32m + 16*s2 .. +15, slot t <-> register 8*s2 + t.
+      bf16x8 b[2];
+#pragma unroll
+      for (int s2 = 0; s2 < 2; ++s2) {
+        const int b8 = 8 * s2;
+        u32x4 t4 = {pack_bf16x2(sacc[b8 + 0], sacc[b8 + 1]), pack_bf16x2(sacc[b8 + 2], sacc[b8 + 3]),
+                    pack_bf16x2(sacc[b8 + 4], sacc[b8 + 5]), pack_bf16x2(sacc[b8 + 6], sacc[b8 + 7])};
+        b[s2] = as_bf16x8(t4);
+      }
+      // dV^T += dO^T P  or  dK^T += Q^T dS: M = head dim, N = keys, K = rows;
+      // the transposed A operand comes straight from the row-major tile.
+#pragma unroll
+      for (int n = 0; n < C::NE; ++n)
 #pragma unroll
         for (int s2 = 0; s2 < 2; ++s2) {
-          const int b8 = 8 * s2;
-          u32x4 tp = {pack_bf16x2(P[b8 + 0], P[b8 + 1]), pack_bf16x2(P[b8 + 2], P[b8 + 3]),
-                      pack_bf16x2(P[b8 + 4], P[b8 + 5]), pack_bf16x2(P[b8 + 6], P[b8 + 7])};
-          u32x4 ts = {pack_bf16x2(dS[b8 + 0], dS[b8 + 1]), pack_bf16x2(dS[b8 + 2], dS[b8 + 3]),
-                      pack_bf16x2(dS[b8 + 4], dS[b8 + 5]), pack_bf16x2(dS[b8 + 6], dS[b8 + 7])};
-          pb[s2] = as_bf16x8(tp);
-          sb[s2] = as_bf16x8(ts);
+          const int ro = (2 * m + s2) * 16 * T::ROW_BYTES;
+          const bf16x8 a = tr_operand(Ts, t_off[n][0] + ro, t_off[n][1] + ro);
+          acc[n] = mfma32x32x16(a, b[s2], acc[n]);
         }
-        // dV^T += dO^T P,  dK^T += Q^T dS on this role's head-dim half; the
-        // transposed A operands come straight from the row-major tiles.
-#pragma unroll
-        for (int n = 0; n < C::NEH; ++n)
-#pragma unroll
-          for (int s2 = 0; s2 < 2; ++s2) {
-            const int ro = (2 * m + s2) * 16 * T::ROW_BYTES;
-            const uint2 dlo = lds_read_tr4(dOs, t_off[n][0] + ro);
-            const uint2 dhi = lds_read_tr4(dOs, t_off[n][1] + ro);
-            const uint2 qlo = lds_read_tr4(Qs, t_off[n][0] + ro);
-            const uint2 qhi = lds_read_tr4(Qs, t_off[n][1] + ro);
-            const u32x4 ad = {dlo.x, dlo.y, dhi.x, dhi.y};
-            const u32x4 aq = {qlo.x, qlo.y, qhi.x, qhi.y};
-            dvacc[n] = mfma32x32x16(as_bf16x8(ad), pb[s2], dvacc[n]);
-            dkacc[n] = mfma32x32x16(as_bf16x8(aq), sb[s2], dkacc[n]);
-          }
-      }
     }
     if (st + 1 < nsteps) store_step((st + 1) & 1);
     __syncthreads();
   }
 
-  // dkacc[n][r] = dK^T[e = 32(role*NEH + n) + 8(r/4) + 4hh + r%4][key]
+  // acc[n][r] = (dV or dK)^T[e = 32n + 8(r/4) + 4hh + r%4][key]
   if (key < S) {
-    float *dkr = dk + ((size_t)(beta * S + key) * Hkl + kvh) * D;
-    float *dvr = dv + ((size_t)(beta * S + key) * Hkl + kvh) * D;
+    float *o = out + ((size_t)(beta * S + key) * Hkl + kvh) * D;
 #pragma unroll
-    for (int n = 0; n < C::NEH; ++n)
+    for (int n = 0; n < C::NE; ++n)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
-        const int e = 32 * (role * C::NEH + n) + 8 * g + 4 * hh;
-        f32x4 a = {dkacc[n][4 * g] * scale, dkacc[n][4 * g + 1] * scale,
-                   dkacc[n][4 * g + 2] * scale, dkacc[n][4 * g + 3] * scale};
-        f32x4 b = {dvacc[n][4 * g], dvacc[n][4 * g + 1], dvacc[n][4 * g + 2],
-                   dvacc[n][4 * g + 3]};
-        *reinterpret_cast<f32x4 *>(dkr + e) = a;
-        *reinterpret_cast<f32x4 *>(dvr + e) = b;
+        f32x4 a = {acc[n][4 * g] * out_scale, acc[n][4 * g + 1] * out_scale,
+                   acc[n][4 * g + 2] * out_scale, acc[n][4 * g + 3] * out_scale};
+        *reinterpret_cast<f32x4 *>(o + 32 * n + 8 * g + 4 * hh) = a;
       }
   }
+}
+
+// ---------------------------------------------------------------- bwd_reduce
+// dK or dV of a key = the sum of the partial sums of the row chunks that
+// exist for its key tile, added in chunk order (deterministic).  One thread
+// per 4 consecutive elements.
+__global__ __launch_bounds__(kThreads) void bwd_reduce_kernel(
+    const float *__restrict__ part, float *__restrict__ out, long long n4 /* b*S*Hkl*D/4 */,
+    int S, int row_elems /* Hkl*D */, int nchunks, int chunk_rows) {
+  const long long i4 = (long long)blockIdx.x * kThreads + threadIdx.x;
+  if (i4 >= n4) return;
+  const long long e = i4 * 4;
+  const int key = (int)((e / row_elems) % S);
+  const int first = (key / kKN) * kKN / chunk_rows;  // first chunk the key tile wrote
+  const long long slice = n4 * 4;
+  f32x4 acc = *reinterpret_cast<const f32x4 *>(part + (size_t)first * slice + e);
+  for (int ch = first + 1; ch < nchunks; ++ch) {
+    const f32x4 x = *reinterpret_cast<const f32x4 *>(part + (size_t)ch * slice + e);
+    acc[0] += x[0];
+    acc[1] += x[1];
+    acc[2] += x[2];
+    acc[3] += x[3];
+  }
+  *reinterpret_cast<f32x4 *>(out + e) = acc;
 }
 
 // ---------------------------------------------------------------- bwd_dq
@@ -487,10 +514,8 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(
 #pragma unroll
           for (int s2 = 0; s2 < 2; ++s2) {
             const int ro = (2 * m + s2) * 16 * T::ROW_BYTES;
-            const uint2 lo = lds_read_tr4(Ks, t_off[n][0] + ro);
-            const uint2 hi = lds_read_tr4(Ks, t_off[n][1] + ro);
-            const u32x4 a4 = {lo.x, lo.y, hi.x, hi.y};
-            qacc[n] = mfma32x32x16(as_bf16x8(a4), sb[s2], qacc[n]);
+            const bf16x8 a = tr_operand(Ks, t_off[n][0] + ro, t_off[n][1] + ro);
+            qacc[n] = mfma32x32x16(a, sb[s2], qacc[n]);
           }
       }
     }
@@ -531,9 +556,27 @@ hipError_t launch_bwd_d(const void *q, const void *k, const void *v, const void 
 
   const int ktiles = (s.S + kKN - 1) / kKN;
   const int kvheads_total = s.b * s.Hkl;
-  hipLaunchKernelGGL(bwd_dkdv_kernel<D>, dim3((unsigned)(ktiles * kvheads_total)),
-                     dim3(kDkdvThreads), 0, stream, qp, kp, vp, dop, lse, Dbuf, dk, dv, s.S,
-                     s.Hl, s.Hkl, n_rep, kvheads_total, c, s.scale);
+  const BwdChunks ck = bwd_chunks(s);
+  const dim3 kv_grid((unsigned)(ck.n * ktiles * kvheads_total));
+  float *dv_out = dv, *dk_out = dk;
+  if (ck.n > 1) {  // partial sums in the workspace, reduced below
+    dv_out = Dbuf + ck.part_offset_floats;
+    dk_out = dv_out + (size_t)ck.n * kvheads_total * s.S * D;
+  }
+  hipLaunchKernelGGL((bwd_kv_kernel<D, kDV>), kv_grid, dim3(kThreads), 0, stream, qp, kp, vp,
+                     dop, lse, Dbuf, dv_out, s.S, s.Hl, s.Hkl, n_rep, kvheads_total, ktiles,
+                     ck.rows, c, 1.f);
+  hipLaunchKernelGGL((bwd_kv_kernel<D, kDK>), kv_grid, dim3(kThreads), 0, stream, qp, kp, vp,
+                     dop, lse, Dbuf, dk_out, s.S, s.Hl, s.Hkl, n_rep, kvheads_total, ktiles,
+                     ck.rows, c, s.scale);
+  if (ck.n > 1) {
+    const long long n4 = (long long)kvheads_total * s.S * D / 4;
+    const dim3 rg((unsigned)((n4 + kThreads - 1) / kThreads));
+    hipLaunchKernelGGL(bwd_reduce_kernel, rg, dim3(kThreads), 0, stream, dv_out, dv, n4, s.S,
+                       s.Hkl * D, ck.n, ck.rows);
+    hipLaunchKernelGGL(bwd_reduce_kernel, rg, dim3(kThreads), 0, stream, dk_out, dk, n4, s.S,
+                       s.Hkl * D, ck.n, ck.rows);
+  }
 
   const int qtiles = (s.S + kDQM - 1) / kDQM;
   const int heads_total = s.b * s.Hl;
@@ -546,8 +589,10 @@ hipError_t launch_bwd_d(const void *q, const void *k, const void *v, const void 
 }  // namespace
 
 size_t attn_bwd_workspace_bytes(const AttnShape &s) {
-  const size_t n = (size_t)s.b * s.Hl * s.S * sizeof(float);
-  return (n + 255) & ~(size_t)255;
+  const BwdChunks ck = bwd_chunks(s);
+  size_t floats = ck.part_offset_floats;
+  if (ck.n > 1) floats += 2 * (size_t)ck.n * s.b * s.Hkl * s.S * s.d;
+  return floats * sizeof(float);
 }
 
 hipError_t launch_attn_bwd(const void *q, const void *k, const void *v,

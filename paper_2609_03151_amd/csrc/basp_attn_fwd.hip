@@ -217,10 +217,9 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(
       for (int n = 0; n < C::NE; ++n)
 #pragma unroll
         for (int s2 = 0; s2 < kBN / 16; ++s2) {
-          const uint2 lo = lds_read_tr4(Vs, v_off[n][0] + s2 * 16 * T::ROW_BYTES);
-          const uint2 hi = lds_read_tr4(Vs, v_off[n][1] + s2 * 16 * T::ROW_BYTES);
-          const u32x4 a4 = {lo.x, lo.y, hi.x, hi.y};
-          oacc[n] = mfma32x32x16(as_bf16x8(a4), pf[s2], oacc[n]);
+          const bf16x8 a = tr_operand(Vs, v_off[n][0] + s2 * 16 * T::ROW_BYTES,
+                                      v_off[n][1] + s2 * 16 * T::ROW_BYTES);
+          oacc[n] = mfma32x32x16(a, pf[s2], oacc[n]);
         }
     }
     if (t + 1 < nt) store_tile((t + 1) & 1);

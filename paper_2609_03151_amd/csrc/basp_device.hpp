@@ -126,6 +126,13 @@ __device__ __forceinline__ uint2 lds_read_tr4(const unsigned char *tile, int byt
   return __builtin_bit_cast(uint2, v);
 }
 
+// One MFMA operand from two transposed 4-element reads (slots 0-3, 4-7).
+__device__ __forceinline__ bf16x8 tr_operand(const unsigned char *tile, int off_lo, int off_hi) {
+  const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)(tile + off_lo));
+  const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)(tile + off_hi));
+  return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+}
+
 // Byte offset, inside an LdsTile<D>, of the 8-byte piece lane `lane` passes to
 // lds_read_tr4 when reading columns [e0, e0+16) over rows [r0, r0+4).
 template <int D>

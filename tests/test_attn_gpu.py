@@ -52,6 +52,8 @@ SMALL = [  # b, S, Hl, Hkl, d
     (1, 77, 2, 2, 128),      # shorter than one tile
     (1, 1, 2, 1, 64),        # a single token
     (1, 2048, 4, 1, 128),    # 16 row tiles, 32 key tiles
+    (1, 2500, 2, 1, 128),    # dK/dV rows split into 2 chunks, ragged tail
+    (1, 4096, 4, 2, 64),     # 2 chunks, d = 64
 ]
 
 
