@@ -79,9 +79,6 @@ __device__ __forceinline__ rsrc_t make_rsrc(const void *base, uint32_t num_bytes
 __device__ __forceinline__ u32x4 buf_load16(rsrc_t r, uint32_t off) {
   return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
 }
-__device__ __forceinline__ float buf_load_f32(rsrc_t r, uint32_t off) {
-  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
-}
 
 // ------------------------------------------------------------- LDS tiles
 // A [rows][D] bf16 tile stored row-major without padding, its 16-byte chunks
@@ -119,14 +116,8 @@ typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 // every group of 16 lanes, lane i receives element i%4 of the 8-byte pieces
 // addressed by lanes i/4, i/4+4, i/4+8, i/4+12.  With lane c of the group
 // addressing row r0 + c/4, columns e0 + 4(c%4) .. +3, lane i therefore gets
-// the column e0 + i over rows r0 .. r0+3: a transposed read.
-__device__ __forceinline__ uint2 lds_read_tr4(const unsigned char *tile, int byte_off) {
-  i16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-      (lds_i16x4 *)(tile + byte_off));
-  return __builtin_bit_cast(uint2, v);
-}
-
-// One MFMA operand from two transposed 4-element reads (slots 0-3, 4-7).
+// the column e0 + i over rows r0 .. r0+3: a transposed read.  Two such reads
+// give one MFMA operand (slots 0-3 and 4-7).
 __device__ __forceinline__ bf16x8 tr_operand(const unsigned char *tile, int off_lo, int off_hi) {
   const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)(tile + off_lo));
   const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4 *)(tile + off_hi));
@@ -134,7 +125,7 @@ __device__ __forceinline__ bf16x8 tr_operand(const unsigned char *tile, int off_
 }
 
 // Byte offset, inside an LdsTile<D>, of the 8-byte piece lane `lane` passes to
-// lds_read_tr4 when reading columns [e0, e0+16) over rows [r0, r0+4).
+// ds_read_b64_tr_b16 when reading columns [e0, e0+16) over rows [r0, r0+4).
 template <int D>
 __device__ __forceinline__ int tr_piece_off(int r0, int e0, int lane) {
   const int c = lane & 15;
