@@ -31,6 +31,37 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
+def kernel_source_sha256() -> str:
+    """Hash of the HIP sources and the C ABI header (matches profiles/traffic_*.txt)."""
+    import glob
+    import hashlib
+    h = hashlib.sha256()
+    paths = sorted(glob.glob(os.path.join(ROOT, "paper_2609_03151_amd", "csrc", "*")))
+    paths.append(os.path.join(ROOT, "include", "basp.h"))
+    for p in paths:
+        if p.endswith((".hip", ".hpp", ".cpp", ".h")):
+            with open(p, "rb") as f:
+                h.update(f.read())
+    return h.hexdigest()
+
+
+def recorded_traffic(workload: str):
+    """HBM traffic per attention-backward launch from the committed counter
+    summary, or None when the kernels changed since those counters were taken."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.txt")
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    with open(path) as f:
+        for ln in f:
+            if "=" in ln and not ln.startswith("#"):
+                a, b = ln.split("=", 1)
+                kv[a.strip()] = b.strip()
+    if kv.get("source_sha256") != kernel_source_sha256():
+        return None
+    return int(kv["traffic_bytes"])
+
+
 def cpu_baseline(w, target_s: float):
     """Time the oracle (fp64, OpenMP) on a bounded prefix of the workload.
 
@@ -149,10 +180,11 @@ def main():
         "config": {"workload": w.name, "b": w.b, "S": w.S, "H": w.H, "H_kv": w.H_kv, "d": w.d,
                    "G": w.G, "rank": w.rank, "causal": True, "inputs": "bf16 N(0,1), seeded"},
         "roofline": {
-            "kernel": ("basp_attn_bwd (bwd_pre + bwd_kv<dV> + bwd_kv<dK> + bwd_dq)" if dom == "attn_bwd"
-                       else "basp_attn_fwd"),
+            "kernel": ("basp_attn_bwd (bwd_pre, bwd_kv<dV>, bwd_kv<dK>, 2 x bwd_reduce, bwd_dq)"
+                       if dom == "attn_bwd" else "basp_attn_fwd"),
             "bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
-            "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+            "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+            "traffic": recorded_traffic(w.name) if dom == "attn_bwd" else None,
         },
         "attn_fwd_tflops": round(fwd_tf, 2),
         "attn_bwd_tflops": round(bwd_tf, 2),
