@@ -9,8 +9,9 @@
 // changes only rounding.
 //
 // gfx950 mapping
-//   * workgroup = 4 waves = 128 query rows of one (sequence, head); wave w
-//     owns rows q0 + 32w .. +31, one row per lane pair (l, l+32).
+//   * workgroup = 8 waves = 256 query rows of one (sequence, head), one
+//     workgroup per CU (two waves per SIMD); wave w owns rows q0 + 32w .. +31,
+//     one row per lane pair (l, l+32).
 //   * scores are formed transposed, S^T = K Q^T, with
 //     v_mfma_f32_32x32x16_bf16: K (A operand) from LDS, Q (B operand) kept
 //     in registers for the whole loop.  The 32x32 accumulator then gives each
@@ -20,16 +21,22 @@
 //     operand (bf16, round to nearest even).  V^T (A operand) is read from the
 //     row-major V tile with ds_read_b64_tr_b16, two 4-key reads per operand,
 //     in exactly the key order the accumulator holds P in.
-//   * K/V tiles of 64 keys are loaded with 16-byte buffer loads (rows past S
-//     read as zero), stored row-major with an XOR swizzle (conflict-free for
-//     both read patterns), double-buffered and prefetched one tile ahead.
+//   * K/V tiles of 64 keys are copied HBM -> LDS by buffer loads that write
+//     LDS directly (no register staging; rows past S arrive as zeros) into a
+//     ring of four stages, two tiles ahead of the one being consumed.  Tiles
+//     are stored row-major with an XOR swizzle that is conflict-free for both
+//     read patterns.  The LDS operand reads are scheduled one step ahead of
+//     the MFMAs that consume them.
 //   * the running maximum used as the exponent reference only moves when a
 //     row's maximum grows by more than 8 (in log2 units): P <= 2^8 stays exact
 //     in bf16's relative precision and O is rescaled only on those tiles.
-//   * tiles past a wave's last row are skipped; only tiles crossing the
-//     diagonal are masked.  The grid is one-dimensional, heaviest query tiles
+//   * tiles strictly below the workgroup's diagonal band run a loop without
+//     any masking code; band tiles are masked, and a wave skips band tiles
+//     past its last row.  The grid is one-dimensional, heaviest query tiles
 //     first, heads fastest, so heads sharing a kv head run side by side.
 #include <math.h>
+
+#include <type_traits>
 
 #include "basp_device.hpp"
 #include "basp_internal.hpp"
@@ -37,10 +44,16 @@
 namespace basp {
 namespace {
 
-constexpr int kThreads = 256;
-constexpr int kBM = 128;          // query rows per workgroup
+constexpr int kThreads = 512;
+constexpr int kWaves = 8;
+constexpr int kBM = 32 * kWaves;   // query rows per workgroup
+constexpr int kStages = 4;
+constexpr int kPD = 2;            // tiles prefetched ahead
 constexpr int kBN = 64;           // keys per tile
 constexpr float kRescaleSlack = 8.f;  // log2 headroom before the reference max moves
+// Instruction classes of __builtin_amdgcn_sched_group_barrier.
+constexpr int kSchedMfma = 0x008;
+constexpr int kSchedDsRead = 0x100;
 
 template <int D>
 struct FwdCfg {
@@ -49,18 +62,18 @@ struct FwdCfg {
   static constexpr int NS = D / 16;                   // 16-deep steps over the head dim
   static constexpr int NE = D / 32;                   // 32-wide head-dim subtiles of O
   static constexpr int CPR = D / 8;                   // 16-byte chunks per row
-  static constexpr int CHUNKS = kBN * CPR / kThreads; // chunks per thread per tile
+  static constexpr int DMA_PER_WAVE = kBN * CPR / kThreads;  // 1 KB loads per wave per tensor
 };
 
 template <int D>
-__global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(
+__global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
     const uint16_t *__restrict__ q, const uint16_t *__restrict__ k,
     const uint16_t *__restrict__ v, uint16_t *__restrict__ o,
     float *__restrict__ lse, int S, int Hl, int Hkl, int n_rep, int heads_total,
     int qtiles, float c /* scale * log2(e) */) {
   using C = FwdCfg<D>;
   using T = LdsTile<D>;
-  __shared__ __attribute__((aligned(16))) unsigned char smem[2 * C::STAGE_BYTES];
+  __shared__ __attribute__((aligned(16))) unsigned char smem[kStages * C::STAGE_BYTES];
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int l32 = lane & 31, hh = lane >> 5;
@@ -87,33 +100,27 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(
   const int kv_end = min(S, q0 + kBM);
   const int nt = (kv_end + kBN - 1) / kBN;
 
-  // Per-thread chunk coordinates of the tile loads (fixed across tiles).
-  uint32_t g_off[C::CHUNKS];
-  int s_off[C::CHUNKS];
+  uint32_t g_off[C::DMA_PER_WAVE];
 #pragma unroll
-  for (int r = 0; r < C::CHUNKS; ++r) {
-    const int cidx = tid + r * kThreads;
-    const int jr = cidx / C::CPR, cc = cidx % C::CPR;
-    g_off[r] = (uint32_t)jr * kv_row_bytes + cc * 16;
-    s_off[r] = T::off(jr, cc);
-  }
-  u32x4 kreg[C::CHUNKS], vreg[C::CHUNKS];
-  auto load_tile = [&](int t) {
+  for (int i = 0; i < C::DMA_PER_WAVE; ++i)
+    g_off[i] = dma_src_off<D>((w * C::DMA_PER_WAVE + i) * 64 + lane, kv_row_bytes);
+  auto load_tile = [&](int t) {  // issue; lands asynchronously in stage t % kStages
+    unsigned char *Ks = smem + (t % kStages) * C::STAGE_BYTES;
+    unsigned char *Vs = Ks + C::TILE_BYTES;
     const uint32_t base = (uint32_t)(t * kBN) * kv_row_bytes;
 #pragma unroll
-    for (int r = 0; r < C::CHUNKS; ++r) {
-      kreg[r] = buf_load16(rk, base + g_off[r]);
-      vreg[r] = buf_load16(rv, base + g_off[r]);
+    for (int i = 0; i < C::DMA_PER_WAVE; ++i) {
+      const int lds_off = (w * C::DMA_PER_WAVE + i) * 1024;
+      buf_load16_lds(rk, base + g_off[i], Ks + lds_off);
+      buf_load16_lds(rv, base + g_off[i], Vs + lds_off);
     }
   };
-  auto store_tile = [&](int buf) {
-    unsigned char *Ks = smem + buf * C::STAGE_BYTES;
-    unsigned char *Vs = Ks + C::TILE_BYTES;
-#pragma unroll
-    for (int r = 0; r < C::CHUNKS; ++r) {
-      *reinterpret_cast<u32x4 *>(Ks + s_off[r]) = kreg[r];
-      *reinterpret_cast<u32x4 *>(Vs + s_off[r]) = vreg[r];
-    }
+  // Wait until this wave's loads of tile t landed, with `ahead` later tiles
+  // (2 * DMA_PER_WAVE loads each) still in flight.
+  auto wait_tile = [&](int ahead) {
+    if (ahead >= 2) wait_vmcnt<4 * C::DMA_PER_WAVE>();
+    else if (ahead == 1) wait_vmcnt<2 * C::DMA_PER_WAVE>();
+    else wait_vmcnt<0>();
   };
 
   // LDS offsets of this lane's operand reads (fixed across tiles).
@@ -121,7 +128,10 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(
   // row modulo 16 only, so row 32 + r sits 32 rows further on.
   int k_off[C::NS];
 #pragma unroll
-  for (int s = 0; s < C::NS; ++s) k_off[s] = T::off(l32, 2 * s + hh);
+  for (int s = 0; s < C::NS; ++s) {
+    k_off[s] = T::off(l32, 2 * s + hh);
+    asm volatile("" : "+v"(k_off[s]));  // keep in a register, do not recompute per tile
+  }
   // A of O^T: V^T rows e = 32n + l32, keys 16*s2 + 4hh + {0..3} and + 8.
   // Transposed A operand: rows 16*s2 + 4hh (+8), columns 32n + 16*((lane/16)&1);
   // row block s2 sits 16*s2 rows further on (same swizzle).
@@ -129,8 +139,10 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(
 #pragma unroll
   for (int n = 0; n < C::NE; ++n)
 #pragma unroll
-    for (int x = 0; x < 2; ++x)
+    for (int x = 0; x < 2; ++x) {
       v_off[n][x] = tr_piece_off<D>(4 * hh + 8 * x, 32 * n + 16 * ((lane >> 4) & 1), lane);
+      asm volatile("" : "+v"(v_off[n][x]));
+    }
 
   f32x16 oacc[C::NE];
 #pragma unroll
@@ -139,91 +151,121 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(
     for (int r = 0; r < 16; ++r) oacc[n][r] = 0.f;
   float m_ref = -INFINITY, l_run = 0.f;
 
-  load_tile(0);
-  store_tile(0);
-  __syncthreads();
+  for (int t = 0; t < kPD && t < nt; ++t) load_tile(t);
 
-  for (int t = 0; t < nt; ++t) {
-    if (t + 1 < nt) load_tile(t + 1);
+  // One tile: scores, softmax update, P V.  MASK only for tiles that can
+  // hold keys past some row of the workgroup (the diagonal band).
+  auto tile = [&](int t, auto mask_tag) {
+    constexpr bool MASK = decltype(mask_tag)::value;
     const int j0 = t * kBN;
-    if (j0 <= wrow0 + 31) {  // wave-uniform: tile has keys visible to this wave
-      const unsigned char *Ks = smem + (t & 1) * C::STAGE_BYTES;
-      const unsigned char *Vs = Ks + C::TILE_BYTES;
+    const unsigned char *Ks = smem + (t % kStages) * C::STAGE_BYTES;
+    const unsigned char *Vs = Ks + C::TILE_BYTES;
 
-      f32x16 sacc[2];
+    f32x16 sacc[2];
 #pragma unroll
-      for (int m = 0; m < 2; ++m)
+    for (int m = 0; m < 2; ++m) {
+      const bf16x8 a = *reinterpret_cast<const bf16x8 *>(Ks + k_off[0] + m * 32 * T::ROW_BYTES);
+      sacc[m] = mfma32x32x16(a, qf[0], f32x16{});
+    }
 #pragma unroll
-        for (int r = 0; r < 16; ++r) sacc[m][r] = 0.f;
+    for (int s = 1; s < C::NS; ++s)
 #pragma unroll
-      for (int s = 0; s < C::NS; ++s)
+      for (int m = 0; m < 2; ++m) {
+        const bf16x8 a = *reinterpret_cast<const bf16x8 *>(Ks + k_off[s] + m * 32 * T::ROW_BYTES);
+        sacc[m] = mfma32x32x16(a, qf[s], sacc[m]);
+      }
+    // Schedule: LDS reads run one k-step ahead of the MFMAs.
+    __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 4, 0);
 #pragma unroll
-        for (int m = 0; m < 2; ++m) {
-          const bf16x8 a = *reinterpret_cast<const bf16x8 *>(Ks + k_off[s] + m * 32 * T::ROW_BYTES);
-          sacc[m] = mfma32x32x16(a, qf[s], sacc[m]);
-        }
+    for (int i = 0; i < C::NS - 2; ++i) {
+      __builtin_amdgcn_sched_group_barrier(kSchedMfma, 2, 0);
+      __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 2, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(kSchedMfma, 4, 0);
 
-      // sacc[m][r] = S^T[key j0 + 32m + 8(r/4) + 4hh + r%4][query row]
-      if (j0 + kBN - 1 > wrow0) {
-#pragma unroll
-        for (int m = 0; m < 2; ++m)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int j = j0 + 32 * m + 8 * (r >> 2) + 4 * hh + (r & 3);
-            if (j > row) sacc[m][r] = -INFINITY;
-          }
-      }
-      float mx = -INFINITY;
-#pragma unroll
-      for (int m = 0; m < 2; ++m)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[m][r]);
-      mx = fmaxf(mx, swap_halves(mx)) * c;
-      // Move the reference only when the row maximum outgrew it by the slack
-      // (always on a row's first tile, where m_ref is -inf).
-      const bool grow = mx > m_ref + kRescaleSlack;
-      if (__builtin_amdgcn_ballot_w64(grow)) {  // wave-uniform
-        const float m_new = grow ? mx : m_ref;
-        const float alpha = fast_exp2(m_ref - m_new);
-        m_ref = m_new;
-        l_run *= alpha;
-#pragma unroll
-        for (int n = 0; n < C::NE; ++n)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) oacc[n][r] *= alpha;
-      }
-      float psum = 0.f;
+    // sacc[m][r] = S^T[key j0 + 32m + 8(r/4) + 4hh + r%4][query row]
+    if constexpr (MASK) {
 #pragma unroll
       for (int m = 0; m < 2; ++m)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const float p = fast_exp2(fmaf(sacc[m][r], c, -m_ref));
-          sacc[m][r] = p;
-          psum += p;
+          const int j = j0 + 32 * m + 8 * (r >> 2) + 4 * hh + (r & 3);
+          if (j > row) sacc[m][r] = -INFINITY;
         }
-      l_run += psum;
-
-      bf16x8 pf[kBN / 16];
+    }
+    float mx = -INFINITY;
 #pragma unroll
-      for (int s2 = 0; s2 < kBN / 16; ++s2) {
-        const int m = s2 >> 1, b8 = (s2 & 1) * 8;
-        u32x4 t4 = {pack_bf16x2(sacc[m][b8 + 0], sacc[m][b8 + 1]),
-                    pack_bf16x2(sacc[m][b8 + 2], sacc[m][b8 + 3]),
-                    pack_bf16x2(sacc[m][b8 + 4], sacc[m][b8 + 5]),
-                    pack_bf16x2(sacc[m][b8 + 6], sacc[m][b8 + 7])};
-        pf[s2] = as_bf16x8(t4);
-      }
+    for (int m = 0; m < 2; ++m)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[m][r]);
+    mx = fmaxf(mx, swap_halves(mx)) * c;
+    // Move the reference only when the row maximum outgrew it by the slack
+    // (always on a row's first tile, where m_ref is -inf).
+    const bool grow = mx > m_ref + kRescaleSlack;
+    if (__builtin_amdgcn_ballot_w64(grow)) {  // wave-uniform, rare after the first tiles
+      asm volatile("" ::: "memory");  // keep this a real branch (no if-conversion)
+      const float m_new = grow ? mx : m_ref;
+      const float alpha = fast_exp2(m_ref - m_new);
+      m_ref = m_new;
+      l_run *= alpha;
 #pragma unroll
       for (int n = 0; n < C::NE; ++n)
 #pragma unroll
-        for (int s2 = 0; s2 < kBN / 16; ++s2) {
-          const bf16x8 a = tr_operand(Vs, v_off[n][0] + s2 * 16 * T::ROW_BYTES,
-                                      v_off[n][1] + s2 * 16 * T::ROW_BYTES);
-          oacc[n] = mfma32x32x16(a, pf[s2], oacc[n]);
-        }
+        for (int r = 0; r < 16; ++r) oacc[n][r] *= alpha;
     }
-    if (t + 1 < nt) store_tile((t + 1) & 1);
+    float psum = 0.f;
+#pragma unroll
+    for (int m = 0; m < 2; ++m)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float p = fast_exp2(fmaf(sacc[m][r], c, -m_ref));
+        sacc[m][r] = p;
+        psum += p;
+      }
+    l_run += psum;
+
+    bf16x8 pf[kBN / 16];
+#pragma unroll
+    for (int s2 = 0; s2 < kBN / 16; ++s2) {
+      const int m = s2 >> 1, b8 = (s2 & 1) * 8;
+      u32x4 t4 = {pack_bf16x2(sacc[m][b8 + 0], sacc[m][b8 + 1]),
+                  pack_bf16x2(sacc[m][b8 + 2], sacc[m][b8 + 3]),
+                  pack_bf16x2(sacc[m][b8 + 4], sacc[m][b8 + 5]),
+                  pack_bf16x2(sacc[m][b8 + 6], sacc[m][b8 + 7])};
+      pf[s2] = as_bf16x8(t4);
+    }
+#pragma unroll
+    for (int n = 0; n < C::NE; ++n)
+#pragma unroll
+      for (int s2 = 0; s2 < kBN / 16; ++s2) {
+        const bf16x8 a = tr_operand(Vs, v_off[n][0] + s2 * 16 * T::ROW_BYTES,
+                                    v_off[n][1] + s2 * 16 * T::ROW_BYTES);
+        oacc[n] = mfma32x32x16(a, pf[s2], oacc[n]);
+      }
+    // Schedule: transposed reads run two operands ahead of the MFMAs.
+    __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 4, 0);
+#pragma unroll
+    for (int i = 0; i < C::NE * (kBN / 16) - 2; ++i) {
+      __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 2, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(kSchedMfma, 2, 0);
+  };
+  auto step = [&](int t) {
+    // Stage (t+kPD) % 4 last held tile t-2, finished before this wave passed
+    // the barrier of iteration t-1.
+    if (t + kPD < nt) load_tile(t + kPD);
+    wait_tile(min(kPD, nt - 1 - t));
     __syncthreads();
+  };
+  const int t_mask = min(nt, q0 / kBN);  // tiles before t_mask need no mask
+  for (int t = 0; t < t_mask; ++t) {
+    step(t);
+    tile(t, std::false_type{});
+  }
+  for (int t = t_mask; t < nt; ++t) {
+    step(t);
+    if (t * kBN <= wrow0 + 31) tile(t, std::true_type{});  // wave-uniform
   }
 
   // oacc[n][r] = O^T[e = 32n + 8(r/4) + 4hh + r%4][query row] (unnormalised)

@@ -54,15 +54,6 @@ __device__ __forceinline__ float swap_halves(float x) {
   return __shfl_xor(x, 32, kWave);
 }
 
-// Byte-select of two dwords: the low halves of a and b -> {a.lo, b.lo}.
-__device__ __forceinline__ uint32_t lo_halves(uint32_t a, uint32_t b) {
-  return __builtin_amdgcn_perm(b, a, 0x05040100u);
-}
-// The high halves of a and b -> {a.hi, b.hi}.
-__device__ __forceinline__ uint32_t hi_halves(uint32_t a, uint32_t b) {
-  return __builtin_amdgcn_perm(b, a, 0x07060302u);
-}
-
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 
 // ---------------------------------------------------------------- buffers
@@ -78,6 +69,23 @@ __device__ __forceinline__ rsrc_t make_rsrc(const void *base, uint32_t num_bytes
 }
 __device__ __forceinline__ u32x4 buf_load16(rsrc_t r, uint32_t off) {
   return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+}
+
+// 16 bytes per lane from buffer offset `off` straight into LDS, bypassing
+// registers: lane l's bytes land at lds_base + 16*l (lds_base is the same for
+// the whole wave).  Out-of-range offsets write zeros.  Completion is counted
+// by vmcnt like any buffer load; a barrier is still needed before other waves
+// read the data.
+__device__ __forceinline__ void buf_load16_lds(rsrc_t r, uint32_t off, void *lds_base) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void *)lds_base,
+                                           16, off, 0, 0, 0);
+}
+
+// s_waitcnt vmcnt(n) with the other counters left alone (n < 64).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt is 6 bits");
+  __builtin_amdgcn_s_waitcnt(0x0F70 | (N & 15) | ((N >> 4) << 14));
 }
 
 // ------------------------------------------------------------- LDS tiles
@@ -109,6 +117,18 @@ struct LdsTile<64> {
     return r * ROW_BYTES + ((chunk ^ swz(r)) << 4);
   }
 };
+
+// Source offset, within a tile of rows `row_bytes` apart in memory, of the
+// 16-byte chunk that a linear LDS copy places at chunk slot `pos` of an
+// LdsTile<D>: slot pos holds row pos / (D/8), stored chunk pos % (D/8), i.e.
+// logical chunk (stored chunk) ^ swz(row).  Copying chunk slots in order with
+// buf_load16_lds therefore leaves the tile in its swizzled layout.
+template <int D>
+__device__ __forceinline__ uint32_t dma_src_off(int pos, uint32_t row_bytes) {
+  constexpr int CPR = D / 8;
+  const int r = pos / CPR, pc = pos % CPR;
+  return (uint32_t)r * row_bytes + ((pc ^ LdsTile<D>::swz(r)) << 4);
+}
 
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
