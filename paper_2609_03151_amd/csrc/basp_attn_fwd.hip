@@ -25,8 +25,10 @@
 //     LDS directly (no register staging; rows past S arrive as zeros) into a
 //     ring of four stages, two tiles ahead of the one being consumed.  Tiles
 //     are stored row-major with an XOR swizzle that is conflict-free for both
-//     read patterns.  The LDS operand reads are scheduled one step ahead of
-//     the MFMAs that consume them.
+//     read patterns.  Each wave waits only for its own copies of the tile it
+//     needs next and then passes a fence-free barrier, so later tiles stay in
+//     flight.  The LDS operand reads are scheduled one step ahead of the
+//     MFMAs that consume them.
 //   * the running maximum used as the exponent reference only moves when a
 //     row's maximum grows by more than 8 (in log2 units): P <= 2^8 stays exact
 //     in bf16's relative precision and O is rescaled only on those tiles.
@@ -88,14 +90,20 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
 
   const uint32_t q_row_bytes = (uint32_t)Hl * D * 2, kv_row_bytes = (uint32_t)Hkl * D * 2;
   const rsrc_t rq = make_rsrc(q + ((size_t)beta * S * Hl + h) * D, (uint32_t)S * q_row_bytes);
-  const rsrc_t rk = make_rsrc(k + ((size_t)beta * S * Hkl + kvh) * D, (uint32_t)S * kv_row_bytes);
-  const rsrc_t rv = make_rsrc(v + ((size_t)beta * S * Hkl + kvh) * D, (uint32_t)S * kv_row_bytes);
+  const u32x4 rk = make_rsrc_words(k + ((size_t)beta * S * Hkl + kvh) * D, (uint32_t)S * kv_row_bytes);
+  const u32x4 rv = make_rsrc_words(v + ((size_t)beta * S * Hkl + kvh) * D, (uint32_t)S * kv_row_bytes);
+  const int wu = __builtin_amdgcn_readfirstlane(w);
+  const uint32_t smem_lds = lds_addr_of(smem);
 
   // Q fragments (B operand of S^T = K Q^T): row `row`, e = 16s + 8hh .. +7.
   bf16x8 qf[C::NS];
 #pragma unroll
   for (int s = 0; s < C::NS; ++s)
     qf[s] = as_bf16x8(buf_load16(rq, (uint32_t)row * q_row_bytes + (2 * s + hh) * 16));
+  // Retire the Q loads before any tile copy is in flight: the compiler does
+  // not count the copies, and a wait for Q inside the tile loop would also
+  // drain the prefetched tiles.
+  wait_vmcnt<0>();
 
   const int kv_end = min(S, q0 + kBM);
   const int nt = (kv_end + kBN - 1) / kBN;
@@ -105,14 +113,13 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
   for (int i = 0; i < C::DMA_PER_WAVE; ++i)
     g_off[i] = dma_src_off<D>((w * C::DMA_PER_WAVE + i) * 64 + lane, kv_row_bytes);
   auto load_tile = [&](int t) {  // issue; lands asynchronously in stage t % kStages
-    unsigned char *Ks = smem + (t % kStages) * C::STAGE_BYTES;
-    unsigned char *Vs = Ks + C::TILE_BYTES;
+    const uint32_t ks = smem_lds + (t % kStages) * C::STAGE_BYTES;
     const uint32_t base = (uint32_t)(t * kBN) * kv_row_bytes;
 #pragma unroll
     for (int i = 0; i < C::DMA_PER_WAVE; ++i) {
-      const int lds_off = (w * C::DMA_PER_WAVE + i) * 1024;
-      buf_load16_lds(rk, base + g_off[i], Ks + lds_off);
-      buf_load16_lds(rv, base + g_off[i], Vs + lds_off);
+      const uint32_t lds_off = ks + (wu * C::DMA_PER_WAVE + i) * 1024;
+      buf_load16_lds_async(rk, base + g_off[i], lds_off);
+      buf_load16_lds_async(rv, base + g_off[i], lds_off + C::TILE_BYTES);
     }
   };
   // Wait until this wave's loads of tile t landed, with `ahead` later tiles
@@ -198,7 +205,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
     for (int m = 0; m < 2; ++m)
 #pragma unroll
       for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[m][r]);
-    mx = fmaxf(mx, swap_halves(mx)) * c;
+    mx = pair_max(mx) * c;
     // Move the reference only when the row maximum outgrew it by the slack
     // (always on a row's first tile, where m_ref is -inf).
     const bool grow = mx > m_ref + kRescaleSlack;
@@ -256,7 +263,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
     // the barrier of iteration t-1.
     if (t + kPD < nt) load_tile(t + kPD);
     wait_tile(min(kPD, nt - 1 - t));
-    __syncthreads();
+    barrier_no_fence();
   };
   const int t_mask = min(nt, q0 / kBN);  // tiles before t_mask need no mask
   for (int t = 0; t < t_mask; ++t) {
@@ -269,7 +276,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
   }
 
   // oacc[n][r] = O^T[e = 32n + 8(r/4) + 4hh + r%4][query row] (unnormalised)
-  const float l_tot = l_run + swap_halves(l_run);
+  const float l_tot = pair_sum(l_run);
   if (row < S) {
     const float inv = 1.f / l_tot;
     uint16_t *ob = o + ((size_t)(beta * S + row) * Hl + h) * D;

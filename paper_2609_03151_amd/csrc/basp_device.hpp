@@ -13,8 +13,6 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
-constexpr int kWave = 64;
-
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 
@@ -49,11 +47,6 @@ __device__ __forceinline__ float fast_log2(float x) {
   return __builtin_amdgcn_logf(x);
 }
 
-// Value held by lane (l ^ 32).
-__device__ __forceinline__ float swap_halves(float x) {
-  return __shfl_xor(x, 32, kWave);
-}
-
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 
 // ---------------------------------------------------------------- buffers
@@ -72,13 +65,64 @@ __device__ __forceinline__ u32x4 buf_load16(rsrc_t r, uint32_t off) {
 }
 
 // 16 bytes per lane from buffer offset `off` straight into LDS, bypassing
-// registers: lane l's bytes land at lds_base + 16*l (lds_base is the same for
-// the whole wave).  Out-of-range offsets write zeros.  Completion is counted
-// by vmcnt like any buffer load; a barrier is still needed before other waves
-// read the data.
-__device__ __forceinline__ void buf_load16_lds(rsrc_t r, uint32_t off, void *lds_base) {
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void *)lds_base,
-                                           16, off, 0, 0, 0);
+// registers: lane l's bytes land at lds_addr + 16*l.  Out-of-range offsets
+// write zeros.  Completion is counted by vmcnt like any buffer load.
+// Issued through inline asm: the compiler then does not know the
+// instruction writes LDS, so it neither holds later LDS reads back until
+// every copy in flight has landed (which would drain a prefetch ring) nor
+// orders anything against it.  The caller waits (vmcnt) for its own copies
+// and passes a barrier before any wave reads the data.  `rsrc` and
+// `lds_addr` (an LDS byte address) must be wave-uniform.  One wait state
+// separates the M0 write from the load.
+__device__ __forceinline__ void buf_load16_lds_async(u32x4 rsrc, uint32_t off, uint32_t lds_addr) {
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds"
+               :
+               : "v"(off), "s"(rsrc), "s"(lds_addr)
+               : "memory", "m0");
+}
+
+// Raw buffer descriptor as four dwords (same fields make_rsrc sets): base
+// address, stride 0, size in bytes, 32-bit data format.
+__device__ __forceinline__ u32x4 make_rsrc_words(const void *base, uint32_t num_bytes) {
+  const uint64_t a = (uint64_t)(uintptr_t)base;
+  return u32x4{(uint32_t)a, (uint32_t)(a >> 32) & 0xFFFFu, num_bytes, 0x00020000u};
+}
+
+// LDS byte address of a pointer into a __shared__ array.
+__device__ __forceinline__ uint32_t lds_addr_of(const void *p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void *)p;
+}
+
+// Workgroup barrier without the memory fence __syncthreads() adds (that
+// fence waits for every outstanding global load, including prefetches).
+// The empty asm statements keep the compiler from moving memory accesses
+// across it; visibility of LDS copies is the caller's explicit vmcnt wait.
+__device__ __forceinline__ void barrier_no_fence() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// max and sum of the values held by lanes l and l^32, in both lanes.
+// v_permlane32_swap exchanges lanes 32-63 of its first register with lanes
+// 0-31 of its second; with both holding x, the first ends up holding the
+// lower half of x in both halves and the second the upper half.  (Issued as
+// inline asm: the compiler builtin loses its second result.)  The nops
+// cover the VALU-write -> permlane-read hazard and the one after it.
+__device__ __forceinline__ void lane_halves(float x, float &lo, float &hi) {
+  lo = x;
+  hi = x;
+  asm("s_nop 1\n\tv_permlane32_swap_b32 %0, %1\n\ts_nop 1" : "+v"(lo), "+v"(hi));
+}
+__device__ __forceinline__ float pair_max(float x) {
+  float lo, hi;
+  lane_halves(x, lo, hi);
+  return fmaxf(lo, hi);
+}
+__device__ __forceinline__ float pair_sum(float x) {
+  float lo, hi;
+  lane_halves(x, lo, hi);
+  return lo + hi;
 }
 
 // s_waitcnt vmcnt(n) with the other counters left alone (n < 64).
