@@ -8,23 +8,31 @@
 //   dV_j  = sum_{h in group} sum_{i>=j} P_ij dO_i
 //   dK_j  = scale sum_{h in group} sum_{i>=j} dS_ij q_i
 //   dQ_i  = scale sum_{j<=i} dS_ij k_j
-// Four kernels, all deterministic (no atomics):
-//   bwd_pre   D for every (sequence, head, row)
-//   bwd_kv    key-stationary, twice (dV, then dK): a workgroup owns 128
-//             keys of one kv head and sweeps every query row at or after
-//             them, for all query heads of the GQA group, accumulating in
-//             registers
-//   bwd_dq    query-stationary: like the forward, a workgroup owns 128 rows
-//             of one query head and sweeps the keys up to the diagonal
-// On gfx950 both main kernels use v_mfma_f32_32x32x16_bf16 with fp32
-// accumulation.  Which operand order is used is chosen so that every
-// elementwise step (P, dS) happens in the accumulator layout and feeds the
-// next product without a round trip through LDS.  Operands that must be read
-// along the sequence (Q^T, dO^T, K^T) come from the same row-major LDS tiles
-// through ds_read_b64_tr_b16, in the order the accumulator holds P and dS.
-// Tiles are filled with 16-byte buffer loads (rows past S read as zero),
-// double-buffered, and each 64-wide tile is processed in two 32-wide halves.
+// Kernels, all deterministic (no atomics):
+//   bwd_pre    per (sequence, head, row): the pair (LSE in log2 units, D)
+//   bwd_kv     key-stationary, twice (dV, then dK): a workgroup owns 256
+//              keys of one kv head and sweeps the query rows at or after
+//              them (one row chunk of them), for every query head of the
+//              GQA group, accumulating in registers
+//   bwd_reduce sums the row-chunk partials of dK and dV in chunk order
+//   bwd_dq     query-stationary: like the forward, a workgroup owns 256
+//              rows of one query head and sweeps the keys up to the diagonal
+// gfx950 mapping shared by bwd_kv and bwd_dq
+//   * 8 waves per workgroup, one workgroup per CU (two waves per SIMD); each
+//     wave owns 32 keys (bwd_kv) or 32 rows (bwd_dq).
+//   * v_mfma_f32_32x32x16_bf16 with fp32 accumulation.  The operand order
+//     puts every elementwise step (P, dS) in the accumulator layout and feeds
+//     it to the next product without a round trip through LDS.  Operands read
+//     along the sequence (Q^T, dO^T, K^T) come from the same row-major LDS
+//     tiles through ds_read_b64_tr_b16, in the order the accumulator holds P
+//     and dS.
+//   * the streamed tiles (and, for bwd_kv, the rows' (LSE, D) pairs) are
+//     copied HBM -> LDS by buffer loads that write LDS directly (rows past S
+//     arrive as zeros) into a ring of four stages, two steps ahead; each wave
+//     waits only for its own copies and passes a fence-free barrier.
 #include <math.h>
+
+#include <type_traits>
 
 #include "basp_device.hpp"
 #include "basp_internal.hpp"
@@ -32,37 +40,65 @@
 namespace basp {
 namespace {
 
-constexpr int kThreads = 256;
 constexpr float kLog2e = 1.4426950408889634f;
+constexpr int kPreThreads = 256;
+constexpr int kStages = 4;
+// Instruction classes of __builtin_amdgcn_sched_group_barrier.
+constexpr int kSchedMfma = 0x008;
+constexpr int kSchedDsRead = 0x100;
 
-// Row chunking of the key-stationary kernels: 1 chunk up to 2048 rows, 2 up
-// to 8192, else 4 (multiples of 64 rows), enough workgroups to balance the
-// causal triangle over the GPU.  Workspace: D, then (if chunked) the dV and dK
-// partial sums [chunk][b][S][H_kv/G][d].
+// Order the LDS operand reads of a run of MFMAs that each take R reads:
+// the first A reads up front, then one MFMA per R further reads.
+template <int NMFMA, int R, int A>
+__device__ __forceinline__ void sched_reads_ahead() {
+  __builtin_amdgcn_sched_group_barrier(kSchedDsRead, A, 0);
+#pragma unroll
+  for (int i = 0; i < NMFMA - A / R; ++i) {
+    __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(kSchedDsRead, R, 0);
+  }
+  __builtin_amdgcn_sched_group_barrier(kSchedMfma, A / R, 0);
+}
+
+// Workspace: LD [b][Hl][S] of (LSE * log2(e), D), then, when the key
+// passes are chunked, the dV and dK partial sums [chunk][b][S][H_kv/G][d].
+//
+// Work units of the key-stationary passes.  The rows a key tile needs,
+// [k0, S), are cut at multiples of kChunkRows; a unit is one (key tile, row
+// chunk) pair and writes its own partial sum (slice `chunk` of the partial
+// buffer), so no unit holds more than kChunkRows rows per query head.  Units
+// starting at their chunk's first row ("full") come first, chunk by chunk;
+// then the diagonal units (key tile inside its first chunk), longest first,
+// so the shortest work runs last.
+constexpr int kKvKeys = 256;       // keys per key-stationary workgroup
+constexpr int kChunkRows = 2048;   // multiple of kKvKeys
+constexpr int kTilesPerChunk = kChunkRows / kKvKeys;
+
 struct BwdChunks {
-  int n, rows;
+  int n;      // row chunks
+  int units;  // work units per (sequence, kv head)
   size_t part_offset_floats;
 };
 
 BwdChunks bwd_chunks(const AttnShape &s) {
   BwdChunks ck;
-  ck.n = s.S <= 2048 ? 1 : (s.S <= 8192 ? 2 : 4);
-  ck.rows = ((s.S + ck.n - 1) / ck.n + 63) / 64 * 64;
-  ck.n = (s.S + ck.rows - 1) / ck.rows;
+  ck.n = (s.S + kChunkRows - 1) / kChunkRows;
   if (ck.n < 1) ck.n = 1;
-  const size_t d_floats = (size_t)s.b * s.Hl * s.S;
-  ck.part_offset_floats = (d_floats + 63) & ~(size_t)63;  // 256-byte aligned
+  ck.units = kTilesPerChunk * ck.n * (ck.n - 1) / 2 + ck.n + ck.n * (kTilesPerChunk - 1);
+  const size_t ld_floats = 2 * (size_t)s.b * s.Hl * s.S;
+  ck.part_offset_floats = (ld_floats + 63) & ~(size_t)63;  // 256-byte aligned
   return ck;
 }
 
 // ---------------------------------------------------------------- bwd_pre
 // One group of D/8 lanes per (beta, row, head); 16-byte loads of O and dO.
 template <int D>
-__global__ __launch_bounds__(kThreads) void bwd_pre_kernel(
+__global__ __launch_bounds__(kPreThreads) void bwd_pre_kernel(
     const uint16_t *__restrict__ o, const uint16_t *__restrict__ d_o,
-    float *__restrict__ Dbuf, long long rows /* b*S*Hl */, int S, int Hl) {
+    const float *__restrict__ lse, f32x2 *__restrict__ ld, long long rows /* b*S*Hl */,
+    int S, int Hl) {
   constexpr int LPR = D / 8;  // lanes per row
-  const long long gid = (long long)blockIdx.x * kThreads + threadIdx.x;
+  const long long gid = (long long)blockIdx.x * kPreThreads + threadIdx.x;
   const long long r = gid / LPR;
   const int sub = (int)(gid % LPR);
   float acc = 0.f;
@@ -78,65 +114,76 @@ __global__ __launch_bounds__(kThreads) void bwd_pre_kernel(
 #pragma unroll
   for (int off = LPR / 2; off > 0; off >>= 1) acc += __shfl_xor(acc, off, 64);
   if (r < rows && sub == 0) {
-    // r = (beta*S + i)*Hl + h  ->  D[beta][h][i]
+    // r = (beta*S + i)*Hl + h  ->  LD[beta][h][i]
     const long long bi = r / Hl;
     const int h = (int)(r - bi * Hl);
     const long long beta = bi / S;
     const int i = (int)(bi - beta * S);
-    Dbuf[(beta * Hl + h) * S + i] = acc;
+    const size_t idx = (size_t)(beta * Hl + h) * S + i;
+    ld[idx] = f32x2{lse[idx] * kLog2e, acc};
   }
 }
 
-// ------------------------------------------------------ bwd_dv / bwd_dk
-// Key-stationary.  A workgroup of 4 waves owns 128 keys of one kv head (32
-// per wave) and sweeps every 64-row query tile at or after them, for all
-// query heads of the GQA group.  Two instances of one kernel:
-//   kDV: S = Q K^T, P = exp2(S c - LSE2),   dV^T += dO^T P
-//   kDK: S, dP = dO V^T, dS = P (dP - D),   dK^T += Q^T dS
-// Keeping dV and dK in separate launches recomputes S once more, but leaves
-// every wave independent (no exchange between waves, one barrier per step)
-// and small enough for two waves per SIMD.
-constexpr int kKN = 128;  // keys per workgroup (32 per wave)
-constexpr int kQM = 64;   // query rows per step (two 32-row halves)
+// ------------------------------------------------------ bwd_kv (dV / dK)
+// Key-stationary.  A workgroup of 8 waves owns 256 keys of one kv head (32
+// per wave) and sweeps 64-row query steps, for all query heads of the GQA
+// group.  Two instances of one kernel:
+//   kDV: S^T = K Q^T, P = exp2(S c - LSE2),   dV^T += dO^T P
+//   kDK: S^T, dP^T = V dO^T, dS = P (dP - D),   dK^T += Q^T dS
+// Keeping dV and dK in separate launches recomputes S once more, but keeps
+// each wave within two waves per SIMD of registers.
+constexpr int kKvWaves = 8;
+constexpr int kKvThreads = 64 * kKvWaves;
+constexpr int kKN = 32 * kKvWaves;  // keys per workgroup
+static_assert(kKN == kKvKeys, "work units assume 256 keys per workgroup");
+constexpr int kQM = 64;             // query rows per step (two 32-row halves)
 enum KvGrad { kDV = 0, kDK = 1 };
 
 template <int D>
 struct KvCfg {
   static constexpr int TILE_BYTES = kQM * D * 2;
-  // Q tile, dO tile, then 2 x kQM floats (LSE in log2 units, D).
-  static constexpr int STAGE_BYTES = 2 * TILE_BYTES + 2 * kQM * 4;
+  static constexpr int AUX_BYTES = 1024;  // (LSE2, D) of the step's rows (first 512 B)
+  static constexpr int STAGE_BYTES = 2 * TILE_BYTES + AUX_BYTES;  // Q, dO, aux
   static constexpr int NS = D / 16;
   static constexpr int NE = D / 32;
   static constexpr int CPR = D / 8;
-  static constexpr int CHUNKS = kQM * CPR / kThreads;
+  static constexpr int DMA_PER_WAVE = kQM * CPR / kKvThreads;  // 1 KB copies per tile
 };
 
 template <int D, int G>
-__global__ __launch_bounds__(kThreads, 2) void bwd_kv_kernel(
+__global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
     const uint16_t *__restrict__ q, const uint16_t *__restrict__ k,
     const uint16_t *__restrict__ v, const uint16_t *__restrict__ d_o,
-    const float *__restrict__ lse, const float *__restrict__ Dbuf,
-    float *__restrict__ out, int S, int Hl, int Hkl, int n_rep, int kvheads_total,
-    int ktiles, int chunk_rows, float c /* scale*log2e */, float out_scale) {
+    const f32x2 *__restrict__ ld, float *__restrict__ out, int S, int Hl, int Hkl,
+    int n_rep, int kvheads_total, int ktiles, int nchunks, float c /* scale*log2e */,
+    float out_scale) {
   using C = KvCfg<D>;
   using T = LdsTile<D>;
-  __shared__ __attribute__((aligned(16))) unsigned char smem[2 * C::STAGE_BYTES];
+  __shared__ __attribute__((aligned(16))) unsigned char smem[kStages * C::STAGE_BYTES];
 
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l32 = lane & 31, hh = lane >> 5;
-  // Work item: (row chunk ch, key tile kt, sequence x kv head hb).  The rows a
-  // key tile needs, [k0, S), are cut at multiples of chunk_rows; each chunk
-  // writes its own partial sum (slice ch of `out`), so long key tiles are
-  // spread over several workgroups.  Earlier key tiles come first within a
-  // chunk (they have more rows).
+  // Work unit (key tile kt, row chunk ch) of sequence x kv head hb; the
+  // order of units is described with kChunkRows.
   const int L = blockIdx.x;
   const int hb = L % kvheads_total;
-  const int kt = (L / kvheads_total) % ktiles;
-  const int ch = L / (kvheads_total * ktiles);
+  int u = L / kvheads_total, ch = 0, kt;
+  while (ch < nchunks && u >= ch * kTilesPerChunk + 1) {  // full units of chunk ch
+    u -= ch * kTilesPerChunk + 1;
+    ++ch;
+  }
+  if (ch < nchunks) {
+    kt = u;
+  } else {  // diagonal units, j-th key tile of its chunk
+    ch = u % nchunks;
+    kt = ch * kTilesPerChunk + u / nchunks + 1;
+  }
+  if (kt >= ktiles) return;  // workgroup-uniform
   const int beta = hb / Hkl, kvh = hb % Hkl;
   const int k0 = kt * kKN;
-  const int r_lo = max(k0, ch * chunk_rows), r_hi = min(S, (ch + 1) * chunk_rows);
-  if (r_lo >= r_hi) return;  // workgroup-uniform: this chunk lies before the keys
+  const int r_lo = max(k0, ch * kChunkRows), r_hi = min(S, (ch + 1) * kChunkRows);
+  if (r_lo >= r_hi) return;
   const int wk0 = k0 + 32 * w;
   const int key = wk0 + l32;
 
@@ -157,6 +204,7 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_kv_kernel(
         vf[s] = as_bf16x8(buf_load16(rv, (uint32_t)key * kv_row_bytes + (2 * s + hh) * 16));
     }
   }
+  wait_vmcnt<0>();  // retire the tracked loads before untracked copies start
 
   f32x16 acc[C::NE];
 #pragma unroll
@@ -166,135 +214,128 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_kv_kernel(
 
   const int steps_per_head = (r_hi - r_lo + kQM - 1) / kQM;
   const int nsteps = steps_per_head * n_rep;
+  const uint32_t smem_lds = lds_addr_of(smem);
 
-  uint32_t g_off[C::CHUNKS];
-  int s_off[C::CHUNKS];
+  uint32_t g_off[C::DMA_PER_WAVE];
 #pragma unroll
-  for (int r = 0; r < C::CHUNKS; ++r) {
-    const int cidx = tid + r * kThreads;
-    const int ir = cidx / C::CPR, cc = cidx % C::CPR;
-    g_off[r] = (uint32_t)ir * q_row_bytes + cc * 16;
-    s_off[r] = T::off(ir, cc);
-  }
-  // A of S and dP: row l32 (+32 for the second half), chunk 2s + hh.
+  for (int i = 0; i < C::DMA_PER_WAVE; ++i)
+    g_off[i] = dma_src_off<D>((w * C::DMA_PER_WAVE + i) * 64 + lane, q_row_bytes);
+  // A of S^T (Q) and dP^T (dO): row l32 (+32 for the second half), chunk 2s + hh.
   int a_off[C::NS];
 #pragma unroll
-  for (int s = 0; s < C::NS; ++s) a_off[s] = T::off(l32, 2 * s + hh);
+  for (int s = 0; s < C::NS; ++s) {
+    a_off[s] = T::off(l32, 2 * s + hh);
+    asm volatile("" : "+v"(a_off[s]));
+  }
   // Transposed A of dV^T / dK^T: rows 16*s2 + 4hh (+8), columns 32n + 16*((lane/16)&1).
   int t_off[C::NE][2];
 #pragma unroll
   for (int n = 0; n < C::NE; ++n)
 #pragma unroll
-    for (int x = 0; x < 2; ++x)
+    for (int x = 0; x < 2; ++x) {
       t_off[n][x] = tr_piece_off<D>(4 * hh + 8 * x, 32 * n + 16 * ((lane >> 4) & 1), lane);
+      asm volatile("" : "+v"(t_off[n][x]));
+    }
 
-  u32x4 qreg[C::CHUNKS], doreg[C::CHUNKS];
-  float aux = 0.f;  // LSE2 (tid < 64) or D (64 <= tid < 128) of one row
-
-  // Rows past r_hi (in the last step of a chunk that ends before S) are
-  // read as data but carry LSE = +inf, so their P is exactly zero.
-  auto step_coords = [&](int st, int &h, int &i0) {
+  auto step_coords = [&](int st, int &h, int &i0) __attribute__((always_inline)) {
     const int hr = st / steps_per_head;
     h = kvh * n_rep + hr;
     i0 = r_lo + (st - hr * steps_per_head) * kQM;
   };
-
-  auto load_step = [&](int st) {
+  // Copies of step st into stage st % kStages: Q and dO tiles (every wave its
+  // share), the rows' (LSE2, D) pairs (wave 0, 1 KB of which 512 B are used).
+  auto load_step = [&](int st) __attribute__((always_inline)) {
     int h, i0;
     step_coords(st, h, i0);
     const size_t hoff = ((size_t)beta * S * Hl + h) * D;
-    const rsrc_t rq = make_rsrc(q + hoff, (uint32_t)S * q_row_bytes);
-    const rsrc_t rd = make_rsrc(d_o + hoff, (uint32_t)S * q_row_bytes);
+    const u32x4 rq = make_rsrc_words(q + hoff, (uint32_t)S * q_row_bytes);
+    const u32x4 rd = make_rsrc_words(d_o + hoff, (uint32_t)S * q_row_bytes);
     const uint32_t base = (uint32_t)i0 * q_row_bytes;
+    const uint32_t stage = smem_lds + (st % kStages) * C::STAGE_BYTES;
 #pragma unroll
-    for (int r = 0; r < C::CHUNKS; ++r) {
-      qreg[r] = buf_load16(rq, base + g_off[r]);
-      doreg[r] = buf_load16(rd, base + g_off[r]);
+    for (int i = 0; i < C::DMA_PER_WAVE; ++i) {
+      const uint32_t lds = stage + (w * C::DMA_PER_WAVE + i) * 1024;
+      buf_load16_lds_async(rq, base + g_off[i], lds);
+      buf_load16_lds_async(rd, base + g_off[i], lds + C::TILE_BYTES);
     }
-    if (tid < 2 * kQM) {
-      const int i = i0 + (tid & (kQM - 1));
-      const size_t idx = ((size_t)beta * Hl + h) * S + i;
-      if (tid < kQM)
-        aux = i < r_hi ? lse[idx] * kLog2e : INFINITY;
-      else
-        aux = i < r_hi ? Dbuf[idx] : 0.f;
+    if (w == 0) {
+      const u32x4 ra = make_rsrc_words(ld + ((size_t)beta * Hl + h) * S, (uint32_t)S * 8);
+      buf_load16_lds_async(ra, (uint32_t)i0 * 8 + lane * 16, stage + 2 * C::TILE_BYTES);
+    }
+  };
+  // This wave's copies of step st landed, with `ahead` later steps in flight.
+  auto wait_step = [&](int ahead) __attribute__((always_inline)) {
+    constexpr int N = 2 * C::DMA_PER_WAVE;
+    if (w == 0) {
+      if (ahead >= 2) wait_vmcnt<2 * (N + 1)>();
+      else if (ahead == 1) wait_vmcnt<N + 1>();
+      else wait_vmcnt<0>();
+    } else {
+      if (ahead >= 2) wait_vmcnt<2 * N>();
+      else if (ahead == 1) wait_vmcnt<N>();
+      else wait_vmcnt<0>();
     }
   };
 
-  auto store_step = [&](int buf) {
-    unsigned char *Qs = smem + buf * C::STAGE_BYTES;
-    unsigned char *dOs = Qs + C::TILE_BYTES;
-    float *aux_s = reinterpret_cast<float *>(dOs + C::TILE_BYTES);
-#pragma unroll
-    for (int r = 0; r < C::CHUNKS; ++r) {
-      *reinterpret_cast<u32x4 *>(Qs + s_off[r]) = qreg[r];
-      *reinterpret_cast<u32x4 *>(dOs + s_off[r]) = doreg[r];
-    }
-    if (tid < 2 * kQM) aux_s[tid] = aux;
-  };
-
-  load_step(0);
-  store_step(0);
-  __syncthreads();
-
-  for (int st = 0; st < nsteps; ++st) {
-    if (st + 1 < nsteps) load_step(st + 1);
-    int h_unused, i0;
-    step_coords(st, h_unused, i0);
-    const unsigned char *Qs = smem + (st & 1) * C::STAGE_BYTES;
+  // One 64-row step.  MASK: some row of the step precedes one of this wave's
+  // keys (P = 0 there; 32-row halves entirely before the keys are skipped).
+  auto body = [&](int st, int i0, bool MASK) __attribute__((always_inline)) {
+    const unsigned char *Qs = smem + (st % kStages) * C::STAGE_BYTES;
     const unsigned char *dOs = Qs + C::TILE_BYTES;
-    const float *lse_s = reinterpret_cast<const float *>(dOs + C::TILE_BYTES);
-    const float *D_s = lse_s + kQM;
-    // The transposed operand of the accumulation: dO^T for dV, Q^T for dK.
-    const unsigned char *Ts = G == kDV ? dOs : Qs;
-
+    const float *aux = reinterpret_cast<const float *>(dOs + C::TILE_BYTES);
+    const unsigned char *Ts = G == kDV ? dOs : Qs;  // transposed operand of the accumulation
 #pragma unroll
     for (int m = 0; m < 2; ++m) {
-      if (i0 + 32 * m + 31 < wk0) continue;  // wave-uniform: half entirely above the keys
-      // sacc[r] holds row i0 + 32m + 8(r/4) + 4hh + r%4, key `key`.
+      if (MASK && i0 + 32 * m + 31 < wk0) continue;  // wave-uniform
+      // sacc[r]: row i0 + 32m + 8(r/4) + 4hh + r%4, key `key`.
       f32x16 sacc, pacc;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) sacc[r] = 0.f;
-      if constexpr (G == kDK) {
-#pragma unroll
-        for (int r = 0; r < 16; ++r) pacc[r] = 0.f;
+      {
+        const bf16x8 aq = *reinterpret_cast<const bf16x8 *>(Qs + a_off[0] + m * 32 * T::ROW_BYTES);
+        sacc = mfma32x32x16(aq, kf[0], f32x16{});
+        if constexpr (G == kDK) {
+          const bf16x8 ad = *reinterpret_cast<const bf16x8 *>(dOs + a_off[0] + m * 32 * T::ROW_BYTES);
+          pacc = mfma32x32x16(ad, vf[0], f32x16{});
+        }
       }
 #pragma unroll
-      for (int s = 0; s < C::NS; ++s) {
+      for (int s = 1; s < C::NS; ++s) {
         const bf16x8 aq = *reinterpret_cast<const bf16x8 *>(Qs + a_off[s] + m * 32 * T::ROW_BYTES);
         sacc = mfma32x32x16(aq, kf[s], sacc);
         if constexpr (G == kDK) {
-          const bf16x8 ad =
-              *reinterpret_cast<const bf16x8 *>(dOs + a_off[s] + m * 32 * T::ROW_BYTES);
+          const bf16x8 ad = *reinterpret_cast<const bf16x8 *>(dOs + a_off[s] + m * 32 * T::ROW_BYTES);
           pacc = mfma32x32x16(ad, vf[s], pacc);
         }
       }
-      // P (masked on the diagonal), then dS for dK.
-      if (i0 + 32 * m < wk0 + 31) {
+      sched_reads_ahead<(G == kDK ? 2 : 1) * C::NS, 1, (G == kDK ? 4 : 2)>();
+      // Row 32m + 8g + 4hh + x of the step holds (LSE2, D) at aux[2 * row].
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const f32x4 l4 = *reinterpret_cast<const f32x4 *>(lse_s + 32 * m + 8 * g + 4 * hh);
+      for (int g = 0; g < 4; ++g) {
+        const int rr = 32 * m + 8 * g + 4 * hh;
 #pragma unroll
-          for (int x = 0; x < 4; ++x) {
-            const int r = 4 * g + x;
-            const float p = fast_exp2(fmaf(sacc[r], c, -l4[x]));
-            sacc[r] = key > i0 + 32 * m + 8 * g + 4 * hh + x ? 0.f : p;
+        for (int x2 = 0; x2 < 2; ++x2) {
+          const f32x4 a = *reinterpret_cast<const f32x4 *>(aux + 2 * rr + 4 * x2);
+#pragma unroll
+          for (int y = 0; y < 2; ++y) {
+            const int x = 2 * x2 + y, r = 4 * g + x;
+            float p = fast_exp2(fmaf(sacc[r], c, -a[2 * y]));
+            if (MASK && key > i0 + rr + x) p = 0.f;
+            sacc[r] = p;
           }
-        }
-      } else {
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const f32x4 l4 = *reinterpret_cast<const f32x4 *>(lse_s + 32 * m + 8 * g + 4 * hh);
-#pragma unroll
-          for (int x = 0; x < 4; ++x) sacc[4 * g + x] = fast_exp2(fmaf(sacc[4 * g + x], c, -l4[x]));
         }
       }
       if constexpr (G == kDK) {
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
-          const f32x4 d4 = *reinterpret_cast<const f32x4 *>(D_s + 32 * m + 8 * g + 4 * hh);
+          const int rr = 32 * m + 8 * g + 4 * hh;
 #pragma unroll
-          for (int x = 0; x < 4; ++x) sacc[4 * g + x] *= pacc[4 * g + x] - d4[x];
+          for (int x2 = 0; x2 < 2; ++x2) {
+            const f32x4 a = *reinterpret_cast<const f32x4 *>(aux + 2 * rr + 4 * x2);
+#pragma unroll
+            for (int y = 0; y < 2; ++y) {
+              const int r = 4 * g + 2 * x2 + y;
+              sacc[r] *= pacc[r] - a[2 * y + 1];
+            }
+          }
         }
       }
       // P or dS as the B operand along the rows: block s2 covers rows
@@ -307,8 +348,7 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_kv_kernel(
                     pack_bf16x2(sacc[b8 + 4], sacc[b8 + 5]), pack_bf16x2(sacc[b8 + 6], sacc[b8 + 7])};
         b[s2] = as_bf16x8(t4);
       }
-      // dV^T += dO^T P  or  dK^T += Q^T dS: M = head dim, N = keys, K = rows;
-      // the transposed A operand comes straight from the row-major tile.
+      // dV^T += dO^T P  or  dK^T += Q^T dS: M = head dim, N = keys, K = rows.
 #pragma unroll
       for (int n = 0; n < C::NE; ++n)
 #pragma unroll
@@ -317,9 +357,22 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_kv_kernel(
           const bf16x8 a = tr_operand(Ts, t_off[n][0] + ro, t_off[n][1] + ro);
           acc[n] = mfma32x32x16(a, b[s2], acc[n]);
         }
+      sched_reads_ahead<2 * C::NE, 2, 4>();
+      __builtin_amdgcn_sched_barrier(0);  // keep the two halves apart (register pressure)
     }
-    if (st + 1 < nsteps) store_step((st + 1) & 1);
-    __syncthreads();
+  };
+
+  for (int st = 0; st < 2 && st < nsteps; ++st) load_step(st);
+  for (int st = 0; st < nsteps; ++st) {
+    // Stage (st+2) % 4 last held step st-2, finished by every wave before
+    // the barrier of step st-1.
+    if (st + 2 < nsteps) load_step(st + 2);
+    wait_step(min(2, nsteps - 1 - st));
+    barrier_no_fence();
+    int h_unused, i0;
+    step_coords(st, h_unused, i0);
+    if (i0 + kQM - 1 < wk0) continue;          // wave-uniform: all rows before the keys
+    body(st, i0, i0 < wk0 + 31);  // mask when rows and keys overlap
   }
 
   // acc[n][r] = (dV or dK)^T[e = 32n + 8(r/4) + 4hh + r%4][key]
@@ -340,14 +393,14 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_kv_kernel(
 // dK or dV of a key = the sum of the partial sums of the row chunks that
 // exist for its key tile, added in chunk order (deterministic).  One thread
 // per 4 consecutive elements.
-__global__ __launch_bounds__(kThreads) void bwd_reduce_kernel(
+__global__ __launch_bounds__(kPreThreads) void bwd_reduce_kernel(
     const float *__restrict__ part, float *__restrict__ out, long long n4 /* b*S*Hkl*D/4 */,
-    int S, int row_elems /* Hkl*D */, int nchunks, int chunk_rows) {
-  const long long i4 = (long long)blockIdx.x * kThreads + threadIdx.x;
+    int S, int row_elems /* Hkl*D */, int nchunks) {
+  const long long i4 = (long long)blockIdx.x * kPreThreads + threadIdx.x;
   if (i4 >= n4) return;
   const long long e = i4 * 4;
   const int key = (int)((e / row_elems) % S);
-  const int first = (key / kKN) * kKN / chunk_rows;  // first chunk the key tile wrote
+  const int first = (key / kKN) / kTilesPerChunk;  // first chunk the key tile wrote
   const long long slice = n4 * 4;
   f32x4 acc = *reinterpret_cast<const f32x4 *>(part + (size_t)first * slice + e);
   for (int ch = first + 1; ch < nchunks; ++ch) {
@@ -361,8 +414,10 @@ __global__ __launch_bounds__(kThreads) void bwd_reduce_kernel(
 }
 
 // ---------------------------------------------------------------- bwd_dq
-constexpr int kDQM = 128;  // query rows per workgroup (32 per wave)
-constexpr int kDQN = 64;   // keys per tile
+constexpr int kDqWaves = 8;
+constexpr int kDqThreads = 64 * kDqWaves;
+constexpr int kDQM = 32 * kDqWaves;  // query rows per workgroup (32 per wave)
+constexpr int kDQN = 64;             // keys per tile
 
 template <int D>
 struct DqCfg {
@@ -371,21 +426,21 @@ struct DqCfg {
   static constexpr int NS = D / 16;
   static constexpr int NE = D / 32;
   static constexpr int CPR = D / 8;
-  static constexpr int CHUNKS = kDQN * CPR / kThreads;
+  static constexpr int DMA_PER_WAVE = kDQN * CPR / kDqThreads;
 };
 
 template <int D>
-__global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(
+__global__ __launch_bounds__(kDqThreads, 1) void bwd_dq_kernel(
     const uint16_t *__restrict__ q, const uint16_t *__restrict__ k,
     const uint16_t *__restrict__ v, const uint16_t *__restrict__ d_o,
-    const float *__restrict__ lse, const float *__restrict__ Dbuf,
-    float *__restrict__ dq, int S, int Hl, int Hkl, int n_rep, int heads_total,
-    int qtiles, float c, float scale) {
+    const f32x2 *__restrict__ ld, float *__restrict__ dq, int S, int Hl, int Hkl, int n_rep,
+    int heads_total, int qtiles, float c, float scale) {
   using C = DqCfg<D>;
   using T = LdsTile<D>;
-  __shared__ __attribute__((aligned(16))) unsigned char smem[2 * C::STAGE_BYTES];
+  __shared__ __attribute__((aligned(16))) unsigned char smem[kStages * C::STAGE_BYTES];
 
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l32 = lane & 31, hh = lane >> 5;
   const int L = blockIdx.x;
   const int qt = qtiles - 1 - L / heads_total;
@@ -399,8 +454,9 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(
   const size_t hoff = ((size_t)beta * S * Hl + h) * D;
   const rsrc_t rq = make_rsrc(q + hoff, (uint32_t)S * q_row_bytes);
   const rsrc_t rd = make_rsrc(d_o + hoff, (uint32_t)S * q_row_bytes);
-  const rsrc_t rk = make_rsrc(k + ((size_t)beta * S * Hkl + kvh) * D, (uint32_t)S * kv_row_bytes);
-  const rsrc_t rv = make_rsrc(v + ((size_t)beta * S * Hkl + kvh) * D, (uint32_t)S * kv_row_bytes);
+  const u32x4 rk = make_rsrc_words(k + ((size_t)beta * S * Hkl + kvh) * D, (uint32_t)S * kv_row_bytes);
+  const u32x4 rv = make_rsrc_words(v + ((size_t)beta * S * Hkl + kvh) * D, (uint32_t)S * kv_row_bytes);
+  const uint32_t smem_lds = lds_addr_of(smem);
 
   bf16x8 qf[C::NS], df[C::NS];
 #pragma unroll
@@ -408,52 +464,49 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(
     qf[s] = as_bf16x8(buf_load16(rq, (uint32_t)row * q_row_bytes + (2 * s + hh) * 16));
     df[s] = as_bf16x8(buf_load16(rd, (uint32_t)row * q_row_bytes + (2 * s + hh) * 16));
   }
-  const size_t lidx = ((size_t)beta * Hl + h) * S + row;
-  const float lse2 = row < S ? lse[lidx] * kLog2e : INFINITY;
-  const float Drow = row < S ? Dbuf[lidx] : 0.f;
+  f32x2 ldr = {INFINITY, 0.f};  // rows past S: P = 0
+  if (row < S) ldr = ld[((size_t)beta * Hl + h) * S + row];
+  const float lse2 = ldr[0], Drow = ldr[1];
+  wait_vmcnt<0>();  // retire the tracked loads before untracked copies start
 
   const int kv_end = min(S, q0 + kDQM);
   const int nt = (kv_end + kDQN - 1) / kDQN;
 
-  uint32_t g_off[C::CHUNKS];
-  int s_off[C::CHUNKS];
+  uint32_t g_off[C::DMA_PER_WAVE];
 #pragma unroll
-  for (int r = 0; r < C::CHUNKS; ++r) {
-    const int cidx = tid + r * kThreads;
-    const int jr = cidx / C::CPR, cc = cidx % C::CPR;
-    g_off[r] = (uint32_t)jr * kv_row_bytes + cc * 16;
-    s_off[r] = T::off(jr, cc);
-  }
+  for (int i = 0; i < C::DMA_PER_WAVE; ++i)
+    g_off[i] = dma_src_off<D>((w * C::DMA_PER_WAVE + i) * 64 + lane, kv_row_bytes);
+  auto load_tile = [&](int t) __attribute__((always_inline)) {
+    const uint32_t ks = smem_lds + (t % kStages) * C::STAGE_BYTES;
+    const uint32_t base = (uint32_t)(t * kDQN) * kv_row_bytes;
+#pragma unroll
+    for (int i = 0; i < C::DMA_PER_WAVE; ++i) {
+      const uint32_t lds = ks + (w * C::DMA_PER_WAVE + i) * 1024;
+      buf_load16_lds_async(rk, base + g_off[i], lds);
+      buf_load16_lds_async(rv, base + g_off[i], lds + C::TILE_BYTES);
+    }
+  };
+  auto wait_tile = [&](int ahead) __attribute__((always_inline)) {
+    if (ahead >= 2) wait_vmcnt<4 * C::DMA_PER_WAVE>();
+    else if (ahead == 1) wait_vmcnt<2 * C::DMA_PER_WAVE>();
+    else wait_vmcnt<0>();
+  };
+
   int a_off[C::NS];  // row l32 (+32 for m = 1), chunk 2s + hh
 #pragma unroll
-  for (int s = 0; s < C::NS; ++s) a_off[s] = T::off(l32, 2 * s + hh);
-  // Transposed A operand: rows 16*s2 + 4hh (+8), columns 32n + 16*((lane/16)&1);
-  // row block s2 sits 16*s2 rows further on (same swizzle).
+  for (int s = 0; s < C::NS; ++s) {
+    a_off[s] = T::off(l32, 2 * s + hh);
+    asm volatile("" : "+v"(a_off[s]));
+  }
+  // Transposed A operand: rows 16*s2 + 4hh (+8), columns 32n + 16*((lane/16)&1).
   int t_off[C::NE][2];
 #pragma unroll
   for (int n = 0; n < C::NE; ++n)
 #pragma unroll
-    for (int x = 0; x < 2; ++x)
+    for (int x = 0; x < 2; ++x) {
       t_off[n][x] = tr_piece_off<D>(4 * hh + 8 * x, 32 * n + 16 * ((lane >> 4) & 1), lane);
-
-  u32x4 kreg[C::CHUNKS], vreg[C::CHUNKS];
-  auto load_tile = [&](int t) {
-    const uint32_t base = (uint32_t)(t * kDQN) * kv_row_bytes;
-#pragma unroll
-    for (int r = 0; r < C::CHUNKS; ++r) {
-      kreg[r] = buf_load16(rk, base + g_off[r]);
-      vreg[r] = buf_load16(rv, base + g_off[r]);
+      asm volatile("" : "+v"(t_off[n][x]));
     }
-  };
-  auto store_tile = [&](int buf) {
-    unsigned char *Ks = smem + buf * C::STAGE_BYTES;
-    unsigned char *Vs = Ks + C::TILE_BYTES;
-#pragma unroll
-    for (int r = 0; r < C::CHUNKS; ++r) {
-      *reinterpret_cast<u32x4 *>(Ks + s_off[r]) = kreg[r];
-      *reinterpret_cast<u32x4 *>(Vs + s_off[r]) = vreg[r];
-    }
-  };
 
   f32x16 qacc[C::NE];
 #pragma unroll
@@ -461,66 +514,79 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(
 #pragma unroll
     for (int r = 0; r < 16; ++r) qacc[n][r] = 0.f;
 
-  load_tile(0);
-  store_tile(0);
-  __syncthreads();
-
-  for (int t = 0; t < nt; ++t) {
-    if (t + 1 < nt) load_tile(t + 1);
+  // One 64-key tile in two 32-key halves (keeps the score state at 2 x 16
+  // registers).  S^T = K Q^T and dP^T = V dO^T: M = 32 keys, N = this wave's
+  // rows; sacc[r] holds key j0 + 32m + 8(r/4) + 4hh + r%4, query row `row`.
+  auto tile = [&](int t, auto mask_tag) __attribute__((always_inline)) {
+    constexpr bool MASK = decltype(mask_tag)::value;
     const int j0 = t * kDQN;
-    if (j0 <= wrow0 + 31) {
-      const unsigned char *Ks = smem + (t & 1) * C::STAGE_BYTES;
-      const unsigned char *Vs = Ks + C::TILE_BYTES;
-      // Two halves of 32 keys each (keeps the score state at 2 x 16 registers).
-      // S^T = K Q^T and dP^T = V dO^T: M = 32 keys, N = this wave's rows;
-      // acc[r] holds key j0 + 32m + 8(r/4) + 4hh + r%4, query row `row`.
+    const unsigned char *Ks = smem + (t % kStages) * C::STAGE_BYTES;
+    const unsigned char *Vs = Ks + C::TILE_BYTES;
 #pragma unroll
-      for (int m = 0; m < 2; ++m) {
-        if (j0 + 32 * m > wrow0 + 31) continue;  // wave-uniform: half entirely masked
-        f32x16 sacc, pacc;
+    for (int m = 0; m < 2; ++m) {
+      if (MASK && j0 + 32 * m > wrow0 + 31) continue;  // wave-uniform: half entirely masked
+      f32x16 sacc, pacc;
+      {
+        const bf16x8 ak = *reinterpret_cast<const bf16x8 *>(Ks + a_off[0] + m * 32 * T::ROW_BYTES);
+        const bf16x8 av = *reinterpret_cast<const bf16x8 *>(Vs + a_off[0] + m * 32 * T::ROW_BYTES);
+        sacc = mfma32x32x16(ak, qf[0], f32x16{});
+        pacc = mfma32x32x16(av, df[0], f32x16{});
+      }
 #pragma unroll
-        for (int r = 0; r < 16; ++r) sacc[r] = pacc[r] = 0.f;
+      for (int s = 1; s < C::NS; ++s) {
+        const bf16x8 ak = *reinterpret_cast<const bf16x8 *>(Ks + a_off[s] + m * 32 * T::ROW_BYTES);
+        const bf16x8 av = *reinterpret_cast<const bf16x8 *>(Vs + a_off[s] + m * 32 * T::ROW_BYTES);
+        sacc = mfma32x32x16(ak, qf[s], sacc);
+        pacc = mfma32x32x16(av, df[s], pacc);
+      }
+      sched_reads_ahead<2 * C::NS, 1, 4>();
 #pragma unroll
-        for (int s = 0; s < C::NS; ++s) {
-          const bf16x8 ak =
-              *reinterpret_cast<const bf16x8 *>(Ks + a_off[s] + m * 32 * T::ROW_BYTES);
-          const bf16x8 av =
-              *reinterpret_cast<const bf16x8 *>(Vs + a_off[s] + m * 32 * T::ROW_BYTES);
-          sacc = mfma32x32x16(ak, qf[s], sacc);
-          pacc = mfma32x32x16(av, df[s], pacc);
+      for (int r = 0; r < 16; ++r) {
+        float p = fast_exp2(fmaf(sacc[r], c, -lse2));
+        if constexpr (MASK) {
+          const int j = j0 + 32 * m + 8 * (r >> 2) + 4 * hh + (r & 3);
+          if (j > row) p = 0.f;
         }
-        const bool diag = j0 + 32 * m + 31 > wrow0;
+        pacc[r] = p * (pacc[r] - Drow);
+      }
+      bf16x8 sb[2];
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          float p = fast_exp2(fmaf(sacc[r], c, -lse2));
-          if (diag) {
-            const int j = j0 + 32 * m + 8 * (r >> 2) + 4 * hh + (r & 3);
-            if (j > row) p = 0.f;
-          }
-          pacc[r] = p * (pacc[r] - Drow);
-        }
-        bf16x8 sb[2];
+      for (int s2 = 0; s2 < 2; ++s2) {
+        const int b8 = 8 * s2;
+        u32x4 ts = {pack_bf16x2(pacc[b8 + 0], pacc[b8 + 1]), pack_bf16x2(pacc[b8 + 2], pacc[b8 + 3]),
+                    pack_bf16x2(pacc[b8 + 4], pacc[b8 + 5]), pack_bf16x2(pacc[b8 + 6], pacc[b8 + 7])};
+        sb[s2] = as_bf16x8(ts);
+      }
+      // dQ^T += K^T dS^T: M = head dim, N = rows, K = keys; K^T straight
+      // from the row-major K tile.
+#pragma unroll
+      for (int n = 0; n < C::NE; ++n)
 #pragma unroll
         for (int s2 = 0; s2 < 2; ++s2) {
-          const int b8 = 8 * s2;
-          u32x4 ts = {pack_bf16x2(pacc[b8 + 0], pacc[b8 + 1]), pack_bf16x2(pacc[b8 + 2], pacc[b8 + 3]),
-                      pack_bf16x2(pacc[b8 + 4], pacc[b8 + 5]), pack_bf16x2(pacc[b8 + 6], pacc[b8 + 7])};
-          sb[s2] = as_bf16x8(ts);
+          const int ro = (2 * m + s2) * 16 * T::ROW_BYTES;
+          const bf16x8 a = tr_operand(Ks, t_off[n][0] + ro, t_off[n][1] + ro);
+          qacc[n] = mfma32x32x16(a, sb[s2], qacc[n]);
         }
-        // dQ^T += K^T dS^T: M = head dim, N = rows, K = keys; K^T straight
-        // from the row-major K tile.
-#pragma unroll
-        for (int n = 0; n < C::NE; ++n)
-#pragma unroll
-          for (int s2 = 0; s2 < 2; ++s2) {
-            const int ro = (2 * m + s2) * 16 * T::ROW_BYTES;
-            const bf16x8 a = tr_operand(Ks, t_off[n][0] + ro, t_off[n][1] + ro);
-            qacc[n] = mfma32x32x16(a, sb[s2], qacc[n]);
-          }
-      }
+      sched_reads_ahead<2 * C::NE, 2, 4>();
+      __builtin_amdgcn_sched_barrier(0);  // keep the two halves apart (register pressure)
     }
-    if (t + 1 < nt) store_tile((t + 1) & 1);
-    __syncthreads();
+  };
+  auto step = [&](int t) __attribute__((always_inline)) {
+    // Stage (t+2) % 4 last held tile t-2, finished by every wave before the
+    // barrier of iteration t-1.
+    if (t + 2 < nt) load_tile(t + 2);
+    wait_tile(min(2, nt - 1 - t));
+    barrier_no_fence();
+  };
+  for (int t = 0; t < 2 && t < nt; ++t) load_tile(t);
+  const int t_mask = min(nt, q0 / kDQN);  // tiles before t_mask need no mask
+  for (int t = 0; t < t_mask; ++t) {
+    step(t);
+    tile(t, std::false_type{});
+  }
+  for (int t = t_mask; t < nt; ++t) {
+    step(t);
+    if (t * kDQN <= wrow0 + 31) tile(t, std::true_type{});  // wave-uniform
   }
 
   if (row < S) {
@@ -539,50 +605,51 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(
 template <int D>
 hipError_t launch_bwd_d(const void *q, const void *k, const void *v, const void *o,
                         const float *lse, const void *d_o, float *dq, float *dk,
-                        float *dv, float *Dbuf, const AttnShape &s, hipStream_t stream) {
+                        float *dv, float *ws, const AttnShape &s, hipStream_t stream) {
   auto *qp = static_cast<const uint16_t *>(q);
   auto *kp = static_cast<const uint16_t *>(k);
   auto *vp = static_cast<const uint16_t *>(v);
   auto *op = static_cast<const uint16_t *>(o);
   auto *dop = static_cast<const uint16_t *>(d_o);
+  auto *ld = reinterpret_cast<f32x2 *>(ws);
   const float c = s.scale * kLog2e;
   const int n_rep = s.Hl / s.Hkl;
 
   const long long rows = (long long)s.b * s.S * s.Hl;
   const long long pre_threads = rows * (D / 8);
-  const long long pre_blocks = (pre_threads + kThreads - 1) / kThreads;
-  hipLaunchKernelGGL(bwd_pre_kernel<D>, dim3((unsigned)pre_blocks), dim3(kThreads), 0, stream,
-                     op, dop, Dbuf, rows, s.S, s.Hl);
+  const long long pre_blocks = (pre_threads + kPreThreads - 1) / kPreThreads;
+  hipLaunchKernelGGL(bwd_pre_kernel<D>, dim3((unsigned)pre_blocks), dim3(kPreThreads), 0, stream,
+                     op, dop, lse, ld, rows, s.S, s.Hl);
 
   const int ktiles = (s.S + kKN - 1) / kKN;
   const int kvheads_total = s.b * s.Hkl;
   const BwdChunks ck = bwd_chunks(s);
-  const dim3 kv_grid((unsigned)(ck.n * ktiles * kvheads_total));
+  const dim3 kv_grid((unsigned)(ck.units * kvheads_total));
   float *dv_out = dv, *dk_out = dk;
   if (ck.n > 1) {  // partial sums in the workspace, reduced below
-    dv_out = Dbuf + ck.part_offset_floats;
+    dv_out = ws + ck.part_offset_floats;
     dk_out = dv_out + (size_t)ck.n * kvheads_total * s.S * D;
   }
-  hipLaunchKernelGGL((bwd_kv_kernel<D, kDV>), kv_grid, dim3(kThreads), 0, stream, qp, kp, vp,
-                     dop, lse, Dbuf, dv_out, s.S, s.Hl, s.Hkl, n_rep, kvheads_total, ktiles,
-                     ck.rows, c, 1.f);
-  hipLaunchKernelGGL((bwd_kv_kernel<D, kDK>), kv_grid, dim3(kThreads), 0, stream, qp, kp, vp,
-                     dop, lse, Dbuf, dk_out, s.S, s.Hl, s.Hkl, n_rep, kvheads_total, ktiles,
-                     ck.rows, c, s.scale);
+  hipLaunchKernelGGL((bwd_kv_kernel<D, kDV>), kv_grid, dim3(kKvThreads), 0, stream, qp, kp, vp,
+                     dop, ld, dv_out, s.S, s.Hl, s.Hkl, n_rep, kvheads_total, ktiles, ck.n, c,
+                     1.f);
+  hipLaunchKernelGGL((bwd_kv_kernel<D, kDK>), kv_grid, dim3(kKvThreads), 0, stream, qp, kp, vp,
+                     dop, ld, dk_out, s.S, s.Hl, s.Hkl, n_rep, kvheads_total, ktiles, ck.n, c,
+                     s.scale);
   if (ck.n > 1) {
     const long long n4 = (long long)kvheads_total * s.S * D / 4;
-    const dim3 rg((unsigned)((n4 + kThreads - 1) / kThreads));
-    hipLaunchKernelGGL(bwd_reduce_kernel, rg, dim3(kThreads), 0, stream, dv_out, dv, n4, s.S,
-                       s.Hkl * D, ck.n, ck.rows);
-    hipLaunchKernelGGL(bwd_reduce_kernel, rg, dim3(kThreads), 0, stream, dk_out, dk, n4, s.S,
-                       s.Hkl * D, ck.n, ck.rows);
+    const dim3 rg((unsigned)((n4 + kPreThreads - 1) / kPreThreads));
+    hipLaunchKernelGGL(bwd_reduce_kernel, rg, dim3(kPreThreads), 0, stream, dv_out, dv, n4, s.S,
+                       s.Hkl * D, ck.n);
+    hipLaunchKernelGGL(bwd_reduce_kernel, rg, dim3(kPreThreads), 0, stream, dk_out, dk, n4, s.S,
+                       s.Hkl * D, ck.n);
   }
 
   const int qtiles = (s.S + kDQM - 1) / kDQM;
   const int heads_total = s.b * s.Hl;
-  hipLaunchKernelGGL(bwd_dq_kernel<D>, dim3((unsigned)(qtiles * heads_total)), dim3(kThreads),
-                     0, stream, qp, kp, vp, dop, lse, Dbuf, dq, s.S, s.Hl, s.Hkl, n_rep,
-                     heads_total, qtiles, c, s.scale);
+  hipLaunchKernelGGL(bwd_dq_kernel<D>, dim3((unsigned)(qtiles * heads_total)), dim3(kDqThreads),
+                     0, stream, qp, kp, vp, dop, ld, dq, s.S, s.Hl, s.Hkl, n_rep, heads_total,
+                     qtiles, c, s.scale);
   return hipGetLastError();
 }
 
@@ -600,10 +667,10 @@ hipError_t launch_attn_bwd(const void *q, const void *k, const void *v,
                            float *dq, float *dk, float *dv, void *workspace,
                            const AttnShape &s, hipStream_t stream) {
   if ((long long)s.b * s.S == 0) return hipSuccess;
-  float *Dbuf = static_cast<float *>(workspace);
+  float *ws = static_cast<float *>(workspace);
   if (s.d == 128)
-    return launch_bwd_d<128>(q, k, v, o, lse, d_o, dq, dk, dv, Dbuf, s, stream);
-  return launch_bwd_d<64>(q, k, v, o, lse, d_o, dq, dk, dv, Dbuf, s, stream);
+    return launch_bwd_d<128>(q, k, v, o, lse, d_o, dq, dk, dv, ws, s, stream);
+  return launch_bwd_d<64>(q, k, v, o, lse, d_o, dq, dk, dv, ws, s, stream);
 }
 
 }  // namespace basp

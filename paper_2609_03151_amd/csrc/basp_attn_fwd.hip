@@ -77,7 +77,8 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
   using T = LdsTile<D>;
   __shared__ __attribute__((aligned(16))) unsigned char smem[kStages * C::STAGE_BYTES];
 
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave index, held in an SGPR
   const int l32 = lane & 31, hh = lane >> 5;
 
   const int L = blockIdx.x;
@@ -92,7 +93,6 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
   const rsrc_t rq = make_rsrc(q + ((size_t)beta * S * Hl + h) * D, (uint32_t)S * q_row_bytes);
   const u32x4 rk = make_rsrc_words(k + ((size_t)beta * S * Hkl + kvh) * D, (uint32_t)S * kv_row_bytes);
   const u32x4 rv = make_rsrc_words(v + ((size_t)beta * S * Hkl + kvh) * D, (uint32_t)S * kv_row_bytes);
-  const int wu = __builtin_amdgcn_readfirstlane(w);
   const uint32_t smem_lds = lds_addr_of(smem);
 
   // Q fragments (B operand of S^T = K Q^T): row `row`, e = 16s + 8hh .. +7.
@@ -117,7 +117,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
     const uint32_t base = (uint32_t)(t * kBN) * kv_row_bytes;
 #pragma unroll
     for (int i = 0; i < C::DMA_PER_WAVE; ++i) {
-      const uint32_t lds_off = ks + (wu * C::DMA_PER_WAVE + i) * 1024;
+      const uint32_t lds_off = ks + (w * C::DMA_PER_WAVE + i) * 1024;
       buf_load16_lds_async(rk, base + g_off[i], lds_off);
       buf_load16_lds_async(rv, base + g_off[i], lds_off + C::TILE_BYTES);
     }

@@ -72,13 +72,13 @@ __device__ __forceinline__ u32x4 buf_load16(rsrc_t r, uint32_t off) {
 // every copy in flight has landed (which would drain a prefetch ring) nor
 // orders anything against it.  The caller waits (vmcnt) for its own copies
 // and passes a barrier before any wave reads the data.  `rsrc` and
-// `lds_addr` (an LDS byte address) must be wave-uniform.  One wait state
-// separates the M0 write from the load.
+// `lds_addr` (an LDS byte address, passed in M0) must be wave-uniform.  One
+// wait state separates the compiler's M0 write from the load.
 __device__ __forceinline__ void buf_load16_lds_async(u32x4 rsrc, uint32_t off, uint32_t lds_addr) {
-  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds"
+  asm volatile("s_nop 0\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds"
                :
-               : "v"(off), "s"(rsrc), "s"(lds_addr)
-               : "memory", "m0");
+               : "v"(off), "s"(rsrc), "{m0}"(lds_addr)
+               : "memory");
 }
 
 // Raw buffer descriptor as four dwords (same fields make_rsrc sets): base
