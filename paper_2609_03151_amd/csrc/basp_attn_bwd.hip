@@ -316,12 +316,17 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
           const f32x4 a = *reinterpret_cast<const f32x4 *>(aux + 2 * rr + 4 * x2);
 #pragma unroll
           for (int y = 0; y < 2; ++y) {
-            const int x = 2 * x2 + y, r = 4 * g + x;
-            float p = fast_exp2(fmaf(sacc[r], c, -a[2 * y]));
-            if (MASK && key > i0 + rr + x) p = 0.f;
-            sacc[r] = p;
+            const int r = 4 * g + 2 * x2 + y;
+            sacc[r] = fast_exp2(fmaf(sacc[r], c, -a[2 * y]));
           }
         }
+      }
+      if (MASK) {  // wave-uniform; a real branch, taken on diagonal steps only
+        asm volatile("" ::: "memory");
+        const int lim = key - i0 - 32 * m - 4 * hh;  // row offset in the half must be >= lim
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          if (8 * (r >> 2) + (r & 3) < lim) sacc[r] = 0.f;
       }
       if constexpr (G == kDK) {
 #pragma unroll
