@@ -6,7 +6,9 @@ already resident in HBM:
   pack(dO) -> attention bwd -> unpack(dQ, dK, dV)
 The reported value is attention FLOPs (fwd + bwd, causal half of S^2,
 bwd = 2.5 x fwd) divided by the whole step's time, in TFLOP/s; the pack and
-unpack permutations are inside the step and also reported as GB/s.
+unpack permutations are inside the step and also reported as GB/s, both as
+timed in the step and with cold caches (each call alone after a 1 GiB
+scratch write), next to a plain device copy under the same conditions.
 
 Prints one JSON line.  With --gpus N > 1 it exits: this build runs one rank's
 share on one GPU (the exchange between ranks is not part of it).
@@ -97,6 +99,44 @@ def cpu_baseline(w, target_s: float):
             "sample": f"fp64 oracle fwd+bwd, sequence 0, all {w.Hl} local heads, first {Sp} "
                       f"of {w.S} tokens ({secs:.1f} s)",
             "seconds": secs}
+
+
+def cold_permutation_rates(sh, reps: int = 5):
+    """Each pack/unpack call timed alone with cold caches: a 1 GiB scratch
+    write (larger than L2 and the 256 MB MALL) precedes every timed call; the
+    median of `reps` runs per call.  Also a plain device-to-device copy of
+    the largest permutation's size under the same conditions, as the
+    achievable HBM rate."""
+    import statistics
+    import torch
+    scratch = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+
+    def cold(fn):
+        ts = []
+        for _ in range(reps):
+            scratch.fill_(1.0)
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        return statistics.median(ts)
+
+    calls = sh.permutation_calls()
+    per = {name: (cold(fn), nbytes) for name, fn, nbytes in calls}
+    total_ms = sum(t for t, _ in per.values())
+    total_bytes = sum(b for _, b in per.values())
+    biggest = max(b for _, b in per.values()) // 2
+    src = torch.empty(biggest // 4, dtype=torch.float32, device="cuda").fill_(2.0)
+    dst = torch.empty_like(src)
+    copy_ms = cold(lambda: dst.copy_(src))
+    del scratch, src, dst
+    return {
+        "pack_unpack_cold_gbps": round(total_bytes / (total_ms * 1e-3) / 1e9, 1),
+        "pack_unpack_cold_gbps_by_call": {n: round(b / (t * 1e-3) / 1e9, 1) for n, (t, b) in per.items()},
+        "hbm_copy_cold_gbps": round(2 * biggest / (copy_ms * 1e-3) / 1e9, 1),
+    }
 
 
 def main():
@@ -196,6 +236,9 @@ def main():
         "phase_ms": {p: round(t, 4) for p, t in phase_ms.items()},
         "cpu_baseline": None,
     }
+    out.update(cold_permutation_rates(sh))
+    log(f"[bench] cold permutations {out['pack_unpack_cold_gbps']} GB/s, "
+        f"device copy {out['hbm_copy_cold_gbps']} GB/s")
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle sample")
         out["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)

@@ -92,8 +92,8 @@ int basp_validate(int b, int S, int H, int H_kv, int d, int G, int rank);
  * dst: device [b, S, n/G, d].  dtype selects 2-byte (BASP_BF16) or 4-byte
  * (BASP_F32) elements; values are copied bit for bit.
  * Alignment: every pointer aligned to the element size.
- * Errors: NULL, SHAPE, RANK, UNSUPPORTED (dtype, G > BASP_MAX_GROUP), ALIGN,
- * HIP. */
+ * Errors: NULL, SHAPE, RANK, UNSUPPORTED (dtype, G > BASP_MAX_GROUP,
+ * (S/G)*(n/G)*d >= 2^32 elements, or b*G > 65535), ALIGN, HIP. */
 int basp_pack(const void *const *src_shards, void *dst, int b, int S,
               int n_heads, int d, int G, int rank, int dtype, void *stream);
 

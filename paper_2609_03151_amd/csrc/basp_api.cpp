@@ -44,6 +44,10 @@ int check_perm(const void *const *shards, const void *local, int b, int S, int n
   if (rank < 0 || rank >= G) return BASP_ERR_RANK;
   if (dtype != BASP_BF16 && dtype != BASP_F32) return BASP_ERR_UNSUPPORTED;
   if (G > BASP_MAX_GROUP) return BASP_ERR_UNSUPPORTED;
+  // The kernels index one (sequence, shard) block of S/G rows with 32-bit
+  // element counts and put b*G blocks on a grid dimension.
+  if ((uint64_t)(S / G) * (uint64_t)(n / G) * (uint64_t)d >= (1ull << 32)) return BASP_ERR_UNSUPPORTED;
+  if ((uint64_t)b * (uint64_t)G > 65535) return BASP_ERR_UNSUPPORTED;
   out->b = b;
   out->S = S;
   out->G = G;

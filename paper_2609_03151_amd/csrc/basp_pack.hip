@@ -6,11 +6,14 @@
 // unpack: the inverse, written into the rank's head slice of each shard.
 //
 // For one token the rank's heads are a contiguous run of nl*d elements on
-// both sides, so either kernel is a batch of row copies: row r of the local
-// tensor (r = beta*S + s, s = j*S/G + t) <-> row (beta*S/G + t) of shard j,
-// at head offset rank*nl.  Each thread moves V-sized vectors (16 bytes when
-// the row length and the pointers allow), U of them in flight, with
-// non-temporal accesses: every byte is touched exactly once.
+// both sides, so for each (sequence beta, shard j) either kernel is a 2-D
+// copy of S/G rows: the local side is contiguous (rows j*S/G .. of sequence
+// beta), the shard side strided by the shard's row length, at head offset
+// rank*nl.  Workgroup L works on block (beta, j) number L % (b*G);
+// each thread moves V-sized vectors (16 bytes when the row length and the
+// pointers allow), U of them in flight, with non-temporal accesses: every
+// byte is touched exactly once.  The only index arithmetic per vector is a
+// division by the row length, done as a multiply-high.
 #include "basp_device.hpp"
 #include "basp_internal.hpp"
 
@@ -29,71 +32,87 @@ __device__ __forceinline__ void nt_store(V v, V *p) {
   __builtin_nontemporal_store(v, p);
 }
 
-// Row mapping shared by both directions.  `vec` indexes V-vectors of the
-// local tensor; returns the shard index and the vector offset inside it.
-struct RowMap {
-  uint32_t row_vecs;   // nl*d*elem / sizeof(V)
-  uint32_t S, Sg;
+// n / d for 32-bit n and a divisor d fixed per launch, by multiplication
+// (Granlund and Montgomery, "Division by invariant integers using
+// multiplication", 1994: the round-up multiplier with the fix-up add).
+struct FastDiv {
+  uint32_t m, s1, s2;
+  static FastDiv make(uint32_t d) {
+    uint32_t l = 0;
+    while (l < 32 && (1ull << l) < d) ++l;  // ceil(log2 d)
+    FastDiv f;
+    f.m = (uint32_t)((((1ull << 32) * ((1ull << l) - d)) / d + 1) & 0xFFFFFFFFull);
+    f.s1 = l < 1 ? l : 1;
+    f.s2 = l > 1 ? l - 1 : 0;
+    return f;
+  }
+  __device__ __forceinline__ uint32_t div(uint32_t n) const {
+    const uint32_t t1 = __umulhi(m, n);
+    return (t1 + ((n - t1) >> s1)) >> s2;
+  }
+};
+
+// One (beta, shard) block of rows.  `rows_vecs` = S/G * row_vecs vectors on
+// the local side, contiguous; shard-side row rt starts at rt * shard_row_vecs.
+struct CopyGeom {
+  uint32_t row_vecs;        // nl*d*elem / sizeof(V)
+  FastDiv by_row;           // division by row_vecs
+  uint32_t block_vecs;      // S/G * row_vecs (< 2^32, checked on the host)
+  uint32_t S, Sg, G;
+  uint32_t jb_count, bx_count;  // (beta, shard) blocks, and workgroups per block
   uint64_t shard_row_vecs;  // n*d*elem / sizeof(V)
   uint64_t head_off_vecs;   // rank*nl*d*elem / sizeof(V)
-
-  __device__ __forceinline__ void map(uint64_t vec, uint32_t &j,
-                                      uint64_t &shard_off) const {
-    uint64_t r = vec / row_vecs;
-    uint32_t c = (uint32_t)(vec - r * row_vecs);
-    uint64_t beta = r / S;
-    uint32_t s = (uint32_t)(r - beta * S);
-    j = s / Sg;
-    uint32_t t = s - j * Sg;
-    shard_off = (beta * Sg + t) * shard_row_vecs + head_off_vecs + c;
-  }
 };
 
 template <typename V, int U>
 __global__ __launch_bounds__(256) void pack_kernel(ShardTable src, V *__restrict__ dst,
-                                                   uint64_t total, RowMap m) {
-  const uint64_t stride = (uint64_t)gridDim.x * 256u;
-  for (uint64_t base = (uint64_t)blockIdx.x * 256u + threadIdx.x; base < total;
-       base += stride * U) {
+                                                   CopyGeom g) {
+  const uint32_t jb = blockIdx.x % g.jb_count, bx = blockIdx.x / g.jb_count;
+  const uint32_t j = jb % g.G, beta = jb / g.G;
+  const V *s = static_cast<const V *>(src.p[j]) + (uint64_t)beta * g.Sg * g.shard_row_vecs +
+               g.head_off_vecs;
+  V *d = dst + ((uint64_t)beta * g.S + (uint64_t)j * g.Sg) * g.row_vecs;
+  const uint32_t step = g.bx_count * 256u * U;
+  for (uint32_t base = bx * 256u * U + threadIdx.x; base < g.block_vecs; base += step) {
     V v[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      uint64_t idx = base + u * stride;
-      if (idx < total) {
-        uint32_t j;
-        uint64_t off;
-        m.map(idx, j, off);
-        v[u] = nt_load(static_cast<const V *>(src.p[j]) + off);
+      const uint32_t i = base + u * 256u;
+      if (i < g.block_vecs) {
+        const uint32_t rt = g.by_row.div(i);
+        v[u] = nt_load(s + (uint64_t)rt * g.shard_row_vecs + (i - rt * g.row_vecs));
       }
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      uint64_t idx = base + u * stride;
-      if (idx < total) nt_store(v[u], dst + idx);
+      const uint32_t i = base + u * 256u;
+      if (i < g.block_vecs) nt_store(v[u], d + i);
     }
   }
 }
 
 template <typename V, int U>
 __global__ __launch_bounds__(256) void unpack_kernel(const V *__restrict__ src, ShardTable dst,
-                                                     uint64_t total, RowMap m) {
-  const uint64_t stride = (uint64_t)gridDim.x * 256u;
-  for (uint64_t base = (uint64_t)blockIdx.x * 256u + threadIdx.x; base < total;
-       base += stride * U) {
+                                                     CopyGeom g) {
+  const uint32_t jb = blockIdx.x % g.jb_count, bx = blockIdx.x / g.jb_count;
+  const uint32_t j = jb % g.G, beta = jb / g.G;
+  const V *s = src + ((uint64_t)beta * g.S + (uint64_t)j * g.Sg) * g.row_vecs;
+  V *d = static_cast<V *>(const_cast<void *>(dst.p[j])) + (uint64_t)beta * g.Sg * g.shard_row_vecs +
+         g.head_off_vecs;
+  const uint32_t step = g.bx_count * 256u * U;
+  for (uint32_t base = bx * 256u * U + threadIdx.x; base < g.block_vecs; base += step) {
     V v[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      uint64_t idx = base + u * stride;
-      if (idx < total) v[u] = nt_load(src + idx);
+      const uint32_t i = base + u * 256u;
+      if (i < g.block_vecs) v[u] = nt_load(s + i);
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      uint64_t idx = base + u * stride;
-      if (idx < total) {
-        uint32_t j;
-        uint64_t off;
-        m.map(idx, j, off);
-        nt_store(v[u], static_cast<V *>(const_cast<void *>(dst.p[j])) + off);
+      const uint32_t i = base + u * 256u;
+      if (i < g.block_vecs) {
+        const uint32_t rt = g.by_row.div(i);
+        nt_store(v[u], d + (uint64_t)rt * g.shard_row_vecs + (i - rt * g.row_vecs));
       }
     }
   }
@@ -104,26 +123,37 @@ namespace {
 template <typename V>
 hipError_t launch_typed(bool is_pack, const void *const *shards, void *local,
                         const PermShape &s, hipStream_t stream) {
-  constexpr int U = 4;
+  constexpr int U = 8;
   const uint64_t vsz = sizeof(V);
-  RowMap m;
-  m.row_vecs = (uint32_t)(s.row_bytes / vsz);
-  m.S = (uint32_t)s.S;
-  m.Sg = (uint32_t)(s.S / s.G);
-  m.shard_row_vecs = s.shard_row_bytes / vsz;
-  m.head_off_vecs = s.head_off_bytes / vsz;
-  const uint64_t total = (uint64_t)s.b * (uint64_t)s.S * m.row_vecs;
+  CopyGeom g;
+  g.row_vecs = (uint32_t)(s.row_bytes / vsz);
+  g.by_row = FastDiv::make(g.row_vecs);
+  g.S = (uint32_t)s.S;
+  g.Sg = (uint32_t)(s.S / s.G);
+  g.G = (uint32_t)s.G;
+  g.block_vecs = (uint32_t)((uint64_t)g.Sg * g.row_vecs);
+  g.shard_row_vecs = s.shard_row_bytes / vsz;
+  g.head_off_vecs = s.head_off_bytes / vsz;
   ShardTable t;
   for (int j = 0; j < s.G; ++j) t.p[j] = shards[j];
-  uint64_t blocks = (total + 256 * U - 1) / (256 * U);
-  if (blocks > 32768) blocks = 32768;
-  if (blocks == 0) return hipSuccess;
+  const uint64_t blocks_y = (uint64_t)s.b * s.G;
+  if (blocks_y == 0 || g.block_vecs == 0) return hipSuccess;
+  // Enough workgroups in total to fill the GPU several times over, each
+  // moving at least 256*U vectors per pass.
+  uint64_t bx = ((uint64_t)g.block_vecs + 256 * U - 1) / (256 * U);
+  const uint64_t want = (8192 + blocks_y - 1) / blocks_y;
+  if (bx > want) bx = want;
+  g.jb_count = (uint32_t)blocks_y;
+  g.bx_count = (uint32_t)bx;
+  // Consecutive workgroups take different (beta, shard) blocks, so the
+  // shard buffers are read (or written) side by side.
+  const dim3 grid((unsigned)(bx * blocks_y));
   if (is_pack)
-    hipLaunchKernelGGL((pack_kernel<V, U>), dim3((unsigned)blocks), dim3(256), 0, stream,
-                       t, static_cast<V *>(local), total, m);
+    hipLaunchKernelGGL((pack_kernel<V, U>), grid, dim3(256), 0, stream, t, static_cast<V *>(local),
+                       g);
   else
-    hipLaunchKernelGGL((unpack_kernel<V, U>), dim3((unsigned)blocks), dim3(256), 0, stream,
-                       static_cast<const V *>(local), t, total, m);
+    hipLaunchKernelGGL((unpack_kernel<V, U>), grid, dim3(256), 0, stream,
+                       static_cast<const V *>(local), t, g);
   return hipGetLastError();
 }
 

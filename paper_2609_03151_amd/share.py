@@ -97,6 +97,20 @@ class RankShare:
     def attn_bwd_flops(self) -> float:
         return 2.5 * self.attn_fwd_flops()
 
+    def permutation_calls(self) -> list:
+        """(name, call, bytes read + written) of each of the eight pack/unpack calls of a step."""
+        two = lambda t: 2 * t.numel() * t.element_size()
+        return [
+            ("pack_q", lambda: pack(self.q_shards, self.rank, out=self.q), two(self.q)),
+            ("pack_k", lambda: pack(self.k_shards, self.rank, out=self.k), two(self.k)),
+            ("pack_v", lambda: pack(self.v_shards, self.rank, out=self.v), two(self.v)),
+            ("unpack_o", lambda: unpack(self.o, self.o_shards, self.rank), two(self.o)),
+            ("pack_do", lambda: pack(self.do_shards, self.rank, out=self.do), two(self.do)),
+            ("unpack_dq", lambda: unpack(self.dq, self.dq_shards, self.rank), two(self.dq)),
+            ("unpack_dk", lambda: unpack(self.dk, self.dk_shards, self.rank), two(self.dk)),
+            ("unpack_dv", lambda: unpack(self.dv, self.dv_shards, self.rank), two(self.dv)),
+        ]
+
     def pack_unpack_bytes(self) -> dict:
         """Bytes read + written by each permutation (each moved element twice)."""
         bq = self.q.numel() * 2

@@ -103,6 +103,19 @@ def test_pack_rejects_group_beyond_maximum():
     assert L.basp_pack(ptrs, _fake(0x100000), 1, G, G, 8, G, 0, 0, None) == UNSUP
 
 
+def test_pack_rejects_sizes_beyond_32bit_block_index():
+    """(S/G)*(n/G)*d must stay below 2^32 elements and b*G within a grid
+    dimension (65535); both are rejected before the pointers are looked at."""
+    L = basp.lib()
+    good = (ctypes.c_void_p * 2)(0x1000, 0x2000)
+    dst = _fake(0x3000)
+    # (S/G)*(n/G)*d = 2^22 * 2^4 * 2^6 = 2^32
+    assert L.basp_pack(good, dst, 1, 1 << 23, 32, 64, 2, 0, 0, None) == UNSUP
+    assert L.basp_unpack(dst, good, 1, 1 << 23, 32, 64, 2, 0, 0, None) == UNSUP
+    assert L.basp_pack(good, dst, 32768, 64, 8, 64, 2, 0, 0, None) == UNSUP   # b*G = 65536
+    assert L.basp_pack(None, dst, 1, 1 << 23, 32, 64, 2, 0, 0, None) == UNSUP  # before NULL
+
+
 def test_attn_rejects_before_any_hip_call():
     L = basp.lib()
     p = [_fake(0x10000 * (i + 1)) for i in range(10)]
