@@ -53,6 +53,8 @@ def lib():
     L.oracle_seq_partition.argtypes = [c_long, c_long, c_long, lp, lp, lp, lp]
     L.oracle_pack.argtypes = [ctypes.POINTER(vp), vp] + [c_long] * 7
     L.oracle_unpack.argtypes = [vp, ctypes.POINTER(vp)] + [c_long] * 7
+    L.oracle_a2a_pack.argtypes = [vp, vp] + [c_long] * 6
+    L.oracle_a2a_unpack.argtypes = [vp, vp] + [c_long] * 6
     L.oracle_attn_fwd.argtypes = [vp] * 5 + [c_long] * 5 + [c_double, c_long, c_long]
     L.oracle_attn_bwd.argtypes = [vp] * 9 + [c_long] * 5 + [c_double, c_long]
     L.oracle_attn_rows.argtypes = ([vp] * 4 + [c_long] * 5 + [c_double, c_long]
@@ -151,6 +153,27 @@ def unpack(local, shards, rank: int):
                              src.dtype.itemsize)
     _check(rc, "unpack")
     return shards
+
+
+def a2a_pack(own, G: int) -> np.ndarray:
+    """Own shard [b, S/G, n, d] -> send buffer [G, b, S/G, n/G, d] (raw bytes)."""
+    src = _np(own)
+    b, Sg, n, d = src.shape
+    out = np.empty((G, b, Sg, n // G if n % G == 0 else 0, d), dtype=src.dtype)
+    rc = lib().oracle_a2a_pack(_ptr(src), _ptr(out), b, Sg * G, n, d, G, src.dtype.itemsize)
+    _check(rc, "a2a_pack")
+    return out
+
+
+def a2a_unpack(recv) -> np.ndarray:
+    """Received blocks [G, b, S/G, n/G, d] -> own shard [b, S/G, n, d] (raw bytes)."""
+    src = _np(recv)
+    G, b, Sg, nl, d = src.shape
+    out = np.empty((b, Sg, G * nl, d), dtype=src.dtype)
+    rc = lib().oracle_a2a_unpack(_ptr(src), _ptr(out), b, Sg * G, G * nl, d, G,
+                                 src.dtype.itemsize)
+    _check(rc, "a2a_unpack")
+    return out
 
 
 # -------------------------------------------------------------- attention

@@ -137,6 +137,44 @@ int oracle_unpack(const void *src, void *const *dst, long b, long S, long n,
   return ORC_OK;
 }
 
+int oracle_a2a_pack(const void *own, void *send, long b, long S, long n,
+                    long d, long G, long elem) {
+  int rc = perm_args_ok(b, S, n, d, G, 0, elem);
+  if (rc) return rc;
+  if (!own || !send) return ORC_ERR_NULL;
+  long Sg = S / G, nl = n / G;
+  for (long j = 0; j < G; ++j)
+    for (long beta = 0; beta < b; ++beta)
+      for (long t = 0; t < Sg; ++t)
+        for (long h = 0; h < nl; ++h)
+          for (long e = 0; e < d; ++e) {
+            long from = ((beta * Sg + t) * n + (j * nl + h)) * d + e;
+            long to = (((j * b + beta) * Sg + t) * nl + h) * d + e;
+            memcpy((unsigned char *)send + to * elem,
+                   (const unsigned char *)own + from * elem, (size_t)elem);
+          }
+  return ORC_OK;
+}
+
+int oracle_a2a_unpack(const void *recv, void *own, long b, long S, long n,
+                      long d, long G, long elem) {
+  int rc = perm_args_ok(b, S, n, d, G, 0, elem);
+  if (rc) return rc;
+  if (!recv || !own) return ORC_ERR_NULL;
+  long Sg = S / G, nl = n / G;
+  for (long j = 0; j < G; ++j)
+    for (long beta = 0; beta < b; ++beta)
+      for (long t = 0; t < Sg; ++t)
+        for (long h = 0; h < nl; ++h)
+          for (long e = 0; e < d; ++e) {
+            long from = (((j * b + beta) * Sg + t) * nl + h) * d + e;
+            long to = ((beta * Sg + t) * n + (j * nl + h)) * d + e;
+            memcpy((unsigned char *)own + to * elem,
+                   (const unsigned char *)recv + from * elem, (size_t)elem);
+          }
+  return ORC_OK;
+}
+
 /* ------------------------------------------------------------ attention */
 static double dot(const double *x, const double *y, long d) {
   double acc = 0.0;

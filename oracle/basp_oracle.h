@@ -41,6 +41,21 @@ int oracle_pack(const void *const *src, void *dst, long b, long S, long n,
 int oracle_unpack(const void *src, void *const *dst, long b, long S, long n,
                   long d, long G, long rank, long elem);
 
+/* Send side of the all-to-all, on the owner of a sequence shard (Sec. II-C:
+ * each member sends every other member its share of the heads): the own
+ * shard [b, S/G, n, d], all heads, split by destination member j into
+ *   send[j][beta][t][h][e] = own[beta][t][j*n/G + h][e],  send [G, b, S/G, n/G, d].
+ * elem = bytes per element (2 or 4); copied as raw bytes. */
+int oracle_a2a_pack(const void *own, void *send, long b, long S, long n,
+                    long d, long G, long elem);
+
+/* Receive side of the reverse all-to-all (the output goes back to the
+ * sequence owners): block j, the heads [j*n/G, (j+1)*n/G) member j computed,
+ * into the own shard:
+ *   own[beta][t][j*n/G + h][e] = recv[j][beta][t][h][e],  recv [G, b, S/G, n/G, d]. */
+int oracle_a2a_unpack(const void *recv, void *own, long b, long S, long n,
+                      long d, long G, long elem);
+
 /* Causal scaled dot-product attention (Sec. II-A), local q head h reads local
  * kv head h / (Hl/Hkl).  Computes rows [r0, r1) of every (beta, h):
  *   o   [b, r1-r0, Hl, d],  lse [b, Hl, r1-r0].
