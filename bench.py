@@ -106,7 +106,8 @@ def cold_permutation_rates(sh, reps: int = 5):
     write (larger than L2 and the 256 MB MALL) precedes every timed call; the
     median of `reps` runs per call.  Also a plain device-to-device copy of
     the largest permutation's size under the same conditions, as the
-    achievable HBM rate."""
+    achievable HBM rate, and the send/receive-side permutations of the
+    owner's shard (basp_a2a_pack / basp_a2a_unpack) at the same shapes."""
     import statistics
     import torch
     scratch = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
@@ -125,17 +126,34 @@ def cold_permutation_rates(sh, reps: int = 5):
 
     calls = sh.permutation_calls()
     per = {name: (cold(fn), nbytes) for name, fn, nbytes in calls}
+    # The owner's side of the same exchanges (send pack of the own Q and K
+    # shards, receive unpack of O and of fp32 dQ), outside the step.
+    import paper_2609_03151_amd as basp
+    G, r = sh.G, sh.rank
+    own_q, own_k = sh.q_shards[r], sh.k_shards[r]
+    send_q = basp.a2a_pack(own_q, G)
+    send_k = basp.a2a_pack(own_k, G)
+    own_dq = torch.empty(sh.dq_shards[r].shape, dtype=torch.float32, device="cuda")
+    recv_dq = basp.a2a_pack(own_dq.zero_(), G)
+    two = lambda t: 2 * t.numel() * t.element_size()
+    a2a = {
+        "a2a_pack_q": (cold(lambda: basp.a2a_pack(own_q, G, out=send_q)), two(own_q)),
+        "a2a_pack_k": (cold(lambda: basp.a2a_pack(own_k, G, out=send_k)), two(own_k)),
+        "a2a_unpack_o": (cold(lambda: basp.a2a_unpack(send_q, out=sh.o_shards[r])), two(own_q)),
+        "a2a_unpack_dq": (cold(lambda: basp.a2a_unpack(recv_dq, out=own_dq)), two(own_dq)),
+    }
     total_ms = sum(t for t, _ in per.values())
     total_bytes = sum(b for _, b in per.values())
     biggest = max(b for _, b in per.values()) // 2
     src = torch.empty(biggest // 4, dtype=torch.float32, device="cuda").fill_(2.0)
     dst = torch.empty_like(src)
     copy_ms = cold(lambda: dst.copy_(src))
-    del scratch, src, dst
+    del scratch, src, dst, send_q, send_k, own_dq, recv_dq
     return {
         "pack_unpack_cold_gbps": round(total_bytes / (total_ms * 1e-3) / 1e9, 1),
         "pack_unpack_cold_gbps_by_call": {n: round(b / (t * 1e-3) / 1e9, 1) for n, (t, b) in per.items()},
         "hbm_copy_cold_gbps": round(2 * biggest / (copy_ms * 1e-3) / 1e9, 1),
+        "a2a_cold_gbps_by_call": {n: round(b / (t * 1e-3) / 1e9, 1) for n, (t, b) in a2a.items()},
     }
 
 

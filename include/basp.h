@@ -14,6 +14,8 @@
  *   basp_attn_fwd  causal GQA attention on the rank's H/G query heads
  *   basp_attn_bwd  its backward (dQ, dK, dV in fp32)
  *   basp_unpack    head-sharded result -> the rank's head slice of G shards
+ *   basp_a2a_pack / basp_a2a_unpack   the owner's side of the same exchanges:
+ *                  own shard <-> one contiguous block per member
  *
  * The exchange itself (RCCL) is not part of this library.
  *
@@ -93,7 +95,7 @@ int basp_validate(int b, int S, int H, int H_kv, int d, int G, int rank);
  * (BASP_F32) elements; values are copied bit for bit.
  * Alignment: every pointer aligned to the element size.
  * Errors: NULL, SHAPE, RANK, UNSUPPORTED (dtype, G > BASP_MAX_GROUP,
- * (S/G)*(n/G)*d >= 2^32 elements, or b*G > 65535), ALIGN, HIP. */
+ * (S/G)*(n/G)*d >= 2^31 elements, or b*G > 65535), ALIGN, HIP. */
 int basp_pack(const void *const *src_shards, void *dst, int b, int S,
               int n_heads, int d, int G, int rank, int dtype, void *stream);
 
@@ -104,6 +106,29 @@ int basp_pack(const void *const *src_shards, void *dst, int b, int S,
  * untouched.  Arguments and errors as basp_pack. */
 int basp_unpack(const void *src, void *const *dst_shards, int b, int S,
                 int n_heads, int d, int G, int rank, int dtype, void *stream);
+
+/* Send side of the first all-to-all, on the owner of a sequence shard
+ * (Sec. II-C: every member sends each other member that member's share of
+ * the heads; Sec. IV-C runs it inside a batch-aware group): the own shard,
+ * all heads, split into one contiguous block per destination member j,
+ *   send[j][beta][t][h][e] = own[beta][t][j*n/G + h][e]
+ * own: device [b, S/G, n, d]; send: device [G, b, S/G, n/G, d], so block j is
+ * one contiguous run of b*(S/G)*(n/G)*d elements for the exchange.  With the
+ * blocks of every member received, the head-sharded tensor basp_pack builds
+ * is block j at rows j*S/G .. of each sequence (for b = 1, the received
+ * buffer itself).  dtype as basp_pack; values copied bit for bit.
+ * Errors: NULL, SHAPE (S % G, n % G), UNSUPPORTED (as basp_pack), ALIGN, HIP. */
+int basp_a2a_pack(const void *own, void *send, int b, int S, int n_heads, int d,
+                  int G, int dtype, void *stream);
+
+/* Receive side of the second all-to-all (the attention output returns to
+ * the sequence owners): block j, received from member j and holding heads
+ * [j*n/G, (j+1)*n/G) of the own tokens, into the own shard:
+ *   own[beta][t][j*n/G + h][e] = recv[j][beta][t][h][e]
+ * recv: device [G, b, S/G, n/G, d]; own: device [b, S/G, n, d].  Arguments
+ * and errors as basp_a2a_pack. */
+int basp_a2a_unpack(const void *recv, void *own, int b, int S, int n_heads, int d,
+                    int G, int dtype, void *stream);
 
 /* Causal GQA scaled dot-product attention (Sec. II-A) over the full sequence
  * for the rank's H/G query heads:

@@ -27,8 +27,8 @@ STATUS = {
 }
 # Every symbol include/basp.h declares.
 EXPORTS = ("basp_status_str", "basp_group_of", "basp_validate", "basp_pack",
-           "basp_unpack", "basp_attn_fwd", "basp_attn_bwd_workspace_bytes",
-           "basp_attn_bwd")
+           "basp_unpack", "basp_a2a_pack", "basp_a2a_unpack", "basp_attn_fwd",
+           "basp_attn_bwd_workspace_bytes", "basp_attn_bwd")
 
 
 class BaspError(RuntimeError):
@@ -58,12 +58,14 @@ def lib() -> ctypes.CDLL:
     L.basp_validate.argtypes = [i] * 7
     L.basp_pack.argtypes = [ctypes.POINTER(vp), vp] + [i] * 7 + [vp]
     L.basp_unpack.argtypes = [vp, ctypes.POINTER(vp)] + [i] * 7 + [vp]
+    L.basp_a2a_pack.argtypes = [vp, vp] + [i] * 6 + [vp]
+    L.basp_a2a_unpack.argtypes = [vp, vp] + [i] * 6 + [vp]
     L.basp_attn_fwd.argtypes = [vp] * 5 + [i] * 6 + [f, vp]
     L.basp_attn_bwd_workspace_bytes.argtypes = [i] * 6
     L.basp_attn_bwd_workspace_bytes.restype = sz
     L.basp_attn_bwd.argtypes = [vp] * 10 + [sz] + [i] * 6 + [f, vp]
     for name in ("basp_group_of", "basp_validate", "basp_pack", "basp_unpack",
-                 "basp_attn_fwd", "basp_attn_bwd"):
+                 "basp_a2a_pack", "basp_a2a_unpack", "basp_attn_fwd", "basp_attn_bwd"):
         getattr(L, name).restype = i
     _lib = L
     return L
@@ -141,6 +143,27 @@ def unpack(local: torch.Tensor, shards, rank: int):
     _check(lib().basp_unpack(_dev(local, "local"), ptrs, b, Sg * G, n, d, G, rank,
                              _dtype_code(local), _stream(local)), "basp_unpack")
     return shards
+
+
+def a2a_pack(own: torch.Tensor, G: int, out: torch.Tensor | None = None) -> torch.Tensor:
+    """Own shard [b, S/G, n, d] -> send buffer [G, b, S/G, n/G, d], one block per member."""
+    b, Sg, n, d = own.shape
+    if out is None:
+        out = torch.empty((G, b, Sg, max(n // G, 0), d), dtype=own.dtype, device=own.device)
+    _check(lib().basp_a2a_pack(_dev(own, "own"), _dev(out, "out", own.dtype), b, Sg * G, n, d,
+                               G, _dtype_code(own), _stream(own)), "basp_a2a_pack")
+    return out
+
+
+def a2a_unpack(recv: torch.Tensor, out: torch.Tensor | None = None) -> torch.Tensor:
+    """Received blocks [G, b, S/G, n/G, d] -> own shard [b, S/G, n, d]."""
+    G, b, Sg, nl, d = recv.shape
+    if out is None:
+        out = torch.empty((b, Sg, G * nl, d), dtype=recv.dtype, device=recv.device)
+    _check(lib().basp_a2a_unpack(_dev(recv, "recv"), _dev(out, "out", recv.dtype), b, Sg * G,
+                                 G * nl, d, G, _dtype_code(recv), _stream(recv)),
+           "basp_a2a_unpack")
+    return out
 
 
 # -------------------------------------------------------------- attention

@@ -37,46 +37,136 @@ int check_attn(int b, int S, int H, int H_kv, int d, int G, float scale) {
   return BASP_OK;
 }
 
-int check_perm(const void *const *shards, const void *local, int b, int S, int n, int d,
-               int G, int rank, int dtype, basp::PermShape *out) {
+int hip_status(hipError_t e) { return e == hipSuccess ? BASP_OK : BASP_ERR_HIP; }
+
+// Shape rules shared by every permutation.  The kernels index one (member,
+// sequence) block of S/G rows with 32-bit vector counts that must stay below
+// 2^31 including the loop stride, and put b*G blocks on one grid dimension.
+int check_perm_shape(int b, int S, int n, int d, int G, int dtype) {
   if (b < 0 || S < 0 || n < 1 || d < 1 || G < 1) return BASP_ERR_SHAPE;
   if (S % G != 0 || n % G != 0) return BASP_ERR_SHAPE;
-  if (rank < 0 || rank >= G) return BASP_ERR_RANK;
   if (dtype != BASP_BF16 && dtype != BASP_F32) return BASP_ERR_UNSUPPORTED;
   if (G > BASP_MAX_GROUP) return BASP_ERR_UNSUPPORTED;
-  // The kernels index one (sequence, shard) block of S/G rows with 32-bit
-  // element counts and put b*G blocks on a grid dimension.
-  if ((uint64_t)(S / G) * (uint64_t)(n / G) * (uint64_t)d >= (1ull << 32)) return BASP_ERR_UNSUPPORTED;
+  if ((uint64_t)(S / G) * (uint64_t)(n / G) * (uint64_t)d >= (1ull << 31)) return BASP_ERR_UNSUPPORTED;
   if ((uint64_t)b * (uint64_t)G > 65535) return BASP_ERR_UNSUPPORTED;
-  out->b = b;
-  out->S = S;
-  out->G = G;
-  // An empty problem touches no memory: its pointers are not inspected.
-  if ((long long)b * S == 0) return BASP_OK;
-  if (!shards || !local) return BASP_ERR_NULL;
-  for (int j = 0; j < G; ++j)
-    if (!shards[j]) return BASP_ERR_NULL;
-  const uint64_t elem = dtype == BASP_BF16 ? 2 : 4;
-  const uint64_t nl = (uint64_t)(n / G);
-  out->row_bytes = nl * (uint64_t)d * elem;
-  out->shard_row_bytes = (uint64_t)n * (uint64_t)d * elem;
-  out->head_off_bytes = (uint64_t)rank * nl * (uint64_t)d * elem;
-  if (!aligned(local, elem)) return BASP_ERR_ALIGN;
-  for (int j = 0; j < G; ++j)
-    if (!aligned(shards[j], elem)) return BASP_ERR_ALIGN;
-  // Widest access that every row start on both sides allows.
-  int vec = 16;
-  while (vec > (int)elem) {
-    bool ok = out->row_bytes % vec == 0 && aligned(local, vec);
-    for (int j = 0; ok && j < G; ++j) ok = aligned(shards[j], vec);
-    if (ok) break;
-    vec >>= 1;
-  }
-  out->vec_bytes = vec;
   return BASP_OK;
 }
 
-int hip_status(hipError_t e) { return e == hipSuccess ? BASP_OK : BASP_ERR_HIP; }
+// Pointers (G-entry tables, a single buffer repeated) and the widest access
+// every row start on both sides allows.
+int finish_perm(const void *const *src_tab, void *const *dst_tab, uint64_t elem,
+                basp::PermShape *s) {
+  for (int j = 0; j < s->G; ++j)
+    if (!src_tab[j] || !dst_tab[j]) return BASP_ERR_NULL;
+  for (int j = 0; j < s->G; ++j)
+    if (!aligned(src_tab[j], elem) || !aligned(dst_tab[j], elem)) return BASP_ERR_ALIGN;
+  const uint64_t q[] = {s->row_bytes, s->src_beta, s->src_j, s->src_row, s->src_off,
+                        s->dst_beta, s->dst_j, s->dst_row, s->dst_off};
+  int vec = 16;
+  while (vec > (int)elem) {
+    bool ok = true;
+    for (uint64_t x : q) ok = ok && x % vec == 0;
+    for (int j = 0; ok && j < s->G; ++j) ok = aligned(src_tab[j], vec) && aligned(dst_tab[j], vec);
+    if (ok) break;
+    vec >>= 1;
+  }
+  s->vec_bytes = vec;
+  return BASP_OK;
+}
+
+// Sequence-shard side [b, S/G, n, d] at head offset `head0`, or head-sharded
+// side [b, S, n/G, d] with member j's tokens at rows j*S/G ..
+void shard_side(int S, int n, int d, int G, uint64_t elem, uint64_t head0, uint64_t &beta,
+                uint64_t &j, uint64_t &row, uint64_t &off) {
+  beta = (uint64_t)(S / G) * n * d * elem;
+  j = 0;
+  row = (uint64_t)n * d * elem;
+  off = head0 * d * elem;
+}
+void local_side(int S, int n, int d, int G, uint64_t elem, uint64_t &beta, uint64_t &j,
+                uint64_t &row, uint64_t &off) {
+  const uint64_t nl = (uint64_t)(n / G);
+  beta = (uint64_t)S * nl * d * elem;
+  j = (uint64_t)(S / G) * nl * d * elem;
+  row = nl * d * elem;
+  off = 0;
+}
+
+basp::PermShape perm_base(int b, int S, int n, int d, int G, uint64_t elem) {
+  basp::PermShape s{};
+  s.b = b;
+  s.G = G;
+  s.Sg = S / G;
+  s.row_bytes = (uint64_t)(n / G) * d * elem;
+  return s;
+}
+
+// Receive-side pack (to_local) or send-side unpack of the rank's head slice.
+int run_pack(bool to_local, const void *const *shards, const void *local, int b, int S, int n,
+             int d, int G, int rank, int dtype, void *stream) {
+  int rc = check_perm_shape(b, S, n, d, G, dtype);
+  if (rc) return rc;
+  if (rank < 0 || rank >= G) return BASP_ERR_RANK;
+  // An empty problem touches no memory: its pointers are not inspected.
+  if ((long long)b * S == 0) return BASP_OK;
+  if (!shards || !local) return BASP_ERR_NULL;
+  const uint64_t elem = dtype == BASP_BF16 ? 2 : 4;
+  basp::PermShape s = perm_base(b, S, n, d, G, elem);
+  const void *one[BASP_MAX_GROUP];
+  for (int j = 0; j < G; ++j) one[j] = local;
+  const uint64_t head0 = (uint64_t)rank * (n / G);
+  if (to_local) {
+    shard_side(S, n, d, G, elem, head0, s.src_beta, s.src_j, s.src_row, s.src_off);
+    local_side(S, n, d, G, elem, s.dst_beta, s.dst_j, s.dst_row, s.dst_off);
+    rc = finish_perm(shards, const_cast<void *const *>(one), elem, &s);
+    if (rc) return rc;
+    (void)hipGetLastError();
+    return hip_status(basp::launch_permute(shards, const_cast<void *const *>(one), s,
+                                           (hipStream_t)stream));
+  }
+  local_side(S, n, d, G, elem, s.src_beta, s.src_j, s.src_row, s.src_off);
+  shard_side(S, n, d, G, elem, head0, s.dst_beta, s.dst_j, s.dst_row, s.dst_off);
+  rc = finish_perm(one, const_cast<void *const *>(shards), elem, &s);
+  if (rc) return rc;
+  (void)hipGetLastError();
+  return hip_status(basp::launch_permute(one, const_cast<void *const *>(shards), s,
+                                         (hipStream_t)stream));
+}
+
+// Send-side split of the own shard (to_send) or its receive-side inverse.
+int run_a2a(bool to_send, const void *src, void *dst, int b, int S, int n, int d, int G,
+            int dtype, void *stream) {
+  int rc = check_perm_shape(b, S, n, d, G, dtype);
+  if (rc) return rc;
+  if ((long long)b * S == 0) return BASP_OK;
+  if (!src || !dst) return BASP_ERR_NULL;
+  const uint64_t elem = dtype == BASP_BF16 ? 2 : 4;
+  basp::PermShape s = perm_base(b, S, n, d, G, elem);
+  const uint64_t nl = (uint64_t)(n / G), Sg = (uint64_t)(S / G);
+  // own [b, S/G, n, d]: member j's heads at j*n/G
+  const uint64_t own_beta = Sg * n * d * elem, own_j = nl * d * elem, own_row = (uint64_t)n * d * elem;
+  // send/recv [G, b, S/G, n/G, d]
+  const uint64_t a2a_beta = Sg * nl * d * elem, a2a_j = (uint64_t)b * a2a_beta,
+                 a2a_row = nl * d * elem;
+  if (to_send) {
+    s.src_beta = own_beta, s.src_j = own_j, s.src_row = own_row;
+    s.dst_beta = a2a_beta, s.dst_j = a2a_j, s.dst_row = a2a_row;
+  } else {
+    s.src_beta = a2a_beta, s.src_j = a2a_j, s.src_row = a2a_row;
+    s.dst_beta = own_beta, s.dst_j = own_j, s.dst_row = own_row;
+  }
+  const void *st[BASP_MAX_GROUP];
+  void *dt[BASP_MAX_GROUP];
+  for (int j = 0; j < G; ++j) {
+    st[j] = src;
+    dt[j] = dst;
+  }
+  rc = finish_perm(st, dt, elem, &s);
+  if (rc) return rc;
+  (void)hipGetLastError();
+  return hip_status(basp::launch_permute(st, dt, s, (hipStream_t)stream));
+}
+
 
 }  // namespace
 
@@ -126,23 +216,23 @@ int basp_validate(int b, int S, int H, int H_kv, int d, int G, int rank) {
 
 int basp_pack(const void *const *src_shards, void *dst, int b, int S, int n_heads, int d,
               int G, int rank, int dtype, void *stream) {
-  basp::PermShape s;
-  int rc = check_perm(src_shards, dst, b, S, n_heads, d, G, rank, dtype, &s);
-  if (rc) return rc;
-  if ((long long)b * S == 0) return BASP_OK;
-  (void)hipGetLastError();
-  return hip_status(basp::launch_permute(true, src_shards, dst, s, (hipStream_t)stream));
+  return run_pack(true, src_shards, dst, b, S, n_heads, d, G, rank, dtype, stream);
 }
 
 int basp_unpack(const void *src, void *const *dst_shards, int b, int S, int n_heads, int d,
                 int G, int rank, int dtype, void *stream) {
-  basp::PermShape s;
-  int rc = check_perm(dst_shards, src, b, S, n_heads, d, G, rank, dtype, &s);
-  if (rc) return rc;
-  if ((long long)b * S == 0) return BASP_OK;
-  (void)hipGetLastError();
-  return hip_status(basp::launch_permute(false, dst_shards, const_cast<void *>(src), s,
-                                         (hipStream_t)stream));
+  return run_pack(false, const_cast<const void *const *>(dst_shards), src, b, S, n_heads, d, G,
+                  rank, dtype, stream);
+}
+
+int basp_a2a_pack(const void *own, void *send, int b, int S, int n_heads, int d, int G,
+                  int dtype, void *stream) {
+  return run_a2a(true, own, send, b, S, n_heads, d, G, dtype, stream);
+}
+
+int basp_a2a_unpack(const void *recv, void *own, int b, int S, int n_heads, int d, int G,
+                    int dtype, void *stream) {
+  return run_a2a(false, recv, own, b, S, n_heads, d, G, dtype, stream);
 }
 
 int basp_attn_fwd(const void *q, const void *k, const void *v, void *o, float *lse, int b,

@@ -11,16 +11,22 @@
 
 namespace basp {
 
+// Every permutation of the library is a batch of strided row copies: G*b
+// blocks (member j, sequence beta) of Sg rows, each row a contiguous run of
+// row_bytes.  Row t of block (j, beta) goes from
+//   src_tab[j] + beta*src_beta + j*src_j + t*src_row + src_off
+// to the same expression on the dst side (all in bytes).  A side that is a
+// single buffer repeats its pointer in all G table entries.
 struct PermShape {
-  int b, S, G;
-  uint64_t row_bytes;        // nl*d*elem: one token's run of the rank's heads
-  uint64_t shard_row_bytes;  // n*d*elem:  one token of a shard
-  uint64_t head_off_bytes;   // rank*nl*d*elem
-  int vec_bytes;             // 16, 8, 4 or 2: widest access every row allows
+  int b, G, Sg;
+  uint64_t row_bytes;
+  uint64_t src_beta, src_j, src_row, src_off;
+  uint64_t dst_beta, dst_j, dst_row, dst_off;
+  int vec_bytes;  // 16, 8, 4 or 2: widest access every row start allows
 };
 
-hipError_t launch_permute(bool is_pack, const void *const *shards, void *local,
-                          const PermShape &s, hipStream_t stream);
+hipError_t launch_permute(const void *const *src_tab, void *const *dst_tab, const PermShape &s,
+                          hipStream_t stream);
 
 struct AttnShape {
   int b, S, Hl, Hkl, d;  // local heads

@@ -1,19 +1,21 @@
 // basp_pack.hip -- the rank-local halves of the head-parallel all-to-all
 // (Sec. II-C of the paper; inside a batch-aware group, Sec. IV-C).
 //
-// pack:   G sequence shards [b, S/G, n, d] -> [b, S, n/G, d]
+// receive side, pack:       G sequence shards [b, S/G, n, d] -> [b, S, n/G, d]
 //         dst[beta][j*S/G + t][h][e] = shard_j[beta][t][rank*n/G + h][e]
-// unpack: the inverse, written into the rank's head slice of each shard.
+// send side, unpack:        the inverse, into the rank's head slice of each shard
+// send side, a2a_pack:      own shard [b, S/G, n, d] -> [G, b, S/G, n/G, d]
+//         send[j][beta][t][h][e] = own[beta][t][j*n/G + h][e]
+// receive side, a2a_unpack: the inverse, every member's block into the own shard
 //
-// For one token the rank's heads are a contiguous run of nl*d elements on
-// both sides, so for each (sequence beta, shard j) either kernel is a 2-D
-// copy of S/G rows: the local side is contiguous (rows j*S/G .. of sequence
-// beta), the shard side strided by the shard's row length, at head offset
-// rank*nl.  Workgroup L works on block (beta, j) number L % (b*G);
-// each thread moves V-sized vectors (16 bytes when the row length and the
-// pointers allow), U of them in flight, with non-temporal accesses: every
-// byte is touched exactly once.  The only index arithmetic per vector is a
-// division by the row length, done as a multiply-high.
+// For one token the heads moved are a contiguous run of (n/G)*d elements on
+// both sides, so each of these is, per (member j, sequence beta), a 2-D copy
+// of S/G rows with a row stride on each side (PermShape).  Workgroup L works
+// on block (j, beta) number L % (b*G), so all G buffers stream side by side;
+// each thread moves V-sized vectors (16 bytes when every row start allows),
+// U of them in flight, with non-temporal accesses: every byte is touched
+// exactly once.  The only index arithmetic per vector is a division by the
+// row length, done as a multiply-high.
 #include "basp_device.hpp"
 #include "basp_internal.hpp"
 
@@ -52,68 +54,38 @@ struct FastDiv {
   }
 };
 
-// One (beta, shard) block of rows.  `rows_vecs` = S/G * row_vecs vectors on
-// the local side, contiguous; shard-side row rt starts at rt * shard_row_vecs.
+// One launch's geometry in V-sized vectors.
 struct CopyGeom {
-  uint32_t row_vecs;        // nl*d*elem / sizeof(V)
-  FastDiv by_row;           // division by row_vecs
-  uint32_t block_vecs;      // S/G * row_vecs (< 2^32, checked on the host)
-  uint32_t S, Sg, G;
-  uint32_t jb_count, bx_count;  // (beta, shard) blocks, and workgroups per block
-  uint64_t shard_row_vecs;  // n*d*elem / sizeof(V)
-  uint64_t head_off_vecs;   // rank*nl*d*elem / sizeof(V)
+  uint32_t row_vecs;               // row_bytes / sizeof(V)
+  FastDiv by_row;                  // division by row_vecs
+  uint32_t block_vecs;             // Sg * row_vecs (< 2^32, checked on the host)
+  uint32_t G, jb_count, bx_count;  // members, (j, beta) blocks, workgroups per block
+  uint64_t src_beta, src_j, src_row, src_off;
+  uint64_t dst_beta, dst_j, dst_row, dst_off;
 };
 
 template <typename V, int U>
-__global__ __launch_bounds__(256) void pack_kernel(ShardTable src, V *__restrict__ dst,
-                                                   CopyGeom g) {
+__global__ __launch_bounds__(256) void permute_kernel(ShardTable src, ShardTable dst, CopyGeom g) {
   const uint32_t jb = blockIdx.x % g.jb_count, bx = blockIdx.x / g.jb_count;
   const uint32_t j = jb % g.G, beta = jb / g.G;
-  const V *s = static_cast<const V *>(src.p[j]) + (uint64_t)beta * g.Sg * g.shard_row_vecs +
-               g.head_off_vecs;
-  V *d = dst + ((uint64_t)beta * g.S + (uint64_t)j * g.Sg) * g.row_vecs;
+  const V *s = static_cast<const V *>(src.p[j]) + beta * g.src_beta + j * g.src_j + g.src_off;
+  V *d = static_cast<V *>(const_cast<void *>(dst.p[j])) + beta * g.dst_beta + j * g.dst_j +
+         g.dst_off;
   const uint32_t step = g.bx_count * 256u * U;
   for (uint32_t base = bx * 256u * U + threadIdx.x; base < g.block_vecs; base += step) {
     V v[U];
+    uint32_t rt[U], c[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const uint32_t i = base + u * 256u;
-      if (i < g.block_vecs) {
-        const uint32_t rt = g.by_row.div(i);
-        v[u] = nt_load(s + (uint64_t)rt * g.shard_row_vecs + (i - rt * g.row_vecs));
-      }
+      rt[u] = g.by_row.div(i);
+      c[u] = i - rt[u] * g.row_vecs;
+      if (i < g.block_vecs) v[u] = nt_load(s + (uint64_t)rt[u] * g.src_row + c[u]);
     }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const uint32_t i = base + u * 256u;
-      if (i < g.block_vecs) nt_store(v[u], d + i);
-    }
-  }
-}
-
-template <typename V, int U>
-__global__ __launch_bounds__(256) void unpack_kernel(const V *__restrict__ src, ShardTable dst,
-                                                     CopyGeom g) {
-  const uint32_t jb = blockIdx.x % g.jb_count, bx = blockIdx.x / g.jb_count;
-  const uint32_t j = jb % g.G, beta = jb / g.G;
-  const V *s = src + ((uint64_t)beta * g.S + (uint64_t)j * g.Sg) * g.row_vecs;
-  V *d = static_cast<V *>(const_cast<void *>(dst.p[j])) + (uint64_t)beta * g.Sg * g.shard_row_vecs +
-         g.head_off_vecs;
-  const uint32_t step = g.bx_count * 256u * U;
-  for (uint32_t base = bx * 256u * U + threadIdx.x; base < g.block_vecs; base += step) {
-    V v[U];
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const uint32_t i = base + u * 256u;
-      if (i < g.block_vecs) v[u] = nt_load(s + i);
-    }
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const uint32_t i = base + u * 256u;
-      if (i < g.block_vecs) {
-        const uint32_t rt = g.by_row.div(i);
-        nt_store(v[u], d + (uint64_t)rt * g.shard_row_vecs + (i - rt * g.row_vecs));
-      }
+      if (i < g.block_vecs) nt_store(v[u], d + (uint64_t)rt[u] * g.dst_row + c[u]);
     }
   }
 }
@@ -121,51 +93,51 @@ __global__ __launch_bounds__(256) void unpack_kernel(const V *__restrict__ src, 
 namespace {
 
 template <typename V>
-hipError_t launch_typed(bool is_pack, const void *const *shards, void *local,
-                        const PermShape &s, hipStream_t stream) {
+hipError_t launch_typed(const void *const *src_tab, void *const *dst_tab, const PermShape &s,
+                        hipStream_t stream) {
   constexpr int U = 8;
   const uint64_t vsz = sizeof(V);
   CopyGeom g;
   g.row_vecs = (uint32_t)(s.row_bytes / vsz);
   g.by_row = FastDiv::make(g.row_vecs);
-  g.S = (uint32_t)s.S;
-  g.Sg = (uint32_t)(s.S / s.G);
+  g.block_vecs = (uint32_t)((uint64_t)s.Sg * g.row_vecs);
   g.G = (uint32_t)s.G;
-  g.block_vecs = (uint32_t)((uint64_t)g.Sg * g.row_vecs);
-  g.shard_row_vecs = s.shard_row_bytes / vsz;
-  g.head_off_vecs = s.head_off_bytes / vsz;
-  ShardTable t;
-  for (int j = 0; j < s.G; ++j) t.p[j] = shards[j];
-  const uint64_t blocks_y = (uint64_t)s.b * s.G;
-  if (blocks_y == 0 || g.block_vecs == 0) return hipSuccess;
+  g.src_beta = s.src_beta / vsz;
+  g.src_j = s.src_j / vsz;
+  g.src_row = s.src_row / vsz;
+  g.src_off = s.src_off / vsz;
+  g.dst_beta = s.dst_beta / vsz;
+  g.dst_j = s.dst_j / vsz;
+  g.dst_row = s.dst_row / vsz;
+  g.dst_off = s.dst_off / vsz;
+  ShardTable ts, td;
+  for (int j = 0; j < s.G; ++j) {
+    ts.p[j] = src_tab[j];
+    td.p[j] = dst_tab[j];
+  }
+  const uint64_t blocks = (uint64_t)s.b * s.G;
+  if (blocks == 0 || g.block_vecs == 0) return hipSuccess;
   // Enough workgroups in total to fill the GPU several times over, each
   // moving at least 256*U vectors per pass.
   uint64_t bx = ((uint64_t)g.block_vecs + 256 * U - 1) / (256 * U);
-  const uint64_t want = (8192 + blocks_y - 1) / blocks_y;
+  const uint64_t want = (8192 + blocks - 1) / blocks;
   if (bx > want) bx = want;
-  g.jb_count = (uint32_t)blocks_y;
+  g.jb_count = (uint32_t)blocks;
   g.bx_count = (uint32_t)bx;
-  // Consecutive workgroups take different (beta, shard) blocks, so the
-  // shard buffers are read (or written) side by side.
-  const dim3 grid((unsigned)(bx * blocks_y));
-  if (is_pack)
-    hipLaunchKernelGGL((pack_kernel<V, U>), grid, dim3(256), 0, stream, t, static_cast<V *>(local),
-                       g);
-  else
-    hipLaunchKernelGGL((unpack_kernel<V, U>), grid, dim3(256), 0, stream,
-                       static_cast<const V *>(local), t, g);
+  hipLaunchKernelGGL((permute_kernel<V, U>), dim3((unsigned)(bx * blocks)), dim3(256), 0, stream,
+                     ts, td, g);
   return hipGetLastError();
 }
 
 }  // namespace
 
-hipError_t launch_permute(bool is_pack, const void *const *shards, void *local,
-                          const PermShape &s, hipStream_t stream) {
+hipError_t launch_permute(const void *const *src_tab, void *const *dst_tab, const PermShape &s,
+                          hipStream_t stream) {
   switch (s.vec_bytes) {
-    case 16: return launch_typed<u32x4>(is_pack, shards, local, s, stream);
-    case 8: return launch_typed<u32x2>(is_pack, shards, local, s, stream);
-    case 4: return launch_typed<uint32_t>(is_pack, shards, local, s, stream);
-    default: return launch_typed<uint16_t>(is_pack, shards, local, s, stream);
+    case 16: return launch_typed<u32x4>(src_tab, dst_tab, s, stream);
+    case 8: return launch_typed<u32x2>(src_tab, dst_tab, s, stream);
+    case 4: return launch_typed<uint32_t>(src_tab, dst_tab, s, stream);
+    default: return launch_typed<uint16_t>(src_tab, dst_tab, s, stream);
   }
 }
 

@@ -18,7 +18,7 @@ OK, NULL, SHAPE, RANK, UNSUP, ALIGN, WS, HIP, DP = range(9)
 def _declared():
     with open(os.path.join(ROOT, "include", "basp.h")) as f:
         text = f.read()
-    return sorted(set(re.findall(r"\b(basp_[a-z_]+)\s*\(", text)))
+    return sorted(set(re.findall(r"\b(basp_[a-z0-9_]+)\s*\(", text)))
 
 
 def test_exports_every_declared_symbol():
@@ -103,17 +103,37 @@ def test_pack_rejects_group_beyond_maximum():
     assert L.basp_pack(ptrs, _fake(0x100000), 1, G, G, 8, G, 0, 0, None) == UNSUP
 
 
-def test_pack_rejects_sizes_beyond_32bit_block_index():
-    """(S/G)*(n/G)*d must stay below 2^32 elements and b*G within a grid
+def test_permutations_reject_sizes_beyond_block_index():
+    """(S/G)*(n/G)*d must stay below 2^31 elements and b*G within a grid
     dimension (65535); both are rejected before the pointers are looked at."""
     L = basp.lib()
     good = (ctypes.c_void_p * 2)(0x1000, 0x2000)
     dst = _fake(0x3000)
-    # (S/G)*(n/G)*d = 2^22 * 2^4 * 2^6 = 2^32
-    assert L.basp_pack(good, dst, 1, 1 << 23, 32, 64, 2, 0, 0, None) == UNSUP
-    assert L.basp_unpack(dst, good, 1, 1 << 23, 32, 64, 2, 0, 0, None) == UNSUP
+    # (S/G)*(n/G)*d = 2^21 * 2^4 * 2^6 = 2^31
+    assert L.basp_pack(good, dst, 1, 1 << 22, 32, 64, 2, 0, 0, None) == UNSUP
+    assert L.basp_unpack(dst, good, 1, 1 << 22, 32, 64, 2, 0, 0, None) == UNSUP
+    assert L.basp_a2a_pack(dst, dst, 1, 1 << 22, 32, 64, 2, 0, None) == UNSUP
+    assert L.basp_a2a_unpack(dst, dst, 1, 1 << 22, 32, 64, 2, 0, None) == UNSUP
     assert L.basp_pack(good, dst, 32768, 64, 8, 64, 2, 0, 0, None) == UNSUP   # b*G = 65536
-    assert L.basp_pack(None, dst, 1, 1 << 23, 32, 64, 2, 0, 0, None) == UNSUP  # before NULL
+    assert L.basp_a2a_pack(dst, dst, 32768, 64, 8, 64, 2, 0, None) == UNSUP
+    assert L.basp_pack(None, dst, 1, 1 << 22, 32, 64, 2, 0, 0, None) == UNSUP  # before NULL
+
+
+def test_a2a_rejects_before_any_hip_call():
+    """Only invalid (or empty) calls: the pointers are fake host values."""
+    L = basp.lib()
+    a, c = _fake(0x1000), _fake(0x2000)
+    for fn in (L.basp_a2a_pack, L.basp_a2a_unpack):
+        assert fn(a, c, 1, 63, 8, 64, 2, 0, None) == SHAPE       # S % G
+        assert fn(a, c, 1, 64, 7, 64, 2, 0, None) == SHAPE       # n % G
+        assert fn(a, c, -1, 64, 8, 64, 2, 0, None) == SHAPE
+        assert fn(a, c, 1, 64, 8, 64, 2, 3, None) == UNSUP       # dtype
+        assert fn(a, c, 1, 64, 8, 64, 256, 0, None) == SHAPE     # 64 % 256
+        assert fn(None, c, 1, 64, 8, 64, 2, 0, None) == NULL
+        assert fn(a, None, 1, 64, 8, 64, 2, 0, None) == NULL
+        assert fn(_fake(0x1001), c, 1, 64, 8, 64, 2, 0, None) == ALIGN
+        assert fn(a, _fake(0x2002), 1, 64, 8, 64, 2, 1, None) == ALIGN
+        assert fn(None, None, 0, 64, 8, 64, 2, 0, None) == OK    # empty: nothing enqueued
 
 
 def test_attn_rejects_before_any_hip_call():
