@@ -60,7 +60,7 @@ typedef enum basp_status {
   BASP_ERR_NULL = 1,        /* a required pointer is NULL                    */
   BASP_ERR_SHAPE = 2,       /* negative size, or S%G, H%G, H_kv%G, H%H_kv != 0 */
   BASP_ERR_RANK = 3,        /* rank outside [0, G)                           */
-  BASP_ERR_UNSUPPORTED = 4, /* d, dtype or G outside what the kernels handle */
+  BASP_ERR_UNSUPPORTED = 4, /* d, dtype, G or size outside what the kernels handle */
   BASP_ERR_ALIGN = 5,       /* pointer not aligned as documented             */
   BASP_ERR_WORKSPACE = 6,   /* workspace smaller than the query reports      */
   BASP_ERR_HIP = 7,         /* a HIP launch failed                           */
@@ -85,7 +85,7 @@ int basp_group_of(int world, int micro_batch, int global_rank, int *group,
 
 /* Check a share's parameters (b, S, H, H_kv, d, G, rank) without touching
  * the GPU.  Returns BASP_OK or the code the other entry points would give
- * for the same shape (UNSUPPORTED when d is not 64 or 128). */
+ * for the same shape (UNSUPPORTED when d is not 64, 80, 96 or 128). */
 int basp_validate(int b, int S, int H, int H_kv, int d, int G, int rank);
 
 /* Receive side of the head-parallel all-to-all (Sec. II-C, Sec. IV-C):
@@ -138,8 +138,11 @@ int basp_a2a_unpack(const void *recv, void *own, int b, int S, int n_heads, int 
  * lse [b,H/G,S] fp32 out (kept for the backward).  bf16 MFMA products with
  * fp32 accumulation and an fp32 online softmax.
  * Alignment: q, k, v, o 16 bytes; lse 4 bytes.
- * Errors: NULL, SHAPE, UNSUPPORTED (d not 64 or 128, scale not finite and
- * positive, or S*(H/G)*d*2 >= 2^31 bytes), ALIGN, HIP. */
+ * Head dims 64, 80, 96 and 128 (the Table II models' hidden size / heads);
+ * 80 is computed at width 96 with zero padding, which changes nothing in the
+ * result.
+ * Errors: NULL, SHAPE, UNSUPPORTED (d not 64, 80, 96 or 128, scale not
+ * finite and positive, or S*(H/G)*d*2 >= 2^31 bytes), ALIGN, HIP. */
 int basp_attn_fwd(const void *q, const void *k, const void *v, void *o,
                   float *lse, int b, int S, int H, int H_kv, int d, int G,
                   float scale, void *stream);

@@ -28,7 +28,7 @@ int check_share(int b, int S, int H, int H_kv, int d, int G) {
 int check_attn(int b, int S, int H, int H_kv, int d, int G, float scale) {
   int rc = check_share(b, S, H, H_kv, d, G);
   if (rc) return rc;
-  if (d != 64 && d != 128) return BASP_ERR_UNSUPPORTED;
+  if (d != 64 && d != 80 && d != 96 && d != 128) return BASP_ERR_UNSUPPORTED;
   if (!(scale > 0.f) || !isfinite(scale)) return BASP_ERR_UNSUPPORTED;
   // Row indices inside the kernels are 32-bit: b*S must fit, and one head's
   // span of a tensor (S rows of H/G heads) is addressed with 31-bit offsets.
@@ -209,7 +209,7 @@ int basp_validate(int b, int S, int H, int H_kv, int d, int G, int rank) {
   int rc = check_share(b, S, H, H_kv, d, G);
   if (rc) return rc;
   if (rank < 0 || rank >= G) return BASP_ERR_RANK;
-  if (d != 64 && d != 128) return BASP_ERR_UNSUPPORTED;
+  if (d != 64 && d != 80 && d != 96 && d != 128) return BASP_ERR_UNSUPPORTED;
   if (G > BASP_MAX_GROUP) return BASP_ERR_UNSUPPORTED;
   return BASP_OK;
 }

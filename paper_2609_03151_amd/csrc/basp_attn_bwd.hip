@@ -97,12 +97,12 @@ __global__ __launch_bounds__(kPreThreads) void bwd_pre_kernel(
     const uint16_t *__restrict__ o, const uint16_t *__restrict__ d_o,
     const float *__restrict__ lse, f32x2 *__restrict__ ld, long long rows /* b*S*Hl */,
     int S, int Hl) {
-  constexpr int LPR = D / 8;  // lanes per row
+  constexpr int LPR = D <= 64 ? 8 : 16;  // lanes per row (a power of two >= D/8)
   const long long gid = (long long)blockIdx.x * kPreThreads + threadIdx.x;
   const long long r = gid / LPR;
   const int sub = (int)(gid % LPR);
   float acc = 0.f;
-  if (r < rows) {
+  if (r < rows && sub < D / 8) {
     const u32x4 a = reinterpret_cast<const u32x4 *>(o + r * D)[sub];
     const u32x4 b = reinterpret_cast<const u32x4 *>(d_o + r * D)[sub];
 #pragma unroll
@@ -141,12 +141,14 @@ enum KvGrad { kDV = 0, kDK = 1 };
 
 template <int D>
 struct KvCfg {
-  static constexpr int TILE_BYTES = kQM * D * 2;
+  static constexpr int DC = HeadDim<D>::DC;  // computed width (columns past D are zero)
+  static constexpr int LW = HeadDim<D>::LW;  // LDS row layout
+  static constexpr int TILE_BYTES = kQM * LW * 2;
   static constexpr int AUX_BYTES = 1024;  // (LSE2, D) of the step's rows (first 512 B)
   static constexpr int STAGE_BYTES = 2 * TILE_BYTES + AUX_BYTES;  // Q, dO, aux
-  static constexpr int NS = D / 16;
-  static constexpr int NE = D / 32;
-  static constexpr int CPR = D / 8;
+  static constexpr int NS = DC / 16;
+  static constexpr int NE = DC / 32;
+  static constexpr int CPR = LW / 8;
   static constexpr int DMA_PER_WAVE = kQM * CPR / kKvThreads;  // 1 KB copies per tile
 };
 
@@ -158,7 +160,7 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
     int n_rep, int kvheads_total, int ktiles, int nchunks, float c /* scale*log2e */,
     float out_scale) {
   using C = KvCfg<D>;
-  using T = LdsTile<D>;
+  using T = LdsTile<C::LW>;
   __shared__ __attribute__((aligned(16))) unsigned char smem[kStages * C::STAGE_BYTES];
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -196,12 +198,16 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
     const rsrc_t rk = make_rsrc(k + kvoff, (uint32_t)S * kv_row_bytes);
 #pragma unroll
     for (int s = 0; s < C::NS; ++s)
-      kf[s] = as_bf16x8(buf_load16(rk, (uint32_t)key * kv_row_bytes + (2 * s + hh) * 16));
+      kf[s] = 2 * s < D / 8
+                  ? as_bf16x8(buf_load16(rk, (uint32_t)key * kv_row_bytes + (2 * s + hh) * 16))
+                  : bf16x8{};  // columns past D
     if constexpr (G == kDK) {
       const rsrc_t rv = make_rsrc(v + kvoff, (uint32_t)S * kv_row_bytes);
 #pragma unroll
       for (int s = 0; s < C::NS; ++s)
-        vf[s] = as_bf16x8(buf_load16(rv, (uint32_t)key * kv_row_bytes + (2 * s + hh) * 16));
+        vf[s] = 2 * s < D / 8
+                    ? as_bf16x8(buf_load16(rv, (uint32_t)key * kv_row_bytes + (2 * s + hh) * 16))
+                    : bf16x8{};
     }
   }
   wait_vmcnt<0>();  // retire the tracked loads before untracked copies start
@@ -219,7 +225,7 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
   uint32_t g_off[C::DMA_PER_WAVE];
 #pragma unroll
   for (int i = 0; i < C::DMA_PER_WAVE; ++i)
-    g_off[i] = dma_src_off<D>((w * C::DMA_PER_WAVE + i) * 64 + lane, q_row_bytes);
+    g_off[i] = dma_src_off<C::LW, D>((w * C::DMA_PER_WAVE + i) * 64 + lane, q_row_bytes);
   // A of S^T (Q) and dP^T (dO): row l32 (+32 for the second half), chunk 2s + hh.
   int a_off[C::NS];
 #pragma unroll
@@ -233,7 +239,7 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
   for (int n = 0; n < C::NE; ++n)
 #pragma unroll
     for (int x = 0; x < 2; ++x) {
-      t_off[n][x] = tr_piece_off<D>(4 * hh + 8 * x, 32 * n + 16 * ((lane >> 4) & 1), lane);
+      t_off[n][x] = tr_piece_off<C::LW>(4 * hh + 8 * x, 32 * n + 16 * ((lane >> 4) & 1), lane);
       asm volatile("" : "+v"(t_off[n][x]));
     }
 
@@ -387,6 +393,7 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
     for (int n = 0; n < C::NE; ++n)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
+        if (32 * n + 8 * g >= D) continue;  // padding columns
         f32x4 a = {acc[n][4 * g] * out_scale, acc[n][4 * g + 1] * out_scale,
                    acc[n][4 * g + 2] * out_scale, acc[n][4 * g + 3] * out_scale};
         *reinterpret_cast<f32x4 *>(o + 32 * n + 8 * g + 4 * hh) = a;
@@ -426,11 +433,13 @@ constexpr int kDQN = 64;             // keys per tile
 
 template <int D>
 struct DqCfg {
-  static constexpr int TILE_BYTES = kDQN * D * 2;
+  static constexpr int DC = HeadDim<D>::DC;
+  static constexpr int LW = HeadDim<D>::LW;
+  static constexpr int TILE_BYTES = kDQN * LW * 2;
   static constexpr int STAGE_BYTES = 2 * TILE_BYTES;  // K, V
-  static constexpr int NS = D / 16;
-  static constexpr int NE = D / 32;
-  static constexpr int CPR = D / 8;
+  static constexpr int NS = DC / 16;
+  static constexpr int NE = DC / 32;
+  static constexpr int CPR = LW / 8;
   static constexpr int DMA_PER_WAVE = kDQN * CPR / kDqThreads;
 };
 
@@ -441,7 +450,7 @@ __global__ __launch_bounds__(kDqThreads, 1) void bwd_dq_kernel(
     const f32x2 *__restrict__ ld, float *__restrict__ dq, int S, int Hl, int Hkl, int n_rep,
     int heads_total, int qtiles, float c, float scale) {
   using C = DqCfg<D>;
-  using T = LdsTile<D>;
+  using T = LdsTile<C::LW>;
   __shared__ __attribute__((aligned(16))) unsigned char smem[kStages * C::STAGE_BYTES];
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -466,8 +475,13 @@ __global__ __launch_bounds__(kDqThreads, 1) void bwd_dq_kernel(
   bf16x8 qf[C::NS], df[C::NS];
 #pragma unroll
   for (int s = 0; s < C::NS; ++s) {
-    qf[s] = as_bf16x8(buf_load16(rq, (uint32_t)row * q_row_bytes + (2 * s + hh) * 16));
-    df[s] = as_bf16x8(buf_load16(rd, (uint32_t)row * q_row_bytes + (2 * s + hh) * 16));
+    if (2 * s < D / 8) {
+      qf[s] = as_bf16x8(buf_load16(rq, (uint32_t)row * q_row_bytes + (2 * s + hh) * 16));
+      df[s] = as_bf16x8(buf_load16(rd, (uint32_t)row * q_row_bytes + (2 * s + hh) * 16));
+    } else {  // columns past D
+      qf[s] = bf16x8{};
+      df[s] = bf16x8{};
+    }
   }
   f32x2 ldr = {INFINITY, 0.f};  // rows past S: P = 0
   if (row < S) ldr = ld[((size_t)beta * Hl + h) * S + row];
@@ -480,7 +494,7 @@ __global__ __launch_bounds__(kDqThreads, 1) void bwd_dq_kernel(
   uint32_t g_off[C::DMA_PER_WAVE];
 #pragma unroll
   for (int i = 0; i < C::DMA_PER_WAVE; ++i)
-    g_off[i] = dma_src_off<D>((w * C::DMA_PER_WAVE + i) * 64 + lane, kv_row_bytes);
+    g_off[i] = dma_src_off<C::LW, D>((w * C::DMA_PER_WAVE + i) * 64 + lane, kv_row_bytes);
   auto load_tile = [&](int t) __attribute__((always_inline)) {
     const uint32_t ks = smem_lds + (t % kStages) * C::STAGE_BYTES;
     const uint32_t base = (uint32_t)(t * kDQN) * kv_row_bytes;
@@ -509,7 +523,7 @@ __global__ __launch_bounds__(kDqThreads, 1) void bwd_dq_kernel(
   for (int n = 0; n < C::NE; ++n)
 #pragma unroll
     for (int x = 0; x < 2; ++x) {
-      t_off[n][x] = tr_piece_off<D>(4 * hh + 8 * x, 32 * n + 16 * ((lane >> 4) & 1), lane);
+      t_off[n][x] = tr_piece_off<C::LW>(4 * hh + 8 * x, 32 * n + 16 * ((lane >> 4) & 1), lane);
       asm volatile("" : "+v"(t_off[n][x]));
     }
 
@@ -600,6 +614,7 @@ __global__ __launch_bounds__(kDqThreads, 1) void bwd_dq_kernel(
     for (int n = 0; n < C::NE; ++n)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
+        if (32 * n + 8 * g >= D) continue;  // padding columns
         f32x4 a = {qacc[n][4 * g] * scale, qacc[n][4 * g + 1] * scale,
                    qacc[n][4 * g + 2] * scale, qacc[n][4 * g + 3] * scale};
         *reinterpret_cast<f32x4 *>(dqr + 32 * n + 8 * g + 4 * hh) = a;
@@ -621,7 +636,7 @@ hipError_t launch_bwd_d(const void *q, const void *k, const void *v, const void 
   const int n_rep = s.Hl / s.Hkl;
 
   const long long rows = (long long)s.b * s.S * s.Hl;
-  const long long pre_threads = rows * (D / 8);
+  const long long pre_threads = rows * (D <= 64 ? 8 : 16);
   const long long pre_blocks = (pre_threads + kPreThreads - 1) / kPreThreads;
   hipLaunchKernelGGL(bwd_pre_kernel<D>, dim3((unsigned)pre_blocks), dim3(kPreThreads), 0, stream,
                      op, dop, lse, ld, rows, s.S, s.Hl);
@@ -673,9 +688,12 @@ hipError_t launch_attn_bwd(const void *q, const void *k, const void *v,
                            const AttnShape &s, hipStream_t stream) {
   if ((long long)s.b * s.S == 0) return hipSuccess;
   float *ws = static_cast<float *>(workspace);
-  if (s.d == 128)
-    return launch_bwd_d<128>(q, k, v, o, lse, d_o, dq, dk, dv, ws, s, stream);
-  return launch_bwd_d<64>(q, k, v, o, lse, d_o, dq, dk, dv, ws, s, stream);
+  switch (s.d) {
+    case 64: return launch_bwd_d<64>(q, k, v, o, lse, d_o, dq, dk, dv, ws, s, stream);
+    case 80: return launch_bwd_d<80>(q, k, v, o, lse, d_o, dq, dk, dv, ws, s, stream);
+    case 96: return launch_bwd_d<96>(q, k, v, o, lse, d_o, dq, dk, dv, ws, s, stream);
+    default: return launch_bwd_d<128>(q, k, v, o, lse, d_o, dq, dk, dv, ws, s, stream);
+  }
 }
 
 }  // namespace basp

@@ -59,11 +59,13 @@ constexpr int kSchedDsRead = 0x100;
 
 template <int D>
 struct FwdCfg {
-  static constexpr int TILE_BYTES = kBN * D * 2;
+  static constexpr int DC = HeadDim<D>::DC;  // computed width (columns past D are zero)
+  static constexpr int LW = HeadDim<D>::LW;  // LDS row layout
+  static constexpr int TILE_BYTES = kBN * LW * 2;
   static constexpr int STAGE_BYTES = 2 * TILE_BYTES;  // K, V
-  static constexpr int NS = D / 16;                   // 16-deep steps over the head dim
-  static constexpr int NE = D / 32;                   // 32-wide head-dim subtiles of O
-  static constexpr int CPR = D / 8;                   // 16-byte chunks per row
+  static constexpr int NS = DC / 16;                  // 16-deep steps over the head dim
+  static constexpr int NE = DC / 32;                  // 32-wide head-dim subtiles of O
+  static constexpr int CPR = LW / 8;                  // 16-byte chunk slots per LDS row
   static constexpr int DMA_PER_WAVE = kBN * CPR / kThreads;  // 1 KB loads per wave per tensor
 };
 
@@ -74,7 +76,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
     float *__restrict__ lse, int S, int Hl, int Hkl, int n_rep, int heads_total,
     int qtiles, float c /* scale * log2(e) */) {
   using C = FwdCfg<D>;
-  using T = LdsTile<D>;
+  using T = LdsTile<C::LW>;
   __shared__ __attribute__((aligned(16))) unsigned char smem[kStages * C::STAGE_BYTES];
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -99,7 +101,8 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
   bf16x8 qf[C::NS];
 #pragma unroll
   for (int s = 0; s < C::NS; ++s)
-    qf[s] = as_bf16x8(buf_load16(rq, (uint32_t)row * q_row_bytes + (2 * s + hh) * 16));
+    qf[s] = 2 * s < D / 8 ? as_bf16x8(buf_load16(rq, (uint32_t)row * q_row_bytes + (2 * s + hh) * 16))
+                          : bf16x8{};  // columns past D
   // Retire the Q loads before any tile copy is in flight: the compiler does
   // not count the copies, and a wait for Q inside the tile loop would also
   // drain the prefetched tiles.
@@ -111,7 +114,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
   uint32_t g_off[C::DMA_PER_WAVE];
 #pragma unroll
   for (int i = 0; i < C::DMA_PER_WAVE; ++i)
-    g_off[i] = dma_src_off<D>((w * C::DMA_PER_WAVE + i) * 64 + lane, kv_row_bytes);
+    g_off[i] = dma_src_off<C::LW, D>((w * C::DMA_PER_WAVE + i) * 64 + lane, kv_row_bytes);
   auto load_tile = [&](int t) {  // issue; lands asynchronously in stage t % kStages
     const uint32_t ks = smem_lds + (t % kStages) * C::STAGE_BYTES;
     const uint32_t base = (uint32_t)(t * kBN) * kv_row_bytes;
@@ -147,7 +150,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
   for (int n = 0; n < C::NE; ++n)
 #pragma unroll
     for (int x = 0; x < 2; ++x) {
-      v_off[n][x] = tr_piece_off<D>(4 * hh + 8 * x, 32 * n + 16 * ((lane >> 4) & 1), lane);
+      v_off[n][x] = tr_piece_off<C::LW>(4 * hh + 8 * x, 32 * n + 16 * ((lane >> 4) & 1), lane);
       asm volatile("" : "+v"(v_off[n][x]));
     }
 
@@ -284,6 +287,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
     for (int n = 0; n < C::NE; ++n)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
+        if (32 * n + 8 * g >= D) continue;  // padding columns
         u32x2 val = {pack_bf16x2(oacc[n][4 * g] * inv, oacc[n][4 * g + 1] * inv),
                      pack_bf16x2(oacc[n][4 * g + 2] * inv, oacc[n][4 * g + 3] * inv)};
         *reinterpret_cast<u32x2 *>(ob + 32 * n + 8 * g + 4 * hh) = val;
@@ -307,12 +311,16 @@ hipError_t launch_attn_fwd(const void *q, const void *k, const void *v, void *o,
   auto *kp = static_cast<const uint16_t *>(k);
   auto *vp = static_cast<const uint16_t *>(v);
   auto *op = static_cast<uint16_t *>(o);
-  if (s.d == 128)
-    hipLaunchKernelGGL(attn_fwd_kernel<128>, dim3((unsigned)blocks), dim3(kThreads), 0, stream,
-                       qp, kp, vp, op, lse, s.S, s.Hl, s.Hkl, n_rep, heads_total, qtiles, c);
-  else
-    hipLaunchKernelGGL(attn_fwd_kernel<64>, dim3((unsigned)blocks), dim3(kThreads), 0, stream,
-                       qp, kp, vp, op, lse, s.S, s.Hl, s.Hkl, n_rep, heads_total, qtiles, c);
+  auto go = [&](auto kernel) {
+    hipLaunchKernelGGL(kernel, dim3((unsigned)blocks), dim3(kThreads), 0, stream, qp, kp, vp, op,
+                       lse, s.S, s.Hl, s.Hkl, n_rep, heads_total, qtiles, c);
+  };
+  switch (s.d) {
+    case 64: go(attn_fwd_kernel<64>); break;
+    case 80: go(attn_fwd_kernel<80>); break;
+    case 96: go(attn_fwd_kernel<96>); break;
+    default: go(attn_fwd_kernel<128>); break;
+  }
   return hipGetLastError();
 }
 

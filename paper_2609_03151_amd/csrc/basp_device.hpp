@@ -162,16 +162,47 @@ struct LdsTile<64> {
   }
 };
 
+// Head dims the attention kernels take, with the width their MFMA tiles
+// compute at (DC, a multiple of 32) and the LDS row layout they use (LW):
+// 80 and 96 compute at 96, kept in the 128-wide layout; the columns past D
+// are zeros everywhere they enter a product.
+template <int D>
+struct HeadDim;
+template <>
+struct HeadDim<64> {
+  static constexpr int DC = 64, LW = 64;
+};
+template <>
+struct HeadDim<80> {
+  static constexpr int DC = 96, LW = 128;
+};
+template <>
+struct HeadDim<96> {
+  static constexpr int DC = 96, LW = 128;
+};
+template <>
+struct HeadDim<128> {
+  static constexpr int DC = 128, LW = 128;
+};
+
+// A buffer offset no resource of the library reaches (ranges stay below
+// 2^31): loads from it return zeros.
+constexpr uint32_t kZeroOffset = 0x80000000u;
+
 // Source offset, within a tile of rows `row_bytes` apart in memory, of the
 // 16-byte chunk that a linear LDS copy places at chunk slot `pos` of an
-// LdsTile<D>: slot pos holds row pos / (D/8), stored chunk pos % (D/8), i.e.
-// logical chunk (stored chunk) ^ swz(row).  Copying chunk slots in order with
-// buf_load16_lds therefore leaves the tile in its swizzled layout.
-template <int D>
+// LdsTile<LW>: slot pos holds row pos / (LW/8), stored chunk pos % (LW/8),
+// i.e. logical chunk (stored chunk) ^ swz(row).  Copying chunk slots in order
+// with buf_load16_lds_async therefore leaves the tile in its swizzled layout.
+// Logical chunks past the row's D elements read from kZeroOffset, so the
+// padding columns of the tile are zeros.
+template <int LW, int D = LW>
 __device__ __forceinline__ uint32_t dma_src_off(int pos, uint32_t row_bytes) {
-  constexpr int CPR = D / 8;
+  constexpr int CPR = LW / 8;
   const int r = pos / CPR, pc = pos % CPR;
-  return (uint32_t)r * row_bytes + ((pc ^ LdsTile<D>::swz(r)) << 4);
+  const int lc = pc ^ LdsTile<LW>::swz(r);
+  if (D < LW && lc >= D / 8) return kZeroOffset;
+  return (uint32_t)r * row_bytes + (lc << 4);
 }
 
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;

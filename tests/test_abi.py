@@ -62,7 +62,10 @@ def test_group_of_matches_paper_example_and_errors():
     ((1, 512, 12, 8, 64, 4, 0), SHAPE),      # H % H_kv
     ((1, 512, 8, 8, 64, 2, 2), RANK),
     ((1, 512, 8, 8, 64, 2, -1), RANK),
-    ((1, 512, 8, 8, 96, 2, 0), UNSUP),       # head dim
+    ((1, 512, 8, 8, 96, 2, 0), OK),          # head dims of Table II
+    ((1, 512, 8, 8, 80, 2, 0), OK),
+    ((1, 512, 8, 8, 72, 2, 0), UNSUP),       # head dim
+    ((1, 512, 8, 8, 256, 2, 0), UNSUP),
 ])
 def test_validate(args, code):
     assert basp.validate(*args) == code
@@ -140,7 +143,8 @@ def test_attn_rejects_before_any_hip_call():
     L = basp.lib()
     p = [_fake(0x10000 * (i + 1)) for i in range(10)]
     fwd = lambda *a, ptrs=p[:5], scale=0.125: L.basp_attn_fwd(*ptrs, *a, ctypes.c_float(scale), None)
-    assert fwd(1, 128, 8, 2, 96, 2) == UNSUP
+    assert fwd(1, 128, 8, 2, 72, 2) == UNSUP
+    assert fwd(1, 128, 8, 2, 48, 2) == UNSUP
     assert fwd(1, 128, 8, 2, 128, 2, scale=0.0) == UNSUP
     assert fwd(1, 128, 8, 2, 128, 2, scale=float("nan")) == UNSUP
     assert fwd(1, 127, 8, 2, 128, 2) == SHAPE

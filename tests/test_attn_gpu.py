@@ -54,6 +54,10 @@ SMALL = [  # b, S, Hl, Hkl, d
     (1, 2048, 4, 1, 128),    # 16 row tiles, 32 key tiles
     (1, 2500, 2, 1, 128),    # dK/dV rows split into 2 chunks, ragged tail
     (1, 4096, 4, 2, 64),     # 2 chunks, d = 64
+    (1, 384, 8, 2, 96),      # d = 96 (Table II: 3072 / 32), GQA 4
+    (1, 1000, 4, 1, 96),     # d = 96, ragged tail
+    (2, 300, 3, 3, 80),      # d = 80 (Table II: 2560 / 32), computed at 96, ragged
+    (1, 2500, 2, 1, 80),     # d = 80, 2 chunks, ragged tail
 ]
 
 
@@ -135,7 +139,7 @@ def test_bitwise_deterministic():
 
 
 FULL = ["llama3_8b_s32k", "qwen25_7b_s64k", "ulysses_g8_b2_s64k", "basp_g4_b1_s64k",
-        "llama3_70b_s128k"]
+        "llama3_70b_s128k", "llama32_3b_s16k", "qwen25_3b_s16k"]
 
 
 def _sample_rows(S, rng, n=40):
