@@ -53,6 +53,7 @@ def lib():
     L.oracle_seq_partition.argtypes = [c_long, c_long, c_long, lp, lp, lp, lp]
     L.oracle_pack.argtypes = [ctypes.POINTER(vp), vp] + [c_long] * 7
     L.oracle_unpack.argtypes = [vp, ctypes.POINTER(vp)] + [c_long] * 7
+    L.oracle_unpack_add.argtypes = [vp, ctypes.POINTER(vp)] + [c_long] * 6
     L.oracle_a2a_pack.argtypes = [vp, vp] + [c_long] * 6
     L.oracle_a2a_unpack.argtypes = [vp, vp] + [c_long] * 6
     L.oracle_attn_fwd.argtypes = [vp] * 5 + [c_long] * 5 + [c_double, c_long, c_long]
@@ -128,7 +129,8 @@ def pack(shards, rank: int) -> np.ndarray:
     for a in arrs:
         if a.shape != arrs[0].shape or a.dtype != arrs[0].dtype:
             raise OracleError("shards differ in shape or dtype")
-    out = np.empty((b, Sg * G, n // G if n % G == 0 else 0, d), dtype=arrs[0].dtype)
+    nl = n // G if n % G == 0 else (1 if (n < G and G % n == 0) else 0)
+    out = np.empty((b, Sg * G, nl, d), dtype=arrs[0].dtype)
     ptrs = (ctypes.c_void_p * G)(*[a.ctypes.data for a in arrs])
     rc = lib().oracle_pack(ptrs, _ptr(out), b, Sg * G, n, d, G, rank,
                            arrs[0].dtype.itemsize)
@@ -159,21 +161,44 @@ def a2a_pack(own, G: int) -> np.ndarray:
     """Own shard [b, S/G, n, d] -> send buffer [G, b, S/G, n/G, d] (raw bytes)."""
     src = _np(own)
     b, Sg, n, d = src.shape
-    out = np.empty((G, b, Sg, n // G if n % G == 0 else 0, d), dtype=src.dtype)
+    nl = n // G if n % G == 0 else (1 if (n < G and G % n == 0) else 0)
+    out = np.empty((G, b, Sg, nl, d), dtype=src.dtype)
     rc = lib().oracle_a2a_pack(_ptr(src), _ptr(out), b, Sg * G, n, d, G, src.dtype.itemsize)
     _check(rc, "a2a_pack")
     return out
 
 
-def a2a_unpack(recv) -> np.ndarray:
-    """Received blocks [G, b, S/G, n/G, d] -> own shard [b, S/G, n, d] (raw bytes)."""
+def a2a_unpack(recv, n_heads: int | None = None) -> np.ndarray:
+    """Received blocks [G, b, S/G, n/G, d] -> own shard [b, S/G, n, d] (raw bytes).
+
+    ``n_heads`` < G (shared heads, fp32): blocks [G, b, S/G, 1, d] are summed per head."""
     src = _np(recv)
     G, b, Sg, nl, d = src.shape
-    out = np.empty((b, Sg, G * nl, d), dtype=src.dtype)
-    rc = lib().oracle_a2a_unpack(_ptr(src), _ptr(out), b, Sg * G, G * nl, d, G,
+    n = G * nl if n_heads is None else n_heads
+    out = np.empty((b, Sg, n, d), dtype=src.dtype)
+    rc = lib().oracle_a2a_unpack(_ptr(src), _ptr(out), b, Sg * G, n, d, G,
                                  src.dtype.itemsize)
     _check(rc, "a2a_unpack")
     return out
+
+
+def unpack_add(local, shards, rank: int):
+    """fp32: add local [b, S, nl, d] into the rank's head slice of the G shards
+    (numpy float32 arrays, modified in place); nl = n/G, or 1 for a shared head."""
+    src = np.ascontiguousarray(_np(local), dtype=np.float32)
+    G = len(shards)
+    b, Sg, n, d = shards[0].shape
+    for a in shards:
+        if not (isinstance(a, np.ndarray) and a.flags.c_contiguous and a.dtype == np.float32):
+            raise OracleError("unpack_add targets must be C-contiguous float32 numpy arrays")
+    ptrs = (ctypes.c_void_p * G)(*[a.ctypes.data for a in shards])
+    rc = lib().oracle_unpack_add(_ptr(src), ptrs, b, Sg * G, n, d, G, rank)
+    _check(rc, "unpack_add")
+    return shards
+
+
+def heads_per_member(n: int, G: int) -> int:
+    return n // G if n >= G else 1
 
 
 # -------------------------------------------------------------- attention

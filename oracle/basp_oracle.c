@@ -84,10 +84,18 @@ int oracle_seq_partition(long L, long K, long global_rank, long *seq_start,
 }
 
 /* ------------------------------------------------------- pack / unpack */
+/* Heads of a tensor with n heads that group member j handles: n/G of them
+ * from j*n/G when G divides n; when n < G and n divides G (fewer kv heads
+ * than members), the single head j*n/G (integer division), shared by the
+ * G/n members j with the same quotient. */
+static long first_head(long n, long G, long j) { return j * n / G; }
+static long heads_per_member(long n, long G) { return n >= G ? n / G : 1; }
+
 static int perm_args_ok(long b, long S, long n, long d, long G, long rank,
                         long elem) {
   if (b < 0 || S < 0 || n < 1 || d < 1 || G < 1) return ORC_ERR_SHAPE;
-  if (S % G != 0 || n % G != 0) return ORC_ERR_SHAPE;
+  if (S % G != 0) return ORC_ERR_SHAPE;
+  if (!(n % G == 0 || (n < G && G % n == 0))) return ORC_ERR_SHAPE;
   if (rank < 0 || rank >= G) return ORC_ERR_RANK;
   if (elem != 2 && elem != 4) return ORC_ERR_ELEM;
   return ORC_OK;
@@ -98,7 +106,7 @@ int oracle_pack(const void *const *src, void *dst, long b, long S, long n,
   int rc = perm_args_ok(b, S, n, d, G, rank, elem);
   if (rc) return rc;
   if (!src || !dst) return ORC_ERR_NULL;
-  long Sg = S / G, nl = n / G;
+  long Sg = S / G, nl = heads_per_member(n, G), h0 = first_head(n, G, rank);
   for (long j = 0; j < G; ++j) {
     const unsigned char *s = (const unsigned char *)src[j];
     if (!s) return ORC_ERR_NULL;
@@ -106,7 +114,7 @@ int oracle_pack(const void *const *src, void *dst, long b, long S, long n,
       for (long t = 0; t < Sg; ++t)
         for (long h = 0; h < nl; ++h)
           for (long e = 0; e < d; ++e) {
-            long from = ((beta * Sg + t) * n + (rank * nl + h)) * d + e;
+            long from = ((beta * Sg + t) * n + (h0 + h)) * d + e;
             long to = ((beta * S + (j * Sg + t)) * nl + h) * d + e;
             memcpy((unsigned char *)dst + to * elem, s + from * elem,
                    (size_t)elem);
@@ -120,6 +128,7 @@ int oracle_unpack(const void *src, void *const *dst, long b, long S, long n,
   int rc = perm_args_ok(b, S, n, d, G, rank, elem);
   if (rc) return rc;
   if (!src || !dst) return ORC_ERR_NULL;
+  if (n < G) return ORC_ERR_SHAPE; /* a shared head takes oracle_unpack_add */
   long Sg = S / G, nl = n / G;
   for (long j = 0; j < G; ++j) {
     unsigned char *o = (unsigned char *)dst[j];
@@ -137,18 +146,39 @@ int oracle_unpack(const void *src, void *const *dst, long b, long S, long n,
   return ORC_OK;
 }
 
+int oracle_unpack_add(const float *src, float *const *dst, long b, long S, long n,
+                      long d, long G, long rank) {
+  int rc = perm_args_ok(b, S, n, d, G, rank, 4);
+  if (rc) return rc;
+  if (!src || !dst) return ORC_ERR_NULL;
+  long Sg = S / G, nl = heads_per_member(n, G), h0 = first_head(n, G, rank);
+  for (long j = 0; j < G; ++j) {
+    float *o = dst[j];
+    if (!o) return ORC_ERR_NULL;
+    for (long beta = 0; beta < b; ++beta)
+      for (long t = 0; t < Sg; ++t)
+        for (long h = 0; h < nl; ++h)
+          for (long e = 0; e < d; ++e) {
+            long from = ((beta * S + (j * Sg + t)) * nl + h) * d + e;
+            long to = ((beta * Sg + t) * n + (h0 + h)) * d + e;
+            o[to] = o[to] + src[from];
+          }
+  }
+  return ORC_OK;
+}
+
 int oracle_a2a_pack(const void *own, void *send, long b, long S, long n,
                     long d, long G, long elem) {
   int rc = perm_args_ok(b, S, n, d, G, 0, elem);
   if (rc) return rc;
   if (!own || !send) return ORC_ERR_NULL;
-  long Sg = S / G, nl = n / G;
+  long Sg = S / G, nl = heads_per_member(n, G);
   for (long j = 0; j < G; ++j)
     for (long beta = 0; beta < b; ++beta)
       for (long t = 0; t < Sg; ++t)
         for (long h = 0; h < nl; ++h)
           for (long e = 0; e < d; ++e) {
-            long from = ((beta * Sg + t) * n + (j * nl + h)) * d + e;
+            long from = ((beta * Sg + t) * n + (first_head(n, G, j) + h)) * d + e;
             long to = (((j * b + beta) * Sg + t) * nl + h) * d + e;
             memcpy((unsigned char *)send + to * elem,
                    (const unsigned char *)own + from * elem, (size_t)elem);
@@ -161,7 +191,30 @@ int oracle_a2a_unpack(const void *recv, void *own, long b, long S, long n,
   int rc = perm_args_ok(b, S, n, d, G, 0, elem);
   if (rc) return rc;
   if (!recv || !own) return ORC_ERR_NULL;
-  long Sg = S / G, nl = n / G;
+  long Sg = S / G;
+  if (n < G) {
+    /* Shared heads: head h is the sum of the blocks of its G/n members, in
+     * member order (fp32 partial gradients). */
+    if (elem != 4) return ORC_ERR_ELEM;
+    const float *r = (const float *)recv;
+    float *o = (float *)own;
+    for (long h = 0; h < n; ++h)
+      for (long beta = 0; beta < b; ++beta)
+        for (long t = 0; t < Sg; ++t)
+          for (long e = 0; e < d; ++e) {
+            float acc = 0.0f;
+            int first = 1;
+            for (long j = 0; j < G; ++j) {
+              if (first_head(n, G, j) != h) continue;
+              float x = r[((j * b + beta) * Sg + t) * d + e];
+              acc = first ? x : acc + x;
+              first = 0;
+            }
+            o[((beta * Sg + t) * n + h) * d + e] = acc;
+          }
+    return ORC_OK;
+  }
+  long nl = n / G;
   for (long j = 0; j < G; ++j)
     for (long beta = 0; beta < b; ++beta)
       for (long t = 0; t < Sg; ++t)

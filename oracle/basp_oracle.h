@@ -37,14 +37,25 @@ int oracle_seq_partition(long L, long K, long global_rank,
 int oracle_pack(const void *const *src, void *dst, long b, long S, long n,
                 long d, long G, long rank, long elem);
 
-/* Inverse on the rank's head slice; every other head of dst_j is untouched. */
+/* Inverse on the rank's head slice; every other head of dst_j is untouched.
+ * Needs G | n. */
 int oracle_unpack(const void *src, void *const *dst, long b, long S, long n,
                   long d, long G, long rank, long elem);
+
+/* Head slices: with G | n, member `rank` handles heads [rank*n/G, +n/G);
+ * with n < G and n | G (fewer kv heads than members, Sec. II-A's GQA under
+ * Ulysses' head split), the one head rank*n/G, shared by G/n members.
+ * oracle_pack above follows this rule.  The fp32 variant of unpack that
+ * adds the rank's part into the shards, for gradients of a shared head:
+ *   dst_j[beta][t][h0 + h][e] += src[beta][j*S/G + t][h][e]. */
+int oracle_unpack_add(const float *src, float *const *dst, long b, long S,
+                      long n, long d, long G, long rank);
 
 /* Send side of the all-to-all, on the owner of a sequence shard (Sec. II-C:
  * each member sends every other member its share of the heads): the own
  * shard [b, S/G, n, d], all heads, split by destination member j into
- *   send[j][beta][t][h][e] = own[beta][t][j*n/G + h][e],  send [G, b, S/G, n/G, d].
+ *   send[j][beta][t][h][e] = own[beta][t][j*n/G + h][e],  send [G, b, S/G, n/G, d]
+ * (with n < G: the one head j*n/G, send [G, b, S/G, 1, d]).
  * elem = bytes per element (2 or 4); copied as raw bytes. */
 int oracle_a2a_pack(const void *own, void *send, long b, long S, long n,
                     long d, long G, long elem);
@@ -52,7 +63,9 @@ int oracle_a2a_pack(const void *own, void *send, long b, long S, long n,
 /* Receive side of the reverse all-to-all (the output goes back to the
  * sequence owners): block j, the heads [j*n/G, (j+1)*n/G) member j computed,
  * into the own shard:
- *   own[beta][t][j*n/G + h][e] = recv[j][beta][t][h][e],  recv [G, b, S/G, n/G, d]. */
+ *   own[beta][t][j*n/G + h][e] = recv[j][beta][t][h][e],  recv [G, b, S/G, n/G, d].
+ * With n < G (fp32 only): head h is the sum, in member order, of the blocks
+ * of the G/n members that share it. */
 int oracle_a2a_unpack(const void *recv, void *own, long b, long S, long n,
                       long d, long G, long elem);
 
