@@ -75,7 +75,10 @@ def cpu_baseline(w, target_s: float):
     from synth_inputs import global_tensors, shards_of
 
     q, k, v, do = global_tensors(w)
-    loc = lambda x, n: x[w.seq_offset:w.seq_offset + 1, :, w.rank * (n // w.G):(w.rank + 1) * (n // w.G)]
+    def loc(x, n):
+        h0, nl = w.first_head(n), (n // w.G if n >= w.G else 1)
+        return x[w.seq_offset:w.seq_offset + 1, :, h0:h0 + nl]
+
     ql, kl, vl, dl = loc(q, w.H), loc(k, w.H_kv), loc(v, w.H_kv), loc(do, w.H)
 
     def run(Sp):

@@ -14,6 +14,7 @@
  *   basp_attn_fwd  causal GQA attention on the rank's H/G query heads
  *   basp_attn_bwd  its backward (dQ, dK, dV in fp32)
  *   basp_unpack    head-sharded result -> the rank's head slice of G shards
+ *   basp_unpack_add  the same for fp32 gradients, added into the shards
  *   basp_a2a_pack / basp_a2a_unpack   the owner's side of the same exchanges:
  *                  own shard <-> one contiguous block per member
  *
@@ -23,11 +24,18 @@
  * ---------------------------------------
  * Shapes (row-major, innermost last; "n" is the global head count of the
  * tensor at hand: H for Q, O, dO, dQ and H_kv for K, V, dK, dV):
- *   sequence shard j      [b, S/G, n,   d]   tokens [j*S/G, (j+1)*S/G)
- *   head-sharded local    [b, S,   n/G, d]   heads  [rank*n/G, (rank+1)*n/G)
- *   LSE                   [b, H/G, S]        fp32, natural logarithm
- * GQA: local query head h attends with local kv head h / (H/H_kv); the
- * rank's kv heads are the contiguous block [rank*H_kv/G, (rank+1)*H_kv/G).
+ *   sequence shard j      [b, S/G, n,  d]   tokens [j*S/G, (j+1)*S/G)
+ *   head-sharded local    [b, S,   nl, d]   heads  [rank*n/G, rank*n/G + nl)
+ *   LSE                   [b, H/G, S]       fp32, natural logarithm
+ * where nl = n/G when G divides n.  A GQA model may have fewer kv heads
+ * than the group has members (Sec. II-A; e.g. 8 kv heads and G = 16): when
+ * n < G and G is a multiple of n, nl = 1 and member rank takes the single
+ * head rank*n/G (integer division), which the G/n members
+ * [h*G/n, (h+1)*G/n) share.  Their gradients of that head are partial sums
+ * that must be added, not copied: basp_unpack_add and basp_a2a_unpack do
+ * that in fp32; basp_unpack refuses such a tensor.
+ * GQA: local query head h attends with local kv head h / (H/H_kv) (with one
+ * shared kv head, every local query head uses it).
  * Attention is causal (key j is visible to query i iff j <= i, top-left
  * aligned, S queries and S keys), softmax scale is the caller's `scale`
  * (1/sqrt(d) for the usual scaled dot product of Sec. II-A).
@@ -58,7 +66,8 @@ extern "C" {
 typedef enum basp_status {
   BASP_OK = 0,
   BASP_ERR_NULL = 1,        /* a required pointer is NULL                    */
-  BASP_ERR_SHAPE = 2,       /* negative size, or S%G, H%G, H_kv%G, H%H_kv != 0 */
+  BASP_ERR_SHAPE = 2,       /* negative size, S%G or H%G != 0, H_kv neither a
+                               multiple nor a divisor of G, or H%H_kv != 0   */
   BASP_ERR_RANK = 3,        /* rank outside [0, G)                           */
   BASP_ERR_UNSUPPORTED = 4, /* d, dtype, G or size outside what the kernels handle */
   BASP_ERR_ALIGN = 5,       /* pointer not aligned as documented             */
@@ -91,11 +100,13 @@ int basp_validate(int b, int S, int H, int H_kv, int d, int G, int rank);
 /* Receive side of the head-parallel all-to-all (Sec. II-C, Sec. IV-C):
  *   dst[beta][j*S/G + t][h][e] = src_shards[j][beta][t][rank*n/G + h][e]
  * src_shards: host array of G device pointers, each [b, S/G, n, d];
- * dst: device [b, S, n/G, d].  dtype selects 2-byte (BASP_BF16) or 4-byte
- * (BASP_F32) elements; values are copied bit for bit.
+ * dst: device [b, S, nl, d] (nl as above; a shared head is copied to each
+ * of its members).  dtype selects 2-byte (BASP_BF16) or 4-byte (BASP_F32)
+ * elements; values are copied bit for bit.
  * Alignment: every pointer aligned to the element size.
- * Errors: NULL, SHAPE, RANK, UNSUPPORTED (dtype, G > BASP_MAX_GROUP,
- * (S/G)*(n/G)*d >= 2^31 elements, or b*G > 65535), ALIGN, HIP. */
+ * Errors: NULL, SHAPE (S % G, or n neither a multiple nor a divisor of G),
+ * RANK, UNSUPPORTED (dtype, G > BASP_MAX_GROUP, (S/G)*nl*d >= 2^31 elements,
+ * or b*G > 65535), ALIGN, HIP. */
 int basp_pack(const void *const *src_shards, void *dst, int b, int S,
               int n_heads, int d, int G, int rank, int dtype, void *stream);
 
@@ -103,9 +114,23 @@ int basp_pack(const void *const *src_shards, void *dst, int b, int S,
  * all-to-all returns the attention output to the sequence owners):
  *   dst_shards[j][beta][t][rank*n/G + h][e] = src[beta][j*S/G + t][h][e]
  * Heads outside [rank*n/G, (rank+1)*n/G) of every dst shard are left
- * untouched.  Arguments and errors as basp_pack. */
+ * untouched.  Arguments and errors as basp_pack, plus SHAPE when n < G (a
+ * shared head takes basp_unpack_add). */
 int basp_unpack(const void *src, void *const *dst_shards, int b, int S,
                 int n_heads, int d, int G, int rank, int dtype, void *stream);
+
+/* Gradient form of basp_unpack, fp32 only: the rank's rows are added into
+ * the shards instead of written,
+ *   dst_shards[j][beta][t][rank*n/G + h][e] += src[beta][j*S/G + t][h][e]
+ * so that the G/n members sharing a kv head (n < G, Sec. II-A GQA under the
+ * head split of Sec. II-C) accumulate dK and dV of that head; with n a
+ * multiple of G it adds the rank's disjoint slice.  The caller clears the
+ * shards first; calls for members that share a head must not overlap on
+ * the device (each reads and writes the same rows; issue them in member
+ * order on one stream for a deterministic sum).  src: device [b, S, nl, d]
+ * fp32; shards as basp_pack with 4-byte elements.  Errors as basp_pack. */
+int basp_unpack_add(const float *src, float *const *dst_shards, int b, int S,
+                    int n_heads, int d, int G, int rank, void *stream);
 
 /* Send side of the first all-to-all, on the owner of a sequence shard
  * (Sec. II-C: every member sends each other member that member's share of
@@ -116,8 +141,9 @@ int basp_unpack(const void *src, void *const *dst_shards, int b, int S,
  * one contiguous run of b*(S/G)*(n/G)*d elements for the exchange.  With the
  * blocks of every member received, the head-sharded tensor basp_pack builds
  * is block j at rows j*S/G .. of each sequence (for b = 1, the received
- * buffer itself).  dtype as basp_pack; values copied bit for bit.
- * Errors: NULL, SHAPE (S % G, n % G), UNSUPPORTED (as basp_pack), ALIGN, HIP. */
+ * buffer itself).  With n < G, block j holds the one head j*n/G
+ * (send [G, b, S/G, 1, d]).  dtype as basp_pack; values copied bit for bit.
+ * Errors: NULL, SHAPE (as basp_pack), UNSUPPORTED (as basp_pack), ALIGN, HIP. */
 int basp_a2a_pack(const void *own, void *send, int b, int S, int n_heads, int d,
                   int G, int dtype, void *stream);
 
@@ -125,8 +151,12 @@ int basp_a2a_pack(const void *own, void *send, int b, int S, int n_heads, int d,
  * the sequence owners): block j, received from member j and holding heads
  * [j*n/G, (j+1)*n/G) of the own tokens, into the own shard:
  *   own[beta][t][j*n/G + h][e] = recv[j][beta][t][h][e]
- * recv: device [G, b, S/G, n/G, d]; own: device [b, S/G, n, d].  Arguments
- * and errors as basp_a2a_pack. */
+ * recv: device [G, b, S/G, n/G, d]; own: device [b, S/G, n, d].  With n < G
+ * (gradients of shared kv heads, fp32 only) recv is [G, b, S/G, 1, d] and
+ * each head is the sum of its members' blocks, taken in member order:
+ *   own[beta][t][h][e] = recv[h*G/n][..] + recv[h*G/n + 1][..] + ...
+ * Arguments and errors as basp_a2a_pack, plus UNSUPPORTED for a bf16 tensor
+ * with n < G. */
 int basp_a2a_unpack(const void *recv, void *own, int b, int S, int n_heads, int d,
                     int G, int dtype, void *stream);
 
@@ -134,7 +164,8 @@ int basp_a2a_unpack(const void *recv, void *own, int b, int S, int n_heads, int 
  * for the rank's H/G query heads:
  *   O_i = sum_{j<=i} softmax_j(scale * q_i . k_j) v_j,
  *   LSE_i = log sum_{j<=i} exp(scale * q_i . k_j).
- * q [b,S,H/G,d], k/v [b,S,H_kv/G,d] bf16 in; o [b,S,H/G,d] bf16 out,
+ * q [b,S,H/G,d], k/v [b,S,Hkl,d] bf16 in (Hkl = H_kv/G, or 1 when H_kv < G
+ * divides G); o [b,S,H/G,d] bf16 out,
  * lse [b,H/G,S] fp32 out (kept for the backward).  bf16 MFMA products with
  * fp32 accumulation and an fp32 online softmax.
  * Alignment: q, k, v, o 16 bytes; lse 4 bytes.
@@ -153,8 +184,9 @@ size_t basp_attn_bwd_workspace_bytes(int b, int S, int H, int H_kv, int d,
 
 /* Backward of basp_attn_fwd for the loss sum(O * dO): inputs q, k, v, o, d_o
  * (bf16, layouts as above) and lse from the forward; outputs
- * dq [b,S,H/G,d], dk/dv [b,S,H_kv/G,d] in fp32, each fully overwritten
- * (dk/dv sum over the H/H_kv query heads sharing a kv head).  workspace:
+ * dq [b,S,H/G,d], dk/dv [b,S,Hkl,d] in fp32, each fully overwritten
+ * (dk/dv sum over the rank's query heads sharing a kv head; with a kv head
+ * shared by several members these are that member's part).  workspace:
  * device buffer of at least basp_attn_bwd_workspace_bytes(), 16-byte
  * aligned, contents ignored on entry and undefined on return.  Results are
  * deterministic (no atomics).

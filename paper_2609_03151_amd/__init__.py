@@ -27,7 +27,7 @@ STATUS = {
 }
 # Every symbol include/basp.h declares.
 EXPORTS = ("basp_status_str", "basp_group_of", "basp_validate", "basp_pack",
-           "basp_unpack", "basp_a2a_pack", "basp_a2a_unpack", "basp_attn_fwd",
+           "basp_unpack", "basp_unpack_add", "basp_a2a_pack", "basp_a2a_unpack", "basp_attn_fwd",
            "basp_attn_bwd_workspace_bytes", "basp_attn_bwd")
 
 
@@ -58,6 +58,7 @@ def lib() -> ctypes.CDLL:
     L.basp_validate.argtypes = [i] * 7
     L.basp_pack.argtypes = [ctypes.POINTER(vp), vp] + [i] * 7 + [vp]
     L.basp_unpack.argtypes = [vp, ctypes.POINTER(vp)] + [i] * 7 + [vp]
+    L.basp_unpack_add.argtypes = [vp, ctypes.POINTER(vp)] + [i] * 6 + [vp]
     L.basp_a2a_pack.argtypes = [vp, vp] + [i] * 6 + [vp]
     L.basp_a2a_unpack.argtypes = [vp, vp] + [i] * 6 + [vp]
     L.basp_attn_fwd.argtypes = [vp] * 5 + [i] * 6 + [f, vp]
@@ -117,8 +118,16 @@ def validate(b, S, H, H_kv, d, G, rank) -> int:
 
 
 # ------------------------------------------------------------ permutations
+def heads_per_member(n: int, G: int) -> int:
+    """Heads of an n-head tensor one member handles: n/G, or 1 for a head
+    shared by G/n members (n < G, G divisible by n); 0 if neither holds."""
+    if n % G == 0:
+        return n // G
+    return 1 if (n < G and G % n == 0) else 0
+
+
 def pack(shards, rank: int, out: torch.Tensor | None = None) -> torch.Tensor:
-    """G shards [b, S/G, n, d] -> the rank's head-sharded [b, S, n/G, d]."""
+    """G shards [b, S/G, n, d] -> the rank's head-sharded [b, S, nl, d]."""
     G = len(shards)
     b, Sg, n, d = shards[0].shape
     ptrs = (ctypes.c_void_p * G)(*[_dev(s, f"shards[{j}]", shards[0].dtype).value
@@ -127,7 +136,7 @@ def pack(shards, rank: int, out: torch.Tensor | None = None) -> torch.Tensor:
         if s.shape != shards[0].shape or s.device != shards[0].device:
             raise ValueError("shards differ in shape or device")
     if out is None:
-        out = torch.empty((b, Sg * G, max(n // G, 0), d), dtype=shards[0].dtype,
+        out = torch.empty((b, Sg * G, heads_per_member(n, G), d), dtype=shards[0].dtype,
                           device=shards[0].device)
     _check(lib().basp_pack(ptrs, _dev(out, "out", shards[0].dtype), b, Sg * G, n, d, G, rank,
                            _dtype_code(out), _stream(out)), "basp_pack")
@@ -145,39 +154,66 @@ def unpack(local: torch.Tensor, shards, rank: int):
     return shards
 
 
+def unpack_add(local: torch.Tensor, shards, rank: int):
+    """fp32: add local [b, S, nl, d] into the rank's head slice of every shard
+    (gradients of kv heads that several members share)."""
+    G = len(shards)
+    b, Sg, n, d = shards[0].shape
+    ptrs = (ctypes.c_void_p * G)(*[_dev(s, f"shards[{j}]", torch.float32).value
+                                   for j, s in enumerate(shards)])
+    _check(lib().basp_unpack_add(_dev(local, "local", torch.float32), ptrs, b, Sg * G, n, d, G,
+                                 rank, _stream(local)), "basp_unpack_add")
+    return shards
+
+
 def a2a_pack(own: torch.Tensor, G: int, out: torch.Tensor | None = None) -> torch.Tensor:
-    """Own shard [b, S/G, n, d] -> send buffer [G, b, S/G, n/G, d], one block per member."""
+    """Own shard [b, S/G, n, d] -> send buffer [G, b, S/G, nl, d], one block per member."""
     b, Sg, n, d = own.shape
     if out is None:
-        out = torch.empty((G, b, Sg, max(n // G, 0), d), dtype=own.dtype, device=own.device)
+        out = torch.empty((G, b, Sg, heads_per_member(n, G), d), dtype=own.dtype,
+                          device=own.device)
     _check(lib().basp_a2a_pack(_dev(own, "own"), _dev(out, "out", own.dtype), b, Sg * G, n, d,
                                G, _dtype_code(own), _stream(own)), "basp_a2a_pack")
     return out
 
 
-def a2a_unpack(recv: torch.Tensor, out: torch.Tensor | None = None) -> torch.Tensor:
-    """Received blocks [G, b, S/G, n/G, d] -> own shard [b, S/G, n, d]."""
+def a2a_unpack(recv: torch.Tensor, out: torch.Tensor | None = None,
+               n_heads: int | None = None) -> torch.Tensor:
+    """Received blocks [G, b, S/G, n/G, d] -> own shard [b, S/G, n, d].
+
+    ``n_heads`` < G: fp32 gradients of shared heads, blocks [G, b, S/G, 1, d]
+    summed per head in member order."""
     G, b, Sg, nl, d = recv.shape
+    n = G * nl if n_heads is None else n_heads
     if out is None:
-        out = torch.empty((b, Sg, G * nl, d), dtype=recv.dtype, device=recv.device)
+        out = torch.empty((b, Sg, n, d), dtype=recv.dtype, device=recv.device)
     _check(lib().basp_a2a_unpack(_dev(recv, "recv"), _dev(out, "out", recv.dtype), b, Sg * G,
-                                 G * nl, d, G, _dtype_code(recv), _stream(recv)),
+                                 n, d, G, _dtype_code(recv), _stream(recv)),
            "basp_a2a_unpack")
     return out
 
 
 # -------------------------------------------------------------- attention
-def _attn_dims(q, k, G):
+def _attn_dims(q, k, G, H_kv):
     b, S, Hl, d = q.shape
     Hkl = k.shape[2]
     if k.shape[:2] != (b, S) or k.shape[3] != d:
         raise ValueError("q and k/v disagree in shape")
-    return b, S, Hl * G, Hkl * G, d
+    if H_kv is None:
+        H_kv = Hkl * G
+    elif heads_per_member(H_kv, G) != Hkl:
+        raise ValueError(f"k/v hold {Hkl} heads; a member of {G} handles "
+                         f"{heads_per_member(H_kv, G)} of {H_kv}")
+    return b, S, Hl * G, H_kv, d
 
 
-def attn_fwd(q, k, v, G: int = 1, scale: float | None = None, out=None, lse=None):
-    """Causal GQA attention of the local heads: returns (o bf16, lse fp32 [b,Hl,S])."""
-    b, S, H, H_kv, d = _attn_dims(q, k, G)
+def attn_fwd(q, k, v, G: int = 1, scale: float | None = None, out=None, lse=None,
+             H_kv: int | None = None):
+    """Causal GQA attention of the local heads: returns (o bf16, lse fp32 [b,Hl,S]).
+
+    ``H_kv``: global kv heads (default: k's heads times G); give it when fewer
+    kv heads than members share one head per member."""
+    b, S, H, H_kv, d = _attn_dims(q, k, G, H_kv)
     scale = d ** -0.5 if scale is None else scale
     if v.shape != k.shape:
         raise ValueError("v must have k's shape")
@@ -197,9 +233,9 @@ def attn_bwd_workspace_bytes(b, S, H, H_kv, d, G) -> int:
 
 
 def attn_bwd(q, k, v, o, lse, do, G: int = 1, scale: float | None = None,
-             dq=None, dk=None, dv=None, workspace=None):
+             dq=None, dk=None, dv=None, workspace=None, H_kv: int | None = None):
     """Backward of attn_fwd: returns (dq, dk, dv) in fp32."""
-    b, S, H, H_kv, d = _attn_dims(q, k, G)
+    b, S, H, H_kv, d = _attn_dims(q, k, G, H_kv)
     scale = d ** -0.5 if scale is None else scale
     if dq is None:
         dq = torch.empty(q.shape, dtype=torch.float32, device=q.device)

@@ -16,13 +16,27 @@ namespace {
 
 bool aligned(const void *p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
 
+// Heads of an n-head tensor that one member handles: n/G when G divides n;
+// with fewer heads than members (G divisible by n) the single head
+// rank*n/G, which G/n members share.  0 when neither holds.
+int heads_per_member(int n, int G) {
+  if (n % G == 0) return n / G;
+  return (n < G && G % n == 0) ? 1 : 0;
+}
+
 // Shared shape rules of a rank's share: sizes, and the divisibility the
 // head-parallel exchange needs (every group member gets S/G tokens of each
-// sequence and H/G query heads, H_kv/G kv heads).
+// sequence and H/G query heads; H_kv/G kv heads, or one shared kv head when
+// H_kv < G).
 int check_share(int b, int S, int H, int H_kv, int d, int G) {
   if (b < 0 || S < 0 || H < 1 || H_kv < 1 || d < 1 || G < 1) return BASP_ERR_SHAPE;
-  if (S % G != 0 || H % G != 0 || H_kv % G != 0 || H % H_kv != 0) return BASP_ERR_SHAPE;
+  if (S % G != 0 || H % G != 0 || heads_per_member(H_kv, G) == 0 || H % H_kv != 0)
+    return BASP_ERR_SHAPE;
   return BASP_OK;
+}
+
+basp::AttnShape attn_shape(int b, int S, int H, int H_kv, int d, int G, float scale) {
+  return basp::AttnShape{b, S, H / G, heads_per_member(H_kv, G), d, scale};
 }
 
 int check_attn(int b, int S, int H, int H_kv, int d, int G, float scale) {
@@ -44,10 +58,11 @@ int hip_status(hipError_t e) { return e == hipSuccess ? BASP_OK : BASP_ERR_HIP; 
 // 2^31 including the loop stride, and put b*G blocks on one grid dimension.
 int check_perm_shape(int b, int S, int n, int d, int G, int dtype) {
   if (b < 0 || S < 0 || n < 1 || d < 1 || G < 1) return BASP_ERR_SHAPE;
-  if (S % G != 0 || n % G != 0) return BASP_ERR_SHAPE;
+  if (S % G != 0 || heads_per_member(n, G) == 0) return BASP_ERR_SHAPE;
   if (dtype != BASP_BF16 && dtype != BASP_F32) return BASP_ERR_UNSUPPORTED;
   if (G > BASP_MAX_GROUP) return BASP_ERR_UNSUPPORTED;
-  if ((uint64_t)(S / G) * (uint64_t)(n / G) * (uint64_t)d >= (1ull << 31)) return BASP_ERR_UNSUPPORTED;
+  if ((uint64_t)(S / G) * (uint64_t)heads_per_member(n, G) * (uint64_t)d >= (1ull << 31))
+    return BASP_ERR_UNSUPPORTED;
   if ((uint64_t)b * (uint64_t)G > 65535) return BASP_ERR_UNSUPPORTED;
   return BASP_OK;
 }
@@ -61,7 +76,7 @@ int finish_perm(const void *const *src_tab, void *const *dst_tab, uint64_t elem,
   for (int j = 0; j < s->G; ++j)
     if (!aligned(src_tab[j], elem) || !aligned(dst_tab[j], elem)) return BASP_ERR_ALIGN;
   const uint64_t q[] = {s->row_bytes, s->src_beta, s->src_j, s->src_row, s->src_off,
-                        s->dst_beta, s->dst_j, s->dst_row, s->dst_off};
+                        s->src_rep, s->dst_beta, s->dst_j, s->dst_row, s->dst_off};
   int vec = 16;
   while (vec > (int)elem) {
     bool ok = true;
@@ -75,7 +90,8 @@ int finish_perm(const void *const *src_tab, void *const *dst_tab, uint64_t elem,
 }
 
 // Sequence-shard side [b, S/G, n, d] at head offset `head0`, or head-sharded
-// side [b, S, n/G, d] with member j's tokens at rows j*S/G ..
+// side [b, S, nl, d] (nl = heads_per_member) with member j's tokens at rows
+// j*S/G ..
 void shard_side(int S, int n, int d, int G, uint64_t elem, uint64_t head0, uint64_t &beta,
                 uint64_t &j, uint64_t &row, uint64_t &off) {
   beta = (uint64_t)(S / G) * n * d * elem;
@@ -85,7 +101,7 @@ void shard_side(int S, int n, int d, int G, uint64_t elem, uint64_t head0, uint6
 }
 void local_side(int S, int n, int d, int G, uint64_t elem, uint64_t &beta, uint64_t &j,
                 uint64_t &row, uint64_t &off) {
-  const uint64_t nl = (uint64_t)(n / G);
+  const uint64_t nl = (uint64_t)heads_per_member(n, G);
   beta = (uint64_t)S * nl * d * elem;
   j = (uint64_t)(S / G) * nl * d * elem;
   row = nl * d * elem;
@@ -97,16 +113,21 @@ basp::PermShape perm_base(int b, int S, int n, int d, int G, uint64_t elem) {
   s.b = b;
   s.G = G;
   s.Sg = S / G;
-  s.row_bytes = (uint64_t)(n / G) * d * elem;
+  s.row_bytes = (uint64_t)heads_per_member(n, G) * d * elem;
+  s.mode = basp::PermMode::kCopy;
+  s.reps = 1;
   return s;
 }
 
-// Receive-side pack (to_local) or send-side unpack of the rank's head slice.
-int run_pack(bool to_local, const void *const *shards, const void *local, int b, int S, int n,
-             int d, int G, int rank, int dtype, void *stream) {
+// Receive-side pack (to_local) or send-side unpack of the rank's head slice;
+// `add` (fp32 only) adds the local rows into the shards instead.
+int run_pack(bool to_local, bool add, const void *const *shards, const void *local, int b, int S,
+             int n, int d, int G, int rank, int dtype, void *stream) {
   int rc = check_perm_shape(b, S, n, d, G, dtype);
   if (rc) return rc;
   if (rank < 0 || rank >= G) return BASP_ERR_RANK;
+  // A head shared by several members cannot take one member's rows alone.
+  if (!to_local && !add && n < G) return BASP_ERR_SHAPE;
   // An empty problem touches no memory: its pointers are not inspected.
   if ((long long)b * S == 0) return BASP_OK;
   if (!shards || !local) return BASP_ERR_NULL;
@@ -114,7 +135,7 @@ int run_pack(bool to_local, const void *const *shards, const void *local, int b,
   basp::PermShape s = perm_base(b, S, n, d, G, elem);
   const void *one[BASP_MAX_GROUP];
   for (int j = 0; j < G; ++j) one[j] = local;
-  const uint64_t head0 = (uint64_t)rank * (n / G);
+  const uint64_t head0 = (uint64_t)rank * n / G;
   if (to_local) {
     shard_side(S, n, d, G, elem, head0, s.src_beta, s.src_j, s.src_row, s.src_off);
     local_side(S, n, d, G, elem, s.dst_beta, s.dst_j, s.dst_row, s.dst_off);
@@ -126,6 +147,7 @@ int run_pack(bool to_local, const void *const *shards, const void *local, int b,
   }
   local_side(S, n, d, G, elem, s.src_beta, s.src_j, s.src_row, s.src_off);
   shard_side(S, n, d, G, elem, head0, s.dst_beta, s.dst_j, s.dst_row, s.dst_off);
+  if (add) s.mode = basp::PermMode::kAddDst;
   rc = finish_perm(one, const_cast<void *const *>(shards), elem, &s);
   if (rc) return rc;
   (void)hipGetLastError();
@@ -138,35 +160,56 @@ int run_a2a(bool to_send, const void *src, void *dst, int b, int S, int n, int d
             int dtype, void *stream) {
   int rc = check_perm_shape(b, S, n, d, G, dtype);
   if (rc) return rc;
+  const bool shared = n < G;  // one head per member, G/n members per head
+  if (shared && !to_send && dtype != BASP_F32) return BASP_ERR_UNSUPPORTED;
   if ((long long)b * S == 0) return BASP_OK;
   if (!src || !dst) return BASP_ERR_NULL;
   const uint64_t elem = dtype == BASP_BF16 ? 2 : 4;
   basp::PermShape s = perm_base(b, S, n, d, G, elem);
-  const uint64_t nl = (uint64_t)(n / G), Sg = (uint64_t)(S / G);
-  // own [b, S/G, n, d]: member j's heads at j*n/G
-  const uint64_t own_beta = Sg * n * d * elem, own_j = nl * d * elem, own_row = (uint64_t)n * d * elem;
-  // send/recv [G, b, S/G, n/G, d]
-  const uint64_t a2a_beta = Sg * nl * d * elem, a2a_j = (uint64_t)b * a2a_beta,
-                 a2a_row = nl * d * elem;
-  if (to_send) {
-    s.src_beta = own_beta, s.src_j = own_j, s.src_row = own_row;
-    s.dst_beta = a2a_beta, s.dst_j = a2a_j, s.dst_row = a2a_row;
-  } else {
-    s.src_beta = a2a_beta, s.src_j = a2a_j, s.src_row = a2a_row;
-    s.dst_beta = own_beta, s.dst_j = own_j, s.dst_row = own_row;
-  }
+  const uint64_t nl = (uint64_t)heads_per_member(n, G), Sg = (uint64_t)(S / G);
+  const uint64_t hd = (uint64_t)d * elem;
+  // own [b, S/G, n, d]
+  const uint64_t own_beta = Sg * n * hd, own_row = (uint64_t)n * hd;
+  // send/recv [G, b, S/G, nl, d]
+  const uint64_t a2a_beta = Sg * nl * hd, a2a_j = (uint64_t)b * a2a_beta, a2a_row = nl * hd;
+  const char *sp = static_cast<const char *>(src);
+  char *dp = static_cast<char *>(dst);
   const void *st[BASP_MAX_GROUP];
   void *dt[BASP_MAX_GROUP];
-  for (int j = 0; j < G; ++j) {
-    st[j] = src;
-    dt[j] = dst;
+  if (to_send) {
+    // block j holds member j's heads: [j*n/G, +nl) of every own row
+    s.src_beta = own_beta, s.src_j = 0, s.src_row = own_row;
+    s.dst_beta = a2a_beta, s.dst_j = a2a_j, s.dst_row = a2a_row;
+    for (int j = 0; j < G; ++j) {
+      st[j] = sp + (uint64_t)j * n / G * hd;
+      dt[j] = dp;
+    }
+  } else if (!shared) {
+    s.src_beta = a2a_beta, s.src_j = a2a_j, s.src_row = a2a_row;
+    s.dst_beta = own_beta, s.dst_j = nl * hd, s.dst_row = own_row;
+    for (int j = 0; j < G; ++j) {
+      st[j] = src;
+      dt[j] = dst;
+    }
+  } else {
+    // One launch block per head h: the sum of blocks h*R .. h*R+R-1.
+    const int R = G / n;
+    s.G = n;
+    s.mode = basp::PermMode::kSumSrc;
+    s.reps = R;
+    s.src_rep = a2a_j;
+    s.src_beta = a2a_beta, s.src_j = 0, s.src_row = a2a_row;
+    s.dst_beta = own_beta, s.dst_j = 0, s.dst_row = own_row;
+    for (int h = 0; h < n; ++h) {
+      st[h] = sp + (uint64_t)h * R * a2a_j;
+      dt[h] = dp + (uint64_t)h * hd;
+    }
   }
   rc = finish_perm(st, dt, elem, &s);
   if (rc) return rc;
   (void)hipGetLastError();
   return hip_status(basp::launch_permute(st, dt, s, (hipStream_t)stream));
 }
-
 
 }  // namespace
 
@@ -177,7 +220,7 @@ const char *basp_status_str(int status) {
     case BASP_OK: return "BASP_OK";
     case BASP_ERR_NULL: return "BASP_ERR_NULL: a required pointer is NULL";
     case BASP_ERR_SHAPE:
-      return "BASP_ERR_SHAPE: negative size or S, H, H_kv not divisible by G, or H by H_kv";
+      return "BASP_ERR_SHAPE: negative size, S or H not divisible by G, H_kv neither a multiple nor a divisor of G, or H not divisible by H_kv";
     case BASP_ERR_RANK: return "BASP_ERR_RANK: rank outside [0, G)";
     case BASP_ERR_UNSUPPORTED:
       return "BASP_ERR_UNSUPPORTED: head dim, dtype, group size or scale outside what the "
@@ -216,13 +259,19 @@ int basp_validate(int b, int S, int H, int H_kv, int d, int G, int rank) {
 
 int basp_pack(const void *const *src_shards, void *dst, int b, int S, int n_heads, int d,
               int G, int rank, int dtype, void *stream) {
-  return run_pack(true, src_shards, dst, b, S, n_heads, d, G, rank, dtype, stream);
+  return run_pack(true, false, src_shards, dst, b, S, n_heads, d, G, rank, dtype, stream);
 }
 
 int basp_unpack(const void *src, void *const *dst_shards, int b, int S, int n_heads, int d,
                 int G, int rank, int dtype, void *stream) {
-  return run_pack(false, const_cast<const void *const *>(dst_shards), src, b, S, n_heads, d, G,
+  return run_pack(false, false, const_cast<const void *const *>(dst_shards), src, b, S, n_heads, d, G,
                   rank, dtype, stream);
+}
+
+int basp_unpack_add(const float *src, float *const *dst_shards, int b, int S, int n_heads, int d,
+                    int G, int rank, void *stream) {
+  return run_pack(false, true, reinterpret_cast<const void *const *>(dst_shards), src, b, S,
+                  n_heads, d, G, rank, BASP_F32, stream);
 }
 
 int basp_a2a_pack(const void *own, void *send, int b, int S, int n_heads, int d, int G,
@@ -244,14 +293,14 @@ int basp_attn_fwd(const void *q, const void *k, const void *v, void *o, float *l
   if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(o, 16) ||
       !aligned(lse, 4))
     return BASP_ERR_ALIGN;
-  basp::AttnShape s{b, S, H / G, H_kv / G, d, scale};
+  basp::AttnShape s = attn_shape(b, S, H, H_kv, d, G, scale);
   (void)hipGetLastError();
   return hip_status(basp::launch_attn_fwd(q, k, v, o, lse, s, (hipStream_t)stream));
 }
 
 size_t basp_attn_bwd_workspace_bytes(int b, int S, int H, int H_kv, int d, int G) {
   if (check_share(b, S, H, H_kv, d, G) != BASP_OK) return 0;
-  basp::AttnShape s{b, S, H / G, H_kv / G, d, 1.f};
+  basp::AttnShape s = attn_shape(b, S, H, H_kv, d, G, 1.f);
   return basp::attn_bwd_workspace_bytes(s);
 }
 
@@ -267,7 +316,7 @@ int basp_attn_bwd(const void *q, const void *k, const void *v, const void *o, co
       !aligned(d_o, 16) || !aligned(dq, 16) || !aligned(dk, 16) || !aligned(dv, 16) ||
       !aligned(lse, 4))
     return BASP_ERR_ALIGN;
-  basp::AttnShape s{b, S, H / G, H_kv / G, d, scale};
+  basp::AttnShape s = attn_shape(b, S, H, H_kv, d, G, scale);
   const size_t need = basp::attn_bwd_workspace_bytes(s);
   if (workspace_bytes < need) return BASP_ERR_WORKSPACE;
   if (!workspace) return BASP_ERR_NULL;

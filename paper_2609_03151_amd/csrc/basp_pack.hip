@@ -8,6 +8,13 @@
 //         send[j][beta][t][h][e] = own[beta][t][j*n/G + h][e]
 // receive side, a2a_unpack: the inverse, every member's block into the own shard
 //
+// With fewer heads than members (n < G, G divisible by n) member r handles the
+// single head r*n/G, shared by G/n members; gradients of such a head are
+// reduced in fp32 instead of copied:
+// send side, unpack_add:    dst[beta][t][h0][e] += local[beta][j*S/G + t][0][e]
+// receive side, a2a_unpack: own[beta][t][h][e] = sum over the members j that
+//                           share head h, in member order, of recv[j][beta][t][0][e]
+//
 // For one token the heads moved are a contiguous run of (n/G)*d elements on
 // both sides, so each of these is, per (member j, sequence beta), a 2-D copy
 // of S/G rows with a row stride on each side (PermShape).  Workgroup L works
@@ -60,11 +67,24 @@ struct CopyGeom {
   FastDiv by_row;                  // division by row_vecs
   uint32_t block_vecs;             // Sg * row_vecs (< 2^32, checked on the host)
   uint32_t G, jb_count, bx_count;  // members, (j, beta) blocks, workgroups per block
-  uint64_t src_beta, src_j, src_row, src_off;
+  uint32_t reps;                   // kSumSrc: source rows summed per destination row
+  uint64_t src_beta, src_j, src_row, src_off, src_rep;
   uint64_t dst_beta, dst_j, dst_row, dst_off;
 };
 
-template <typename V, int U>
+// Element-wise fp32 sum of two vectors that carry fp32 bit patterns.
+__device__ __forceinline__ uint32_t fadd_bits(uint32_t a, uint32_t b) {
+  return __float_as_uint(__uint_as_float(a) + __uint_as_float(b));
+}
+__device__ __forceinline__ uint32_t vadd(uint32_t a, uint32_t b) { return fadd_bits(a, b); }
+__device__ __forceinline__ u32x2 vadd(u32x2 a, u32x2 b) {
+  return u32x2{fadd_bits(a.x, b.x), fadd_bits(a.y, b.y)};
+}
+__device__ __forceinline__ u32x4 vadd(u32x4 a, u32x4 b) {
+  return u32x4{fadd_bits(a.x, b.x), fadd_bits(a.y, b.y), fadd_bits(a.z, b.z), fadd_bits(a.w, b.w)};
+}
+
+template <typename V, int U, PermMode M>
 __global__ __launch_bounds__(256) void permute_kernel(ShardTable src, ShardTable dst, CopyGeom g) {
   const uint32_t jb = blockIdx.x % g.jb_count, bx = blockIdx.x / g.jb_count;
   const uint32_t j = jb % g.G, beta = jb / g.G;
@@ -82,6 +102,27 @@ __global__ __launch_bounds__(256) void permute_kernel(ShardTable src, ShardTable
       c[u] = i - rt[u] * g.row_vecs;
       if (i < g.block_vecs) v[u] = nt_load(s + (uint64_t)rt[u] * g.src_row + c[u]);
     }
+    if constexpr (M == PermMode::kSumSrc) {
+      for (uint32_t r = 1; r < g.reps; ++r) {
+        V w[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+          if (base + u * 256u < g.block_vecs)
+            w[u] = nt_load(s + r * g.src_rep + (uint64_t)rt[u] * g.src_row + c[u]);
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+          if (base + u * 256u < g.block_vecs) v[u] = vadd(v[u], w[u]);
+      }
+    }
+    if constexpr (M == PermMode::kAddDst) {
+      V w[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+        if (base + u * 256u < g.block_vecs) w[u] = nt_load(d + (uint64_t)rt[u] * g.dst_row + c[u]);
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+        if (base + u * 256u < g.block_vecs) v[u] = vadd(w[u], v[u]);
+    }
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const uint32_t i = base + u * 256u;
@@ -92,7 +133,7 @@ __global__ __launch_bounds__(256) void permute_kernel(ShardTable src, ShardTable
 
 namespace {
 
-template <typename V>
+template <typename V, PermMode M>
 hipError_t launch_typed(const void *const *src_tab, void *const *dst_tab, const PermShape &s,
                         hipStream_t stream) {
   constexpr int U = 8;
@@ -106,6 +147,8 @@ hipError_t launch_typed(const void *const *src_tab, void *const *dst_tab, const 
   g.src_j = s.src_j / vsz;
   g.src_row = s.src_row / vsz;
   g.src_off = s.src_off / vsz;
+  g.src_rep = s.src_rep / vsz;
+  g.reps = (uint32_t)(s.reps > 1 ? s.reps : 1);
   g.dst_beta = s.dst_beta / vsz;
   g.dst_j = s.dst_j / vsz;
   g.dst_row = s.dst_row / vsz;
@@ -124,20 +167,32 @@ hipError_t launch_typed(const void *const *src_tab, void *const *dst_tab, const 
   if (bx > want) bx = want;
   g.jb_count = (uint32_t)blocks;
   g.bx_count = (uint32_t)bx;
-  hipLaunchKernelGGL((permute_kernel<V, U>), dim3((unsigned)(bx * blocks)), dim3(256), 0, stream,
-                     ts, td, g);
+  hipLaunchKernelGGL((permute_kernel<V, U, M>), dim3((unsigned)(bx * blocks)), dim3(256), 0,
+                     stream, ts, td, g);
   return hipGetLastError();
+}
+
+template <PermMode M>
+hipError_t launch_reduce(const void *const *src_tab, void *const *dst_tab, const PermShape &s,
+                         hipStream_t stream) {
+  switch (s.vec_bytes) {
+    case 16: return launch_typed<u32x4, M>(src_tab, dst_tab, s, stream);
+    case 8: return launch_typed<u32x2, M>(src_tab, dst_tab, s, stream);
+    default: return launch_typed<uint32_t, M>(src_tab, dst_tab, s, stream);
+  }
 }
 
 }  // namespace
 
 hipError_t launch_permute(const void *const *src_tab, void *const *dst_tab, const PermShape &s,
                           hipStream_t stream) {
+  if (s.mode == PermMode::kAddDst) return launch_reduce<PermMode::kAddDst>(src_tab, dst_tab, s, stream);
+  if (s.mode == PermMode::kSumSrc) return launch_reduce<PermMode::kSumSrc>(src_tab, dst_tab, s, stream);
   switch (s.vec_bytes) {
-    case 16: return launch_typed<u32x4>(src_tab, dst_tab, s, stream);
-    case 8: return launch_typed<u32x2>(src_tab, dst_tab, s, stream);
-    case 4: return launch_typed<uint32_t>(src_tab, dst_tab, s, stream);
-    default: return launch_typed<uint16_t>(src_tab, dst_tab, s, stream);
+    case 16: return launch_typed<u32x4, PermMode::kCopy>(src_tab, dst_tab, s, stream);
+    case 8: return launch_typed<u32x2, PermMode::kCopy>(src_tab, dst_tab, s, stream);
+    case 4: return launch_typed<uint32_t, PermMode::kCopy>(src_tab, dst_tab, s, stream);
+    default: return launch_typed<uint16_t, PermMode::kCopy>(src_tab, dst_tab, s, stream);
   }
 }
 

@@ -10,6 +10,11 @@ once, and chains the library calls:
   forward:  pack(Q), pack(K), pack(V) -> attn_fwd -> unpack(O)
   backward: pack(dO) -> attn_bwd -> unpack(dQ), unpack(dK), unpack(dV)
 
+With fewer kv heads than members (H_kv < G, G divisible by H_kv) the rank
+holds one kv head shared by G/H_kv members, and its dK, dV are that head's
+partial gradients: they are added into the shards (unpack_add), so the dK/dV
+shard buffers accumulate over repeated backward calls.
+
 The exchange itself (RCCL all-to-all) is outside this share: the shard
 buffers stand for the receive and send buffers of that exchange.
 """
@@ -17,7 +22,8 @@ from __future__ import annotations
 
 import torch
 
-from . import attn_bwd, attn_bwd_workspace_bytes, attn_fwd, pack, unpack
+from . import (attn_bwd, attn_bwd_workspace_bytes, attn_fwd, heads_per_member, pack, unpack,
+               unpack_add)
 
 
 class RankShare:
@@ -29,7 +35,8 @@ class RankShare:
         b, Sg, H, d = q_shards[0].shape
         H_kv = k_shards[0].shape[2]
         self.b, self.S, self.H, self.H_kv, self.d = b, Sg * G, H, H_kv, d
-        self.Hl, self.Hkl = H // G, H_kv // G
+        self.Hl, self.Hkl = H // G, heads_per_member(H_kv, G)
+        self.shared_kv = H_kv < G
         self.scale = d ** -0.5 if scale is None else scale
         dev = q_shards[0].device
         bf, f32 = torch.bfloat16, torch.float32
@@ -59,7 +66,8 @@ class RankShare:
         pack(self.v_shards, self.rank, out=self.v)
 
     def attn_fwd(self):
-        attn_fwd(self.q, self.k, self.v, G=self.G, scale=self.scale, out=self.o, lse=self.lse)
+        attn_fwd(self.q, self.k, self.v, G=self.G, scale=self.scale, out=self.o, lse=self.lse,
+                 H_kv=self.H_kv)
 
     def unpack_o(self):
         unpack(self.o, self.o_shards, self.rank)
@@ -69,12 +77,15 @@ class RankShare:
 
     def attn_bwd(self):
         attn_bwd(self.q, self.k, self.v, self.o, self.lse, self.do, G=self.G, scale=self.scale,
-                 dq=self.dq, dk=self.dk, dv=self.dv, workspace=self.workspace)
+                 dq=self.dq, dk=self.dk, dv=self.dv, workspace=self.workspace, H_kv=self.H_kv)
+
+    def _unpack_kv_grad(self, local, shards):
+        (unpack_add if self.shared_kv else unpack)(local, shards, self.rank)
 
     def unpack_grads(self):
         unpack(self.dq, self.dq_shards, self.rank)
-        unpack(self.dk, self.dk_shards, self.rank)
-        unpack(self.dv, self.dv_shards, self.rank)
+        self._unpack_kv_grad(self.dk, self.dk_shards)
+        self._unpack_kv_grad(self.dv, self.dv_shards)
 
     def forward(self):
         self.pack_qkv()
@@ -100,6 +111,8 @@ class RankShare:
     def permutation_calls(self) -> list:
         """(name, call, bytes read + written) of each of the eight pack/unpack calls of a step."""
         two = lambda t: 2 * t.numel() * t.element_size()
+        # an added gradient is read on both sides and written once
+        kv_grad = (lambda t: 3 * t.numel() * t.element_size()) if self.shared_kv else two
         return [
             ("pack_q", lambda: pack(self.q_shards, self.rank, out=self.q), two(self.q)),
             ("pack_k", lambda: pack(self.k_shards, self.rank, out=self.k), two(self.k)),
@@ -107,8 +120,8 @@ class RankShare:
             ("unpack_o", lambda: unpack(self.o, self.o_shards, self.rank), two(self.o)),
             ("pack_do", lambda: pack(self.do_shards, self.rank, out=self.do), two(self.do)),
             ("unpack_dq", lambda: unpack(self.dq, self.dq_shards, self.rank), two(self.dq)),
-            ("unpack_dk", lambda: unpack(self.dk, self.dk_shards, self.rank), two(self.dk)),
-            ("unpack_dv", lambda: unpack(self.dv, self.dv_shards, self.rank), two(self.dv)),
+            ("unpack_dk", lambda: self._unpack_kv_grad(self.dk, self.dk_shards), kv_grad(self.dk)),
+            ("unpack_dv", lambda: self._unpack_kv_grad(self.dv, self.dv_shards), kv_grad(self.dv)),
         ]
 
     def pack_unpack_bytes(self) -> dict:
@@ -119,5 +132,5 @@ class RankShare:
             "pack_qkv": 2 * (bq + 2 * bkv),
             "unpack_o": 2 * bq,
             "pack_do": 2 * bq,
-            "unpack_grads": 2 * (self.dq.numel() + 2 * self.dk.numel()) * 4,
+            "unpack_grads": (2 * self.dq.numel() + (3 if self.shared_kv else 2) * 2 * self.dk.numel()) * 4,
         }

@@ -45,7 +45,12 @@ class Workload:
 
     @property
     def Hkl(self) -> int:
-        return self.H_kv // self.G
+        """Local kv heads: H_kv/G, or one head shared by G/H_kv members."""
+        return self.H_kv // self.G if self.H_kv >= self.G else 1
+
+    def first_head(self, n: int) -> int:
+        """First head of an n-head tensor that this rank handles."""
+        return self.rank * n // self.G
 
     @property
     def n_rep(self) -> int:
@@ -92,6 +97,10 @@ WORKLOADS = {
                                 G=4, rank=1, seed=6),
     "qwen25_3b_s16k": Workload("qwen25_3b_s16k", b=1, S=16384, H=32, H_kv=8, d=80,
                                G=4, rank=2, seed=7),
+    # Fewer kv heads than group members: Llama-3-8B under one group of 16
+    # (two 8-GPU nodes, micro-batch 1); each kv head is shared by 2 members.
+    "llama3_8b_g16_s64k": Workload("llama3_8b_g16_s64k", b=1, S=65536, H=32, H_kv=8,
+                                   d=128, G=16, rank=5, seed=8),
 }
 
 

@@ -43,8 +43,9 @@ def workload_inputs(name: str):
 
 def local_heads(x: torch.Tensor, w, n: int):
     """The rank's head-sharded tensor, cut from the global batch on the CPU."""
-    nl = n // w.G
-    return x[w.seq_offset:w.seq_offset + w.b, :, w.rank * nl:(w.rank + 1) * nl, :]
+    nl = n // w.G if n >= w.G else 1
+    h0 = w.first_head(n)
+    return x[w.seq_offset:w.seq_offset + w.b, :, h0:h0 + nl, :]
 
 
 def device_shards(x: torch.Tensor, w, dev="cuda"):

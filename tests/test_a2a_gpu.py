@@ -112,7 +112,7 @@ def test_group_exchange_consistent_with_pack_unpack(b, S, n, d, G):
     torch.cuda.synchronize()
 
 
-FULL = ["llama3_8b_s32k", "ulysses_g8_b2_s64k", "llama3_70b_s128k"]
+FULL = ["llama3_8b_s32k", "ulysses_g8_b2_s64k", "llama3_70b_s128k", "llama3_8b_g16_s64k"]
 
 
 @pytest.mark.parametrize("name", FULL)
@@ -122,15 +122,23 @@ def test_a2a_full_size(name):
     w = WORKLOADS[name]
     log(f"[a2a full] {name}")
     q, k, _, _ = workload_inputs(name)
-    for x in (q, k):
+    for x, n in ((q, w.H), (k, w.H_kv)):
         own = device_shards(x, w)[w.rank]
         send = basp.a2a_pack(own, w.G)
         torch.cuda.synchronize()
         own_h = own.cpu()
         ref = oracle.a2a_pack(own_h, w.G)
         assert np.array_equal(_bits(send), ref)
-        back = basp.a2a_unpack(send)
-        torch.cuda.synchronize()
-        assert torch.equal(back.view(torch.int16), own.view(torch.int16))
+        if n >= w.G:
+            back = basp.a2a_unpack(send)
+            torch.cuda.synchronize()
+            assert torch.equal(back.view(torch.int16), own.view(torch.int16))
+        else:
+            # shared heads: the fp32 sum over a head's G/n copies is (G/n) x own
+            own32 = own.float()
+            back = basp.a2a_unpack(basp.a2a_pack(own32, w.G), n_heads=n)
+            torch.cuda.synchronize()
+            assert torch.equal(back, (w.G // n) * own32)
+            del own32
         del own, send, back
     torch.cuda.empty_cache()

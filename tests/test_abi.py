@@ -58,7 +58,10 @@ def test_group_of_matches_paper_example_and_errors():
     ((-1, 512, 8, 8, 64, 2, 0), SHAPE),
     ((1, 510, 8, 8, 64, 4, 0), SHAPE),       # S % G
     ((1, 512, 6, 2, 64, 4, 0), SHAPE),       # H % G
-    ((1, 512, 8, 2, 64, 4, 0), SHAPE),       # H_kv % G
+    ((1, 512, 12, 3, 64, 4, 0), SHAPE),      # H_kv neither a multiple nor a divisor of G
+    ((1, 512, 8, 2, 64, 4, 0), OK),          # 2 kv heads shared by 4 members
+    ((1, 16384, 32, 8, 128, 16, 15), OK),    # 8 kv heads, G = 16
+    ((1, 512, 8, 1, 64, 8, 7), OK),          # MQA
     ((1, 512, 12, 8, 64, 4, 0), SHAPE),      # H % H_kv
     ((1, 512, 8, 8, 64, 2, 2), RANK),
     ((1, 512, 8, 8, 64, 2, -1), RANK),
@@ -137,6 +140,29 @@ def test_a2a_rejects_before_any_hip_call():
         assert fn(_fake(0x1001), c, 1, 64, 8, 64, 2, 0, None) == ALIGN
         assert fn(a, _fake(0x2002), 1, 64, 8, 64, 2, 1, None) == ALIGN
         assert fn(None, None, 0, 64, 8, 64, 2, 0, None) == OK    # empty: nothing enqueued
+
+
+def test_shared_head_calls_reject_before_any_hip_call():
+    """n < G: unpack refuses (a shared head must be added), unpack_add and the
+    replica-summing a2a_unpack are fp32 only; n neither a multiple nor a
+    divisor of G is a shape error everywhere."""
+    L = basp.lib()
+    vp = ctypes.c_void_p
+    good = (vp * 4)(0x1000, 0x2000, 0x3000, 0x4000)
+    a, c = _fake(0x10000), _fake(0x20000)
+    assert L.basp_unpack(a, good, 1, 64, 2, 64, 4, 0, 1, None) == SHAPE
+    assert L.basp_unpack(a, good, 1, 64, 3, 64, 4, 0, 1, None) == SHAPE
+    assert L.basp_pack(good, a, 1, 64, 3, 64, 4, 0, 1, None) == SHAPE
+    assert L.basp_a2a_unpack(a, c, 1, 64, 2, 64, 4, 0, None) == UNSUP   # bf16 sum
+    assert L.basp_a2a_pack(a, c, 1, 64, 3, 64, 4, 0, None) == SHAPE
+    assert L.basp_unpack_add(a, good, 1, 64, 3, 64, 4, 0, None) == SHAPE
+    assert L.basp_unpack_add(a, good, 1, 64, 2, 64, 4, 4, None) == RANK
+    assert L.basp_unpack_add(None, good, 1, 64, 2, 64, 4, 0, None) == NULL
+    assert L.basp_unpack_add(_fake(0x10002), good, 1, 64, 2, 64, 4, 0, None) == ALIGN
+    assert L.basp_unpack_add(None, None, 0, 64, 2, 64, 4, 0, None) == OK   # empty
+    p = [_fake(0x10000 * (i + 1)) for i in range(5)]
+    assert L.basp_attn_fwd(*p, 1, 128, 12, 3, 128, 4, ctypes.c_float(0.1), None) == SHAPE
+    assert L.basp_attn_bwd_workspace_bytes(1, 128, 8, 2, 128, 4) > 0
 
 
 def test_attn_rejects_before_any_hip_call():

@@ -139,7 +139,7 @@ def test_bitwise_deterministic():
 
 
 FULL = ["llama3_8b_s32k", "qwen25_7b_s64k", "ulysses_g8_b2_s64k", "basp_g4_b1_s64k",
-        "llama3_70b_s128k", "llama32_3b_s16k", "qwen25_3b_s16k"]
+        "llama3_70b_s128k", "llama32_3b_s16k", "qwen25_3b_s16k", "llama3_8b_g16_s64k"]
 
 
 def _sample_rows(S, rng, n=40):
@@ -192,7 +192,7 @@ def test_attention_full_size_sampled(name):
     scale_k = sh.dk.double().abs().sum(dim=1)
     assert float((dk_sum.abs() / scale_k.clamp_min(1e-30)).max()) < 1e-3
     dv_sum = sh.dv.double().sum(dim=1)
-    do_sum = dl.double().reshape(w.b, w.S, w.Hkl, w.n_rep, w.d).sum(dim=(1, 3)).cuda()
+    do_sum = dl.double().reshape(w.b, w.S, w.Hkl, w.Hl // w.Hkl, w.d).sum(dim=(1, 3)).cuda()
     rel = ((dv_sum - do_sum).abs().max() / do_sum.abs().max()).item()
     log(f"  sum dV vs sum dO: rel {rel:.2e}")
     assert rel < 1e-3

@@ -102,27 +102,30 @@ def test_empty_is_a_noop():
 
 
 FULL = ["llama3_8b_s32k", "qwen25_7b_s64k", "ulysses_g8_b2_s64k", "basp_g4_b1_s64k",
-        "llama3_70b_s128k", "llama32_3b_s16k", "qwen25_3b_s16k"]
+        "llama3_70b_s128k", "llama32_3b_s16k", "qwen25_3b_s16k", "llama3_8b_g16_s64k"]
 
 
 @pytest.mark.parametrize("name", FULL)
 def test_pack_unpack_full_size(name):
     """Full-size shards: every rank's pack equals the head slice of the
     concatenated shards (bit for bit, compared on the GPU); sampled token
-    windows equal the oracle; unpack of the packed result restores the shards."""
+    windows equal the oracle; unpack of the packed result restores the shards.
+    A head shared by several members (n < G) is checked through unpack_add:
+    every member adding its packed copy back gives (G/n) times the shards."""
     w = WORKLOADS[name]
     log(f"[pack full] {name}")
     q, k, v, _ = workload_inputs(name)
     for x, n in ((q, w.H), (k, w.H_kv)):
         shards = device_shards(x, w)
         glob = torch.cat(shards, dim=1)
-        nl = n // w.G
+        nl = basp.heads_per_member(n, w.G)
         ranks = sorted({0, w.rank, w.G - 1})
         for r in ranks:
             out = basp.pack(shards, r)
             torch.cuda.synchronize()
+            h0 = r * n // w.G
             assert torch.equal(out.view(torch.int16),
-                               glob[:, :, r * nl:(r + 1) * nl].contiguous().view(torch.int16)), r
+                               glob[:, :, h0:h0 + nl].contiguous().view(torch.int16)), r
         # sampled token windows of every shard against the oracle
         r = w.rank
         out = basp.pack(shards, r).cpu()
@@ -132,11 +135,20 @@ def test_pack_unpack_full_size(name):
             ref = oracle.pack(win, r)               # [b, 16*G, nl, d]
             got = torch.cat([out[:, j * Sg + t0:j * Sg + t0 + 16] for j in range(w.G)], dim=1)
             assert np.array_equal(_bits(got), ref)
-        # unpack restores the shards exactly (its slice rewritten, rest untouched)
-        before = [s.clone() for s in shards]
-        basp.unpack(basp.pack(shards, r), shards, r)
-        torch.cuda.synchronize()
-        assert all(torch.equal(a.view(torch.int16), b_.view(torch.int16))
-                   for a, b_ in zip(shards, before))
+        if n >= w.G:
+            # unpack restores the shards exactly (its slice rewritten, rest untouched)
+            before = [s.clone() for s in shards]
+            basp.unpack(basp.pack(shards, r), shards, r)
+            torch.cuda.synchronize()
+            assert all(torch.equal(a.view(torch.int16), b_.view(torch.int16))
+                       for a, b_ in zip(shards, before))
+        else:
+            f32 = [s.float() for s in shards]
+            acc = [torch.zeros_like(s) for s in f32]
+            for r in range(w.G):
+                basp.unpack_add(basp.pack(f32, r), acc, r)
+            torch.cuda.synchronize()
+            assert all(torch.equal(a, (w.G // n) * s) for a, s in zip(acc, f32))
+            del f32, acc
         del shards, glob, out
     torch.cuda.empty_cache()

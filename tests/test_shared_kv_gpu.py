@@ -1,0 +1,179 @@
+"""GPU parity when a group has more members than the model has kv heads
+(n < G, G divisible by n): member r handles the single head r*n/G, and the
+gradients of a shared head are summed over its members.
+
+* basp_pack, basp_unpack_add, basp_a2a_pack and the summing basp_a2a_unpack:
+  bit-exact against the oracle at small sizes, with sentinel guard bands;
+  unpack_add also with G dividing n (disjoint slices);
+* the whole group simulated on one GPU -- every member packs Q/K/V/dO, runs
+  attention forward and backward on its one kv head, unpacks O and dQ and
+  adds dK, dV -- against the oracle's attention of the global tensors
+  (within the attention bar);
+* the same gradients returned through the owner-side exchange (each
+  member's part of its kv head cut into per-owner blocks, a2a_unpack summing
+  each head's blocks) equal the unpack_add route bit for bit."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2609_03151_amd as basp
+from parity import LSE_MAX_ABS, check_close, log
+from synth_inputs import random_shards
+
+pytestmark = pytest.mark.gpu
+
+
+def _bits(t: torch.Tensor) -> np.ndarray:
+    t = t.detach().cpu().contiguous()
+    if t.dtype == torch.bfloat16:
+        return t.view(torch.int16).numpy()
+    return t.view(torch.int32).numpy()
+
+
+def _guarded(shape, dtype, pad=64):
+    n = int(np.prod(shape))
+    itype = torch.int16 if dtype == torch.bfloat16 else torch.int32
+    sent = 0x7F7B if dtype == torch.bfloat16 else 0x7FBADBAD
+    buf = torch.full((pad + n + pad,), sent, dtype=itype, device="cuda")
+    return buf[pad:pad + n].view(dtype).view(shape), buf, sent
+
+
+def _intact(buf, sent):
+    whole = buf.cpu().numpy()
+    s = np.array(sent).astype(whole.dtype)
+    return np.all(whole[:64] == s) and np.all(whole[-64:] == s)
+
+
+SHARED = [  # b, S, n, d, G
+    (1, 256, 2, 128, 4),
+    (2, 96, 1, 64, 8),      # MQA: one kv head for all members
+    (1, 120, 4, 128, 8),
+    (3, 40, 2, 5, 4),       # odd head dim: narrow accesses
+    (1, 1008, 8, 96, 16),   # 8 kv heads over 16 members, 63 tokens per shard
+]
+
+
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
+@pytest.mark.parametrize("b,S,n,d,G", SHARED)
+def test_pack_shared_head_bitexact(b, S, n, d, G, dtype):
+    shards_h = random_shards(b, S, n, d, G, seed=S + n + d + G, dtype=dtype)
+    shards = [s.cuda() for s in shards_h]
+    for r in sorted({0, 1, G // 2, G - 1}):
+        out, buf, sent = _guarded((b, S, 1, d), dtype)
+        basp.pack(shards, r, out=out)
+        torch.cuda.synchronize()
+        assert np.array_equal(_bits(out), oracle.pack(shards_h, r).view(_bits(out).dtype)), r
+        assert _intact(buf, sent)
+
+
+@pytest.mark.parametrize("b,S,n,d,G", SHARED + [(2, 64, 8, 64, 4), (1, 48, 6, 3, 3)])
+def test_unpack_add_bitexact(b, S, n, d, G):
+    """Every member adds its local tensor in member order on random shards;
+    the same order in the oracle gives the same fp32 sums bit for bit."""
+    g = torch.Generator().manual_seed(b + S + n + G)
+    nl = basp.heads_per_member(n, G)
+    Sg = S // G
+    locs = [torch.randn(b, S, nl, d, generator=g) for _ in range(G)]
+    base = [torch.randn(b, Sg, n, d, generator=g) for _ in range(G)]
+    dev, bufs = [], []
+    for x in base:
+        t, buf, sent = _guarded(x.shape, torch.float32)
+        t.copy_(x.cuda())
+        dev.append(t)
+        bufs.append(buf)
+    for l in range(G):
+        basp.unpack_add(locs[l].cuda(), dev, l)
+    torch.cuda.synchronize()
+    ref = [x.numpy().copy() for x in base]
+    for l in range(G):
+        oracle.unpack_add(locs[l].numpy(), ref, l)
+    for j in range(G):
+        assert np.array_equal(_bits(dev[j]), ref[j].view(np.int32)), j
+        assert _intact(bufs[j], sent)
+
+
+@pytest.mark.parametrize("b,S,n,d,G", SHARED)
+def test_a2a_shared_bitexact(b, S, n, d, G):
+    own_bf = random_shards(b, S, n, d, G, seed=7 * S + n + G)[0]
+    send, sbuf, sent = _guarded((G, b, S // G, 1, d), torch.bfloat16)
+    basp.a2a_pack(own_bf.cuda(), G, out=send)
+    torch.cuda.synchronize()
+    assert np.array_equal(_bits(send), oracle.a2a_pack(own_bf, G))
+    assert _intact(sbuf, sent)
+    # fp32 gradient blocks, summed per head on receipt
+    g = torch.Generator().manual_seed(S + d)
+    recv = torch.randn(G, b, S // G, 1, d, generator=g)
+    own, obuf, sent = _guarded((b, S // G, n, d), torch.float32)
+    basp.a2a_unpack(recv.cuda(), out=own, n_heads=n)
+    torch.cuda.synchronize()
+    ref = oracle.a2a_unpack(recv.numpy(), n_heads=n)
+    assert np.array_equal(_bits(own), ref.view(np.int32))
+    assert _intact(obuf, sent)
+
+
+def test_a2a_unpack_shared_bf16_is_refused():
+    recv = torch.zeros(4, 1, 8, 1, 64, dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(basp.BaspError) as e:
+        basp.a2a_unpack(recv, n_heads=2)
+    assert e.value.status == 4
+
+
+GROUP = [  # b, S, H, H_kv, d, G
+    (1, 512, 8, 2, 128, 4),
+    (2, 256, 8, 1, 64, 8),       # MQA
+    (1, 1000, 16, 4, 96, 8),     # ragged tail, d = 96
+    (1, 320, 8, 4, 80, 8),       # d = 80
+]
+
+
+@pytest.mark.parametrize("b,S,H,H_kv,d,G", GROUP)
+def test_whole_group_matches_global_oracle(b, S, H, H_kv, d, G):
+    log(f"[shared kv group] b={b} S={S} H={H} H_kv={H_kv} d={d} G={G}")
+    g = torch.Generator().manual_seed(S + H + H_kv + G)
+    mk = lambda n: torch.randn(b, S, n, d, generator=g).to(torch.bfloat16)
+    q, k, v, do = mk(H), mk(H_kv), mk(H_kv), mk(H)
+    c = 1.0 / math.sqrt(d)
+    Sg = S // G
+    sh = lambda x: [x[:, j * Sg:(j + 1) * Sg].contiguous().cuda() for j in range(G)]
+    qs, ks, vs, ds = sh(q), sh(k), sh(v), sh(do)
+    o_sh = [torch.zeros(b, Sg, H, d, dtype=torch.bfloat16, device="cuda") for _ in range(G)]
+    dq_sh = [torch.zeros(b, Sg, H, d, device="cuda") for _ in range(G)]
+    dk_sh = [torch.zeros(b, Sg, H_kv, d, device="cuda") for _ in range(G)]
+    dv_sh = [torch.zeros(b, Sg, H_kv, d, device="cuda") for _ in range(G)]
+    lse_all = []
+    dk_parts, dv_parts = [], []
+    for l in range(G):
+        ql, kl, vl, dl = (basp.pack(x, l) for x in (qs, ks, vs, ds))
+        assert kl.shape == (b, S, 1, d)
+        o, lse = basp.attn_fwd(ql, kl, vl, G=G, scale=c, H_kv=H_kv)
+        dq, dk, dv = basp.attn_bwd(ql, kl, vl, o, lse, dl, G=G, scale=c, H_kv=H_kv)
+        basp.unpack(o, o_sh, l)
+        basp.unpack(dq, dq_sh, l)
+        basp.unpack_add(dk, dk_sh, l)
+        basp.unpack_add(dv, dv_sh, l)
+        lse_all.append(lse)
+        dk_parts.append(dk)
+        dv_parts.append(dv)
+    torch.cuda.synchronize()
+    ro, rl = oracle.attn_fwd(q, k, v, c)
+    rdq, rdk, rdv = oracle.attn_bwd(q, k, v, do, ro, rl, c)
+    cat = lambda xs: torch.cat(xs, dim=1).double().cpu().numpy()
+    check_close("O", cat(o_sh), ro)
+    check_close("LSE", torch.cat(lse_all, dim=1).double().cpu().numpy(), rl,
+                max_abs=LSE_MAX_ABS, mean_abs=LSE_MAX_ABS)
+    check_close("dQ", cat(dq_sh), rdq)
+    check_close("dK", cat(dk_sh), rdk)
+    check_close("dV", cat(dv_sh), rdv)
+
+    # Owner-side route: member l's part of head h goes back as the fp32 block
+    # [l][beta][own tokens]; a2a_unpack sums each head's blocks in member
+    # order, exactly as unpack_add did in member order above.
+    for r in range(G):
+        for parts, ref_sh in ((dk_parts, dk_sh), (dv_parts, dv_sh)):
+            recv = torch.stack([parts[l][:, r * Sg:(r + 1) * Sg] for l in range(G)]).contiguous()
+            got = basp.a2a_unpack(recv, n_heads=H_kv)
+            torch.cuda.synchronize()
+            assert torch.equal(got, ref_sh[r]), r
