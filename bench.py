@@ -104,6 +104,30 @@ def cpu_baseline(w, target_s: float):
             "seconds": secs}
 
 
+def sharded_step_rate(sh, steps: int, flops: float) -> dict:
+    """The same step with attention run on the shard buffers in place (no
+    pack/unpack pass), timed like the main loop.  Skipped where the in-place
+    path does not take the shape (it raises before launching anything)."""
+    import torch
+    import paper_2609_03151_amd as basp
+
+    try:
+        sh.step_sharded()
+    except basp.BaspError as e:
+        return {"sharded_step": f"not taken: {e}"}
+    torch.cuda.synchronize()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(steps):
+        sh.step_sharded()
+    stop.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(stop) / steps
+    log(f"[bench] in-place step {ms:.3f} ms")
+    return {"sharded_ms_per_step": round(ms, 4),
+            "sharded_tflops": round(flops / (ms * 1e-3) / 1e12, 2)}
+
+
 def cold_permutation_rates(sh, reps: int = 5):
     """Each pack/unpack call timed alone with cold caches: a 1 GiB scratch
     write (larger than L2 and the 256 MB MALL) precedes every timed call; the
@@ -257,6 +281,7 @@ def main():
         "phase_ms": {p: round(t, 4) for p, t in phase_ms.items()},
         "cpu_baseline": None,
     }
+    out.update(sharded_step_rate(sh, args.steps, fwd_f + bwd_f))
     out.update(cold_permutation_rates(sh))
     log(f"[bench] cold permutations {out['pack_unpack_cold_gbps']} GB/s, "
         f"device copy {out['hbm_copy_cold_gbps']} GB/s")

@@ -15,6 +15,8 @@
  *   basp_attn_bwd  its backward (dQ, dK, dV in fp32)
  *   basp_unpack    head-sharded result -> the rank's head slice of G shards
  *   basp_unpack_add  the same for fp32 gradients, added into the shards
+ *   basp_attn_fwd_sharded / basp_attn_bwd_sharded   attention straight on
+ *                  the shard buffers of the exchange (no pack/unpack pass)
  *   basp_a2a_pack / basp_a2a_unpack   the owner's side of the same exchanges:
  *                  own shard <-> one contiguous block per member
  *
@@ -173,10 +175,31 @@ int basp_a2a_unpack(const void *recv, void *own, int b, int S, int n_heads, int 
  * 80 is computed at width 96 with zero padding, which changes nothing in the
  * result.
  * Errors: NULL, SHAPE, UNSUPPORTED (d not 64, 80, 96 or 128, scale not
- * finite and positive, or S*(H/G)*d*2 >= 2^31 bytes), ALIGN, HIP. */
+ * finite and positive, S*(H/G)*d*2 >= 2^31 bytes, b*S >= 2^31 - 1, or
+ * b > 65535), ALIGN, HIP. */
 int basp_attn_fwd(const void *q, const void *k, const void *v, void *o,
                   float *lse, int b, int S, int H, int H_kv, int d, int G,
                   float scale, void *stream);
+
+/* basp_attn_fwd on the exchange's buffers in place (Sec. II-C with
+ * Sec. II-A): Q, K, V are read from the G sequence shards the first
+ * all-to-all delivers and O is written into the rank's head slice of the G
+ * shard buffers of the second, with no pack or unpack pass:
+ *   o_shards[j][beta][t][rank*H/G + h][e] = O[beta][j*S/G + t][h][e]
+ * for O the attention of the rank's heads over the whole sequence.  The
+ * result is bit for bit that of basp_pack, basp_attn_fwd, basp_unpack.
+ * q_shards, o_shards: host arrays of G device pointers, each [b, S/G, H, d]
+ * bf16; k_shards, v_shards: each [b, S/G, H_kv, d] bf16 (the rank reads kv
+ * heads [rank*H_kv/G, ..), or the one shared head when H_kv < G); lse
+ * [b, H/G, S] fp32 as basp_attn_fwd.  Heads of o_shards outside the rank's
+ * slice are untouched.  Alignment: every shard pointer 16 bytes, lse 4.
+ * Errors: as basp_attn_fwd, plus RANK, and UNSUPPORTED when G > 16, S/G is
+ * not a multiple of 256, or (S/G)*max(H, H_kv)*d*4 >= 2^31 bytes. */
+int basp_attn_fwd_sharded(const void *const *q_shards,
+                          const void *const *k_shards,
+                          const void *const *v_shards, void *const *o_shards,
+                          float *lse, int b, int S, int H, int H_kv, int d,
+                          int G, int rank, float scale, void *stream);
 
 /* Bytes of device workspace basp_attn_bwd needs for this shape. */
 size_t basp_attn_bwd_workspace_bytes(int b, int S, int H, int H_kv, int d,
@@ -196,6 +219,26 @@ int basp_attn_bwd(const void *q, const void *k, const void *v, const void *o,
                   float *dv, void *workspace, size_t workspace_bytes, int b,
                   int S, int H, int H_kv, int d, int G, float scale,
                   void *stream);
+
+/* basp_attn_bwd on the exchange's buffers in place: Q, K, V, O and dO are
+ * read from their G sequence shards (layouts as basp_attn_fwd_sharded; dO as
+ * Q) and dQ, dK, dV (fp32) are written into the rank's head slices of their
+ * G shard buffers ([b, S/G, H, d] for dQ, [b, S/G, H_kv, d] for dK and dV);
+ * other heads are untouched.  The result is bit for bit that of basp_pack
+ * (of dO), basp_attn_bwd and basp_unpack of each gradient.  lse and the
+ * workspace (same size as basp_attn_bwd's) as there.
+ * Errors: as basp_attn_fwd_sharded, plus WORKSPACE, and UNSUPPORTED when
+ * H_kv < G (members sharing a kv head would overwrite each other's partial
+ * gradients: use basp_attn_bwd and basp_unpack_add). */
+int basp_attn_bwd_sharded(const void *const *q_shards,
+                          const void *const *k_shards,
+                          const void *const *v_shards,
+                          const void *const *o_shards, const float *lse,
+                          const void *const *do_shards, float *const *dq_shards,
+                          float *const *dk_shards, float *const *dv_shards,
+                          void *workspace, size_t workspace_bytes, int b,
+                          int S, int H, int H_kv, int d, int G, int rank,
+                          float scale, void *stream);
 
 #ifdef __cplusplus
 }

@@ -28,7 +28,8 @@ STATUS = {
 # Every symbol include/basp.h declares.
 EXPORTS = ("basp_status_str", "basp_group_of", "basp_validate", "basp_pack",
            "basp_unpack", "basp_unpack_add", "basp_a2a_pack", "basp_a2a_unpack", "basp_attn_fwd",
-           "basp_attn_bwd_workspace_bytes", "basp_attn_bwd")
+           "basp_attn_fwd_sharded", "basp_attn_bwd_workspace_bytes", "basp_attn_bwd",
+           "basp_attn_bwd_sharded")
 
 
 class BaspError(RuntimeError):
@@ -65,6 +66,10 @@ def lib() -> ctypes.CDLL:
     L.basp_attn_bwd_workspace_bytes.argtypes = [i] * 6
     L.basp_attn_bwd_workspace_bytes.restype = sz
     L.basp_attn_bwd.argtypes = [vp] * 10 + [sz] + [i] * 6 + [f, vp]
+    tab = ctypes.POINTER(vp)
+    L.basp_attn_fwd_sharded.argtypes = [tab] * 4 + [vp] + [i] * 7 + [f, vp]
+    L.basp_attn_bwd_sharded.argtypes = ([tab] * 4 + [vp] + [tab] * 4 + [vp, sz] + [i] * 7
+                                        + [f, vp])
     for name in ("basp_group_of", "basp_validate", "basp_pack", "basp_unpack",
                  "basp_a2a_pack", "basp_a2a_unpack", "basp_attn_fwd", "basp_attn_bwd"):
         getattr(L, name).restype = i
@@ -255,3 +260,51 @@ def attn_bwd(q, k, v, o, lse, do, G: int = 1, scale: float | None = None,
         workspace.numel() * workspace.element_size(), b, S, H, H_kv, d, G, float(scale),
         _stream(q)), "basp_attn_bwd")
     return dq, dk, dv
+
+
+# ------------------------------------------------- attention on the shards
+def _table(shards, name, dtype):
+    return (ctypes.c_void_p * len(shards))(*[_dev(t, f"{name}[{j}]", dtype).value
+                                             for j, t in enumerate(shards)])
+
+
+def attn_fwd_sharded(q_shards, k_shards, v_shards, o_shards, rank: int,
+                     scale: float | None = None, lse=None):
+    """Attention of the rank's heads read from the G sequence shards (each
+    [b, S/G, H or H_kv, d] bf16) and written into the rank's head slice of
+    o_shards; returns lse [b, H/G, S]."""
+    G = len(q_shards)
+    b, Sg, H, d = q_shards[0].shape
+    H_kv = k_shards[0].shape[2]
+    S = Sg * G
+    scale = d ** -0.5 if scale is None else scale
+    if lse is None:
+        lse = torch.empty((b, H // G, S), dtype=torch.float32, device=q_shards[0].device)
+    bf = torch.bfloat16
+    _check(lib().basp_attn_fwd_sharded(
+        _table(q_shards, "q", bf), _table(k_shards, "k", bf), _table(v_shards, "v", bf),
+        _table(o_shards, "o", bf), _dev(lse, "lse", torch.float32), b, S, H, H_kv, d, G, rank,
+        float(scale), _stream(lse)), "basp_attn_fwd_sharded")
+    return lse
+
+
+def attn_bwd_sharded(q_shards, k_shards, v_shards, o_shards, lse, do_shards, dq_shards,
+                     dk_shards, dv_shards, rank: int, scale: float | None = None,
+                     workspace=None):
+    """Backward of attn_fwd_sharded: dQ, dK, dV (fp32) into the rank's head
+    slices of their shard buffers."""
+    G = len(q_shards)
+    b, Sg, H, d = q_shards[0].shape
+    H_kv = k_shards[0].shape[2]
+    S = Sg * G
+    scale = d ** -0.5 if scale is None else scale
+    need = attn_bwd_workspace_bytes(b, S, H, H_kv, d, G)
+    if workspace is None:
+        workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=lse.device)
+    bf, f32 = torch.bfloat16, torch.float32
+    _check(lib().basp_attn_bwd_sharded(
+        _table(q_shards, "q", bf), _table(k_shards, "k", bf), _table(v_shards, "v", bf),
+        _table(o_shards, "o", bf), _dev(lse, "lse", f32), _table(do_shards, "do", bf),
+        _table(dq_shards, "dq", f32), _table(dk_shards, "dk", f32), _table(dv_shards, "dv", f32),
+        _dev(workspace, "workspace"), workspace.numel() * workspace.element_size(),
+        b, S, H, H_kv, d, G, rank, float(scale), _stream(lse)), "basp_attn_bwd_sharded")

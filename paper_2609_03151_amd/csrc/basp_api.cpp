@@ -9,6 +9,8 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <initializer_list>
+
 #include "../../include/basp.h"
 #include "basp_internal.hpp"
 
@@ -47,6 +49,7 @@ int check_attn(int b, int S, int H, int H_kv, int d, int G, float scale) {
   // Row indices inside the kernels are 32-bit: b*S must fit, and one head's
   // span of a tensor (S rows of H/G heads) is addressed with 31-bit offsets.
   if ((long long)b * S >= (long long)INT_MAX) return BASP_ERR_UNSUPPORTED;
+  if (b > 65535) return BASP_ERR_UNSUPPORTED;  // one grid dimension per sequence
   if ((long long)S * (H / G) * d * 2 >= (1LL << 31)) return BASP_ERR_UNSUPPORTED;
   return BASP_OK;
 }
@@ -211,7 +214,54 @@ int run_a2a(bool to_send, const void *src, void *dst, int b, int S, int n, int d
   return hip_status(basp::launch_permute(st, dt, s, (hipStream_t)stream));
 }
 
+// Shape rules of the sharded (in-place) attention entry points, after
+// check_attn: the shard buffers become the kernels' row views, so a view
+// holds at most kMaxViewBuffers buffers, a shard's rows are a multiple of the
+// 256-row workgroup tiles, and one buffer's head span is addressed with
+// 31-bit offsets (fp32 gradients included).
+int check_sharded(int S, int H, int H_kv, int d, int G, int rank) {
+  if (rank < 0 || rank >= G) return BASP_ERR_RANK;
+  if (G > basp::kMaxViewBuffers) return BASP_ERR_UNSUPPORTED;
+  if ((S / G) % 256 != 0) return BASP_ERR_UNSUPPORTED;
+  const int nmax = H > H_kv ? H : H_kv;
+  if ((long long)(S / G) * nmax * d * 4 >= (1LL << 31)) return BASP_ERR_UNSUPPORTED;
+  return BASP_OK;
+}
+
+int check_shard_table(const void *const *tab, int G) {
+  if (!tab) return BASP_ERR_NULL;
+  for (int j = 0; j < G; ++j)
+    if (!tab[j]) return BASP_ERR_NULL;
+  for (int j = 0; j < G; ++j)
+    if (!aligned(tab[j], 16)) return BASP_ERR_ALIGN;
+  return BASP_OK;
+}
+
 }  // namespace
+
+namespace basp {
+
+RowView local_view(const void *p, int S, int nl, int d) {
+  RowView v{};
+  v.p[0] = p;
+  v.rows = (uint32_t)(S > 0 ? S : 1);
+  v.by_rows = FastDiv::make(v.rows);
+  v.row_elems = (uint32_t)(nl * d);
+  v.head0 = 0;
+  return v;
+}
+
+RowView shard_view(const void *const *shards, int G, int S, int n, int d, int rank) {
+  RowView v{};
+  for (int j = 0; j < G; ++j) v.p[j] = shards[j];
+  v.rows = (uint32_t)(S / G);
+  v.by_rows = FastDiv::make(v.rows);
+  v.row_elems = (uint32_t)(n * d);
+  v.head0 = (uint32_t)((long long)rank * n / G);
+  return v;
+}
+
+}  // namespace basp
 
 extern "C" {
 
@@ -294,8 +344,32 @@ int basp_attn_fwd(const void *q, const void *k, const void *v, void *o, float *l
       !aligned(lse, 4))
     return BASP_ERR_ALIGN;
   basp::AttnShape s = attn_shape(b, S, H, H_kv, d, G, scale);
+  const basp::RowView qv = basp::local_view(q, S, s.Hl, d), kv = basp::local_view(k, S, s.Hkl, d),
+                      vv = basp::local_view(v, S, s.Hkl, d), ov = basp::local_view(o, S, s.Hl, d);
   (void)hipGetLastError();
-  return hip_status(basp::launch_attn_fwd(q, k, v, o, lse, s, (hipStream_t)stream));
+  return hip_status(basp::launch_attn_fwd(qv, kv, vv, ov, lse, s, false, (hipStream_t)stream));
+}
+
+int basp_attn_fwd_sharded(const void *const *q_shards, const void *const *k_shards,
+                          const void *const *v_shards, void *const *o_shards, float *lse, int b,
+                          int S, int H, int H_kv, int d, int G, int rank, float scale,
+                          void *stream) {
+  int rc = check_attn(b, S, H, H_kv, d, G, scale);
+  if (rc) return rc;
+  rc = check_sharded(S, H, H_kv, d, G, rank);
+  if (rc) return rc;
+  if ((long long)b * S == 0) return BASP_OK;  // empty: no pointer is inspected
+  for (const void *const *t : {q_shards, k_shards, v_shards, (const void *const *)o_shards})
+    if ((rc = check_shard_table(t, G))) return rc;
+  if (!lse) return BASP_ERR_NULL;
+  if (!aligned(lse, 4)) return BASP_ERR_ALIGN;
+  basp::AttnShape s = attn_shape(b, S, H, H_kv, d, G, scale);
+  const basp::RowView qv = basp::shard_view(q_shards, G, S, H, d, rank),
+                      kv = basp::shard_view(k_shards, G, S, H_kv, d, rank),
+                      vv = basp::shard_view(v_shards, G, S, H_kv, d, rank),
+                      ov = basp::shard_view(o_shards, G, S, H, d, rank);
+  (void)hipGetLastError();
+  return hip_status(basp::launch_attn_fwd(qv, kv, vv, ov, lse, s, true, (hipStream_t)stream));
 }
 
 size_t basp_attn_bwd_workspace_bytes(int b, int S, int H, int H_kv, int d, int G) {
@@ -321,9 +395,54 @@ int basp_attn_bwd(const void *q, const void *k, const void *v, const void *o, co
   if (workspace_bytes < need) return BASP_ERR_WORKSPACE;
   if (!workspace) return BASP_ERR_NULL;
   if (!aligned(workspace, 16)) return BASP_ERR_ALIGN;
+  using basp::local_view;
+  const basp::RowView qv = local_view(q, S, s.Hl, d), kv = local_view(k, S, s.Hkl, d),
+                      vv = local_view(v, S, s.Hkl, d), ov = local_view(o, S, s.Hl, d),
+                      dov = local_view(d_o, S, s.Hl, d), dqv = local_view(dq, S, s.Hl, d),
+                      dkv = local_view(dk, S, s.Hkl, d), dvv = local_view(dv, S, s.Hkl, d);
   (void)hipGetLastError();
-  return hip_status(
-      basp::launch_attn_bwd(q, k, v, o, lse, d_o, dq, dk, dv, workspace, s, (hipStream_t)stream));
+  return hip_status(basp::launch_attn_bwd(qv, kv, vv, ov, lse, dov, dqv, dkv, dvv, workspace, s,
+                                          false, (hipStream_t)stream));
+}
+
+int basp_attn_bwd_sharded(const void *const *q_shards, const void *const *k_shards,
+                          const void *const *v_shards, const void *const *o_shards,
+                          const float *lse, const void *const *do_shards,
+                          float *const *dq_shards, float *const *dk_shards,
+                          float *const *dv_shards, void *workspace, size_t workspace_bytes,
+                          int b, int S, int H, int H_kv, int d, int G, int rank, float scale,
+                          void *stream) {
+  int rc = check_attn(b, S, H, H_kv, d, G, scale);
+  if (rc) return rc;
+  rc = check_sharded(S, H, H_kv, d, G, rank);
+  if (rc) return rc;
+  // A kv head shared by several members gets a partial gradient from each;
+  // written in place, the members would overwrite one another.
+  if (H_kv < G) return BASP_ERR_UNSUPPORTED;
+  if ((long long)b * S == 0) return BASP_OK;  // empty: no pointer is inspected
+  using Tab = const void *const *;
+  for (Tab t : {q_shards, k_shards, v_shards, o_shards, do_shards, (Tab)dq_shards,
+                (Tab)dk_shards, (Tab)dv_shards})
+    if ((rc = check_shard_table(t, G))) return rc;
+  if (!lse) return BASP_ERR_NULL;
+  if (!aligned(lse, 4)) return BASP_ERR_ALIGN;
+  basp::AttnShape s = attn_shape(b, S, H, H_kv, d, G, scale);
+  const size_t need = basp::attn_bwd_workspace_bytes(s);
+  if (workspace_bytes < need) return BASP_ERR_WORKSPACE;
+  if (!workspace) return BASP_ERR_NULL;
+  if (!aligned(workspace, 16)) return BASP_ERR_ALIGN;
+  using basp::shard_view;
+  const basp::RowView qv = shard_view(q_shards, G, S, H, d, rank),
+                      kv = shard_view(k_shards, G, S, H_kv, d, rank),
+                      vv = shard_view(v_shards, G, S, H_kv, d, rank),
+                      ov = shard_view(o_shards, G, S, H, d, rank),
+                      dov = shard_view(do_shards, G, S, H, d, rank),
+                      dqv = shard_view((Tab)dq_shards, G, S, H, d, rank),
+                      dkv = shard_view((Tab)dk_shards, G, S, H_kv, d, rank),
+                      dvv = shard_view((Tab)dv_shards, G, S, H_kv, d, rank);
+  (void)hipGetLastError();
+  return hip_status(basp::launch_attn_bwd(qv, kv, vv, ov, lse, dov, dqv, dkv, dvv, workspace, s,
+                                          true, (hipStream_t)stream));
 }
 
 }  // extern "C"

@@ -30,6 +30,10 @@
 //     copied HBM -> LDS by buffer loads that write LDS directly (rows past S
 //     arrive as zeros) into a ring of four stages, two steps ahead; each wave
 //     waits only for its own copies and passes a fence-free barrier.
+//   * Q, K, V, O, dO and the gradients are addressed through row views:
+//     the local head-sharded tensors, or (SH) the G sequence shards of the
+//     exchange in place (row counts multiples of 256: a workgroup's rows or
+//     keys, and every streamed tile, lie in one shard).
 #include <math.h>
 
 #include <type_traits>
@@ -92,19 +96,30 @@ BwdChunks bwd_chunks(const AttnShape &s) {
 
 // ---------------------------------------------------------------- bwd_pre
 // One group of D/8 lanes per (beta, row, head); 16-byte loads of O and dO.
-template <int D>
+template <int D, bool SH>
 __global__ __launch_bounds__(kPreThreads) void bwd_pre_kernel(
-    const uint16_t *__restrict__ o, const uint16_t *__restrict__ d_o,
-    const float *__restrict__ lse, f32x2 *__restrict__ ld, long long rows /* b*S*Hl */,
-    int S, int Hl) {
+    const RowView ov, const RowView dov, const float *__restrict__ lse, f32x2 *__restrict__ ld,
+    long long rows /* b*S*Hl */, int S, int Hl) {
   constexpr int LPR = D <= 64 ? 8 : 16;  // lanes per row (a power of two >= D/8)
   const long long gid = (long long)blockIdx.x * kPreThreads + threadIdx.x;
   const long long r = gid / LPR;
   const int sub = (int)(gid % LPR);
   float acc = 0.f;
   if (r < rows && sub < D / 8) {
-    const u32x4 a = reinterpret_cast<const u32x4 *>(o + r * D)[sub];
-    const u32x4 b = reinterpret_cast<const u32x4 *>(d_o + r * D)[sub];
+    const uint16_t *orow, *drow;
+    if constexpr (SH) {  // r = (beta*S + i)*Hl + h
+      const long long bi = r / Hl;
+      const int h = (int)(r - bi * Hl);
+      const int beta = (int)(bi / S), i = (int)(bi - (long long)beta * S);
+      uint32_t left;
+      orow = view_row<true, const uint16_t>(ov, beta, i, h, D, left);
+      drow = view_row<true, const uint16_t>(dov, beta, i, h, D, left);
+    } else {  // local [b][S][Hl][D]: row r is r*D elements in
+      orow = static_cast<const uint16_t *>(ov.p[0]) + r * D;
+      drow = static_cast<const uint16_t *>(dov.p[0]) + r * D;
+    }
+    const u32x4 a = reinterpret_cast<const u32x4 *>(orow)[sub];
+    const u32x4 b = reinterpret_cast<const u32x4 *>(drow)[sub];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       acc += bf16_bits_to_f32(a[i] & 0xFFFFu) * bf16_bits_to_f32(b[i] & 0xFFFFu);
@@ -152,12 +167,13 @@ struct KvCfg {
   static constexpr int DMA_PER_WAVE = kQM * CPR / kKvThreads;  // 1 KB copies per tile
 };
 
-template <int D, int G>
+// `outv` is the final dK/dV when there is one row chunk, else the partial
+// buffer of chunk 0 (a local view), chunk ch being ch * chunk_elems further.
+template <int D, int G, bool SH>
 __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
-    const uint16_t *__restrict__ q, const uint16_t *__restrict__ k,
-    const uint16_t *__restrict__ v, const uint16_t *__restrict__ d_o,
-    const f32x2 *__restrict__ ld, float *__restrict__ out, int S, int Hl, int Hkl,
-    int n_rep, int kvheads_total, int ktiles, int nchunks, float c /* scale*log2e */,
+    const RowView qv, const RowView kv, const RowView vv, const RowView dov,
+    const f32x2 *__restrict__ ld, const RowView outv, size_t chunk_elems, int S, int Hl,
+    int Hkl, int n_rep, int kvheads_total, int ktiles, int nchunks, float c /* scale*log2e */,
     float out_scale) {
   using C = KvCfg<D>;
   using T = LdsTile<C::LW>;
@@ -189,25 +205,26 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
   const int wk0 = k0 + 32 * w;
   const int key = wk0 + l32;
 
-  const uint32_t q_row_bytes = (uint32_t)Hl * D * 2, kv_row_bytes = (uint32_t)Hkl * D * 2;
-  const size_t kvoff = ((size_t)beta * S * Hkl + kvh) * D;
-  out += (size_t)ch * ((size_t)kvheads_total * S * D);
+  const uint32_t q_row_bytes = qv.row_elems * 2, kv_row_bytes = kv.row_elems * 2;
   // K (and V for dK) of this lane's key as B operands (B[e][j] = K[j][e]).
   bf16x8 kf[C::NS], vf[G == kDK ? C::NS : 1];
   {
-    const rsrc_t rk = make_rsrc(k + kvoff, (uint32_t)S * kv_row_bytes);
+    uint32_t left;
+    const rsrc_t rk = make_rsrc(view_row<SH, const uint16_t>(kv, beta, k0, kvh, D, left),
+                                left * kv_row_bytes);
 #pragma unroll
     for (int s = 0; s < C::NS; ++s)
-      kf[s] = 2 * s < D / 8
-                  ? as_bf16x8(buf_load16(rk, (uint32_t)key * kv_row_bytes + (2 * s + hh) * 16))
-                  : bf16x8{};  // columns past D
+      kf[s] = 2 * s < D / 8 ? as_bf16x8(buf_load16(rk, (uint32_t)(key - k0) * kv_row_bytes +
+                                                           (2 * s + hh) * 16))
+                            : bf16x8{};  // columns past D
     if constexpr (G == kDK) {
-      const rsrc_t rv = make_rsrc(v + kvoff, (uint32_t)S * kv_row_bytes);
+      const rsrc_t rv = make_rsrc(view_row<SH, const uint16_t>(vv, beta, k0, kvh, D, left),
+                                  left * kv_row_bytes);
 #pragma unroll
       for (int s = 0; s < C::NS; ++s)
-        vf[s] = 2 * s < D / 8
-                    ? as_bf16x8(buf_load16(rv, (uint32_t)key * kv_row_bytes + (2 * s + hh) * 16))
-                    : bf16x8{};
+        vf[s] = 2 * s < D / 8 ? as_bf16x8(buf_load16(rv, (uint32_t)(key - k0) * kv_row_bytes +
+                                                             (2 * s + hh) * 16))
+                              : bf16x8{};
     }
   }
   wait_vmcnt<0>();  // retire the tracked loads before untracked copies start
@@ -253,10 +270,12 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
   auto load_step = [&](int st) __attribute__((always_inline)) {
     int h, i0;
     step_coords(st, h, i0);
-    const size_t hoff = ((size_t)beta * S * Hl + h) * D;
-    const u32x4 rq = make_rsrc_words(q + hoff, (uint32_t)S * q_row_bytes);
-    const u32x4 rd = make_rsrc_words(d_o + hoff, (uint32_t)S * q_row_bytes);
-    const uint32_t base = (uint32_t)i0 * q_row_bytes;
+    uint32_t left;  // the step's rows; rows past the buffer's end read as zeros
+    const u32x4 rq = make_rsrc_words(view_row<SH, const uint16_t>(qv, beta, i0, h, D, left),
+                                     left * q_row_bytes);
+    const u32x4 rd = make_rsrc_words(view_row<SH, const uint16_t>(dov, beta, i0, h, D, left),
+                                     left * q_row_bytes);
+    const uint32_t base = 0;
     const uint32_t stage = smem_lds + (st % kStages) * C::STAGE_BYTES;
 #pragma unroll
     for (int i = 0; i < C::DMA_PER_WAVE; ++i) {
@@ -388,7 +407,9 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
 
   // acc[n][r] = (dV or dK)^T[e = 32n + 8(r/4) + 4hh + r%4][key]
   if (key < S) {
-    float *o = out + ((size_t)(beta * S + key) * Hkl + kvh) * D;
+    uint32_t left;
+    float *o = view_row<true, float>(outv, beta, k0, kvh, D, left) + (size_t)ch * chunk_elems +
+               (size_t)(key - k0) * outv.row_elems;
 #pragma unroll
     for (int n = 0; n < C::NE; ++n)
 #pragma unroll
@@ -404,16 +425,19 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
 // ---------------------------------------------------------------- bwd_reduce
 // dK or dV of a key = the sum of the partial sums of the row chunks that
 // exist for its key tile, added in chunk order (deterministic).  One thread
-// per 4 consecutive elements.
+// per 4 consecutive elements of a key's row of the rank's kv heads; grid.y is
+// the sequence.  The partials are local [chunk][b][S][Hkl][d]; the result
+// goes through the output view (the rank's heads are contiguous in a row).
 __global__ __launch_bounds__(kPreThreads) void bwd_reduce_kernel(
-    const float *__restrict__ part, float *__restrict__ out, long long n4 /* b*S*Hkl*D/4 */,
-    int S, int row_elems /* Hkl*D */, int nchunks) {
-  const long long i4 = (long long)blockIdx.x * kPreThreads + threadIdx.x;
-  if (i4 >= n4) return;
-  const long long e = i4 * 4;
-  const int key = (int)((e / row_elems) % S);
-  const int first = (key / kKN) / kTilesPerChunk;  // first chunk the key tile wrote
-  const long long slice = n4 * 4;
+    const float *__restrict__ part, const RowView outv, uint32_t row_quads /* Hkl*D/4 */,
+    FastDiv by_row_quads, uint32_t seq_quads /* S*row_quads */, size_t slice /* b*S*Hkl*D */,
+    int d, int nchunks) {
+  const uint32_t i = blockIdx.x * kPreThreads + threadIdx.x;
+  if (i >= seq_quads) return;
+  const int beta = blockIdx.y;
+  const uint32_t key = by_row_quads.div(i), cq = i - key * row_quads;
+  const size_t e = ((size_t)beta * seq_quads + i) * 4;
+  const int first = (int)(key / kKN) / kTilesPerChunk;  // first chunk the key tile wrote
   f32x4 acc = *reinterpret_cast<const f32x4 *>(part + (size_t)first * slice + e);
   for (int ch = first + 1; ch < nchunks; ++ch) {
     const f32x4 x = *reinterpret_cast<const f32x4 *>(part + (size_t)ch * slice + e);
@@ -422,7 +446,8 @@ __global__ __launch_bounds__(kPreThreads) void bwd_reduce_kernel(
     acc[2] += x[2];
     acc[3] += x[3];
   }
-  *reinterpret_cast<f32x4 *>(out + e) = acc;
+  uint32_t left;
+  *reinterpret_cast<f32x4 *>(view_row<true, float>(outv, beta, key, 0, d, left) + 4 * cq) = acc;
 }
 
 // ---------------------------------------------------------------- bwd_dq
@@ -443,12 +468,11 @@ struct DqCfg {
   static constexpr int DMA_PER_WAVE = kDQN * CPR / kDqThreads;
 };
 
-template <int D>
+template <int D, bool SH>
 __global__ __launch_bounds__(kDqThreads, 1) void bwd_dq_kernel(
-    const uint16_t *__restrict__ q, const uint16_t *__restrict__ k,
-    const uint16_t *__restrict__ v, const uint16_t *__restrict__ d_o,
-    const f32x2 *__restrict__ ld, float *__restrict__ dq, int S, int Hl, int Hkl, int n_rep,
-    int heads_total, int qtiles, float c, float scale) {
+    const RowView qv, const RowView kv, const RowView vv, const RowView dov,
+    const f32x2 *__restrict__ ld, const RowView dqv, int S, int Hl, int n_rep, int heads_total,
+    int qtiles, float c, float scale) {
   using C = DqCfg<D>;
   using T = LdsTile<C::LW>;
   __shared__ __attribute__((aligned(16))) unsigned char smem[kStages * C::STAGE_BYTES];
@@ -464,20 +488,27 @@ __global__ __launch_bounds__(kDqThreads, 1) void bwd_dq_kernel(
   const int wrow0 = q0 + 32 * w;
   const int row = wrow0 + l32;
 
-  const uint32_t q_row_bytes = (uint32_t)Hl * D * 2, kv_row_bytes = (uint32_t)Hkl * D * 2;
-  const size_t hoff = ((size_t)beta * S * Hl + h) * D;
-  const rsrc_t rq = make_rsrc(q + hoff, (uint32_t)S * q_row_bytes);
-  const rsrc_t rd = make_rsrc(d_o + hoff, (uint32_t)S * q_row_bytes);
-  const u32x4 rk = make_rsrc_words(k + ((size_t)beta * S * Hkl + kvh) * D, (uint32_t)S * kv_row_bytes);
-  const u32x4 rv = make_rsrc_words(v + ((size_t)beta * S * Hkl + kvh) * D, (uint32_t)S * kv_row_bytes);
+  const uint32_t q_row_bytes = qv.row_elems * 2, kv_row_bytes = kv.row_elems * 2;
+  uint32_t left;
+  const rsrc_t rq =
+      make_rsrc(view_row<SH, const uint16_t>(qv, beta, q0, h, D, left), left * q_row_bytes);
+  const rsrc_t rd =
+      make_rsrc(view_row<SH, const uint16_t>(dov, beta, q0, h, D, left), left * q_row_bytes);
+  u32x4 rk = {}, rv = {};  // local K/V: one resource per head; sharded: one per shard
+  if constexpr (!SH) {
+    rk = make_rsrc_words(view_row<false, const uint16_t>(kv, beta, 0, kvh, D, left),
+                         left * kv_row_bytes);
+    rv = make_rsrc_words(view_row<false, const uint16_t>(vv, beta, 0, kvh, D, left),
+                         left * kv_row_bytes);
+  }
   const uint32_t smem_lds = lds_addr_of(smem);
 
   bf16x8 qf[C::NS], df[C::NS];
 #pragma unroll
   for (int s = 0; s < C::NS; ++s) {
     if (2 * s < D / 8) {
-      qf[s] = as_bf16x8(buf_load16(rq, (uint32_t)row * q_row_bytes + (2 * s + hh) * 16));
-      df[s] = as_bf16x8(buf_load16(rd, (uint32_t)row * q_row_bytes + (2 * s + hh) * 16));
+      qf[s] = as_bf16x8(buf_load16(rq, (uint32_t)(row - q0) * q_row_bytes + (2 * s + hh) * 16));
+      df[s] = as_bf16x8(buf_load16(rd, (uint32_t)(row - q0) * q_row_bytes + (2 * s + hh) * 16));
     } else {  // columns past D
       qf[s] = bf16x8{};
       df[s] = bf16x8{};
@@ -495,9 +526,26 @@ __global__ __launch_bounds__(kDqThreads, 1) void bwd_dq_kernel(
 #pragma unroll
   for (int i = 0; i < C::DMA_PER_WAVE; ++i)
     g_off[i] = dma_src_off<C::LW, D>((w * C::DMA_PER_WAVE + i) * 64 + lane, kv_row_bytes);
+  // Sharded: tiles are loaded in order, so the resources move to the next
+  // shard only when the tiles of the current one are used up.
+  uint32_t sh_tiles = 0, sh_base = 0;
   auto load_tile = [&](int t) __attribute__((always_inline)) {
     const uint32_t ks = smem_lds + (t % kStages) * C::STAGE_BYTES;
-    const uint32_t base = (uint32_t)(t * kDQN) * kv_row_bytes;
+    uint32_t base = (uint32_t)(t * kDQN) * kv_row_bytes;
+    if constexpr (SH) {
+      if (sh_tiles == 0) {  // wave-uniform; tile t is the first of its shard
+        uint32_t tl;
+        rk = make_rsrc_words(view_row<true, const uint16_t>(kv, beta, t * kDQN, kvh, D, tl),
+                             tl * kv_row_bytes);
+        rv = make_rsrc_words(view_row<true, const uint16_t>(vv, beta, t * kDQN, kvh, D, tl),
+                             tl * kv_row_bytes);
+        sh_tiles = tl / kDQN;
+        sh_base = 0;
+      }
+      base = sh_base;
+      sh_base += kDQN * kv_row_bytes;
+      --sh_tiles;
+    }
 #pragma unroll
     for (int i = 0; i < C::DMA_PER_WAVE; ++i) {
       const uint32_t lds = ks + (w * C::DMA_PER_WAVE + i) * 1024;
@@ -609,7 +657,7 @@ __global__ __launch_bounds__(kDqThreads, 1) void bwd_dq_kernel(
   }
 
   if (row < S) {
-    float *dqr = dq + ((size_t)(beta * S + row) * Hl + h) * D;
+    float *dqr = view_row<SH, float>(dqv, beta, q0, h, D, left) + (size_t)(row - q0) * dqv.row_elems;
 #pragma unroll
     for (int n = 0; n < C::NE; ++n)
 #pragma unroll
@@ -622,15 +670,11 @@ __global__ __launch_bounds__(kDqThreads, 1) void bwd_dq_kernel(
   }
 }
 
-template <int D>
-hipError_t launch_bwd_d(const void *q, const void *k, const void *v, const void *o,
-                        const float *lse, const void *d_o, float *dq, float *dk,
-                        float *dv, float *ws, const AttnShape &s, hipStream_t stream) {
-  auto *qp = static_cast<const uint16_t *>(q);
-  auto *kp = static_cast<const uint16_t *>(k);
-  auto *vp = static_cast<const uint16_t *>(v);
-  auto *op = static_cast<const uint16_t *>(o);
-  auto *dop = static_cast<const uint16_t *>(d_o);
+template <int D, bool SH>
+hipError_t launch_bwd_d(const RowView &q, const RowView &k, const RowView &v, const RowView &o,
+                        const float *lse, const RowView &d_o, const RowView &dq,
+                        const RowView &dk, const RowView &dv, float *ws, const AttnShape &s,
+                        hipStream_t stream) {
   auto *ld = reinterpret_cast<f32x2 *>(ws);
   const float c = s.scale * kLog2e;
   const int n_rep = s.Hl / s.Hkl;
@@ -638,38 +682,45 @@ hipError_t launch_bwd_d(const void *q, const void *k, const void *v, const void 
   const long long rows = (long long)s.b * s.S * s.Hl;
   const long long pre_threads = rows * (D <= 64 ? 8 : 16);
   const long long pre_blocks = (pre_threads + kPreThreads - 1) / kPreThreads;
-  hipLaunchKernelGGL(bwd_pre_kernel<D>, dim3((unsigned)pre_blocks), dim3(kPreThreads), 0, stream,
-                     op, dop, lse, ld, rows, s.S, s.Hl);
+  hipLaunchKernelGGL((bwd_pre_kernel<D, SH>), dim3((unsigned)pre_blocks), dim3(kPreThreads), 0,
+                     stream, o, d_o, lse, ld, rows, s.S, s.Hl);
 
   const int ktiles = (s.S + kKN - 1) / kKN;
   const int kvheads_total = s.b * s.Hkl;
   const BwdChunks ck = bwd_chunks(s);
   const dim3 kv_grid((unsigned)(ck.units * kvheads_total));
-  float *dv_out = dv, *dk_out = dk;
+  RowView dv_out = dv, dk_out = dk;
+  size_t chunk_elems = 0;
+  float *dv_part = nullptr, *dk_part = nullptr;
   if (ck.n > 1) {  // partial sums in the workspace, reduced below
-    dv_out = ws + ck.part_offset_floats;
-    dk_out = dv_out + (size_t)ck.n * kvheads_total * s.S * D;
+    chunk_elems = (size_t)kvheads_total * s.S * D;
+    dv_part = ws + ck.part_offset_floats;
+    dk_part = dv_part + (size_t)ck.n * chunk_elems;
+    dv_out = local_view(dv_part, s.S, s.Hkl, D);
+    dk_out = local_view(dk_part, s.S, s.Hkl, D);
   }
-  hipLaunchKernelGGL((bwd_kv_kernel<D, kDV>), kv_grid, dim3(kKvThreads), 0, stream, qp, kp, vp,
-                     dop, ld, dv_out, s.S, s.Hl, s.Hkl, n_rep, kvheads_total, ktiles, ck.n, c,
-                     1.f);
-  hipLaunchKernelGGL((bwd_kv_kernel<D, kDK>), kv_grid, dim3(kKvThreads), 0, stream, qp, kp, vp,
-                     dop, ld, dk_out, s.S, s.Hl, s.Hkl, n_rep, kvheads_total, ktiles, ck.n, c,
-                     s.scale);
+  hipLaunchKernelGGL((bwd_kv_kernel<D, kDV, SH>), kv_grid, dim3(kKvThreads), 0, stream, q, k, v,
+                     d_o, ld, dv_out, chunk_elems, s.S, s.Hl, s.Hkl, n_rep, kvheads_total, ktiles,
+                     ck.n, c, 1.f);
+  hipLaunchKernelGGL((bwd_kv_kernel<D, kDK, SH>), kv_grid, dim3(kKvThreads), 0, stream, q, k, v,
+                     d_o, ld, dk_out, chunk_elems, s.S, s.Hl, s.Hkl, n_rep, kvheads_total, ktiles,
+                     ck.n, c, s.scale);
   if (ck.n > 1) {
-    const long long n4 = (long long)kvheads_total * s.S * D / 4;
-    const dim3 rg((unsigned)((n4 + kPreThreads - 1) / kPreThreads));
-    hipLaunchKernelGGL(bwd_reduce_kernel, rg, dim3(kPreThreads), 0, stream, dv_out, dv, n4, s.S,
-                       s.Hkl * D, ck.n);
-    hipLaunchKernelGGL(bwd_reduce_kernel, rg, dim3(kPreThreads), 0, stream, dk_out, dk, n4, s.S,
-                       s.Hkl * D, ck.n);
+    const uint32_t row_quads = (uint32_t)(s.Hkl * D / 4);
+    const uint32_t seq_quads = (uint32_t)s.S * row_quads;
+    const dim3 rg((seq_quads + kPreThreads - 1) / kPreThreads, (unsigned)s.b);
+    const FastDiv by_rq = FastDiv::make(row_quads);
+    hipLaunchKernelGGL(bwd_reduce_kernel, rg, dim3(kPreThreads), 0, stream, dv_part, dv,
+                       row_quads, by_rq, seq_quads, chunk_elems, D, ck.n);
+    hipLaunchKernelGGL(bwd_reduce_kernel, rg, dim3(kPreThreads), 0, stream, dk_part, dk,
+                       row_quads, by_rq, seq_quads, chunk_elems, D, ck.n);
   }
 
   const int qtiles = (s.S + kDQM - 1) / kDQM;
   const int heads_total = s.b * s.Hl;
-  hipLaunchKernelGGL(bwd_dq_kernel<D>, dim3((unsigned)(qtiles * heads_total)), dim3(kDqThreads),
-                     0, stream, qp, kp, vp, dop, ld, dq, s.S, s.Hl, s.Hkl, n_rep, heads_total,
-                     qtiles, c, s.scale);
+  hipLaunchKernelGGL((bwd_dq_kernel<D, SH>), dim3((unsigned)(qtiles * heads_total)),
+                     dim3(kDqThreads), 0, stream, q, k, v, d_o, ld, dq, s.S, s.Hl, n_rep,
+                     heads_total, qtiles, c, s.scale);
   return hipGetLastError();
 }
 
@@ -682,18 +733,23 @@ size_t attn_bwd_workspace_bytes(const AttnShape &s) {
   return floats * sizeof(float);
 }
 
-hipError_t launch_attn_bwd(const void *q, const void *k, const void *v,
-                           const void *o, const float *lse, const void *d_o,
-                           float *dq, float *dk, float *dv, void *workspace,
-                           const AttnShape &s, hipStream_t stream) {
+hipError_t launch_attn_bwd(const RowView &q, const RowView &k, const RowView &v,
+                           const RowView &o, const float *lse, const RowView &d_o,
+                           const RowView &dq, const RowView &dk, const RowView &dv,
+                           void *workspace, const AttnShape &s, bool sharded,
+                           hipStream_t stream) {
   if ((long long)s.b * s.S == 0) return hipSuccess;
   float *ws = static_cast<float *>(workspace);
-  switch (s.d) {
-    case 64: return launch_bwd_d<64>(q, k, v, o, lse, d_o, dq, dk, dv, ws, s, stream);
-    case 80: return launch_bwd_d<80>(q, k, v, o, lse, d_o, dq, dk, dv, ws, s, stream);
-    case 96: return launch_bwd_d<96>(q, k, v, o, lse, d_o, dq, dk, dv, ws, s, stream);
-    default: return launch_bwd_d<128>(q, k, v, o, lse, d_o, dq, dk, dv, ws, s, stream);
-  }
+  auto by_dim = [&](auto sh) {
+    constexpr bool SH = decltype(sh)::value;
+    switch (s.d) {
+      case 64: return launch_bwd_d<64, SH>(q, k, v, o, lse, d_o, dq, dk, dv, ws, s, stream);
+      case 80: return launch_bwd_d<80, SH>(q, k, v, o, lse, d_o, dq, dk, dv, ws, s, stream);
+      case 96: return launch_bwd_d<96, SH>(q, k, v, o, lse, d_o, dq, dk, dv, ws, s, stream);
+      default: return launch_bwd_d<128, SH>(q, k, v, o, lse, d_o, dq, dk, dv, ws, s, stream);
+    }
+  };
+  return sharded ? by_dim(std::true_type{}) : by_dim(std::false_type{});
 }
 
 }  // namespace basp

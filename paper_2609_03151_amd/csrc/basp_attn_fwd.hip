@@ -36,6 +36,11 @@
 //     any masking code; band tiles are masked, and a wave skips band tiles
 //     past its last row.  The grid is one-dimensional, heaviest query tiles
 //     first, heads fastest, so heads sharing a kv head run side by side.
+//   * tensors are read and written through row views: the local
+//     head-sharded tensors, or (SH) the G sequence shards of the exchange in
+//     place, whose row counts are multiples of 256 so that a workgroup's
+//     rows and a key tile each lie in one shard; K/V tiles then take the
+//     buffer of their own rows.
 #include <math.h>
 
 #include <type_traits>
@@ -69,12 +74,11 @@ struct FwdCfg {
   static constexpr int DMA_PER_WAVE = kBN * CPR / kThreads;  // 1 KB loads per wave per tensor
 };
 
-template <int D>
+template <int D, bool SH>
 __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
-    const uint16_t *__restrict__ q, const uint16_t *__restrict__ k,
-    const uint16_t *__restrict__ v, uint16_t *__restrict__ o,
-    float *__restrict__ lse, int S, int Hl, int Hkl, int n_rep, int heads_total,
-    int qtiles, float c /* scale * log2(e) */) {
+    const RowView qv, const RowView kv, const RowView vv, const RowView ov,
+    float *__restrict__ lse, int S, int Hl, int n_rep, int heads_total, int qtiles,
+    float c /* scale * log2(e) */) {
   using C = FwdCfg<D>;
   using T = LdsTile<C::LW>;
   __shared__ __attribute__((aligned(16))) unsigned char smem[kStages * C::STAGE_BYTES];
@@ -91,18 +95,28 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
   const int wrow0 = q0 + 32 * w;
   const int row = wrow0 + l32;
 
-  const uint32_t q_row_bytes = (uint32_t)Hl * D * 2, kv_row_bytes = (uint32_t)Hkl * D * 2;
-  const rsrc_t rq = make_rsrc(q + ((size_t)beta * S * Hl + h) * D, (uint32_t)S * q_row_bytes);
-  const u32x4 rk = make_rsrc_words(k + ((size_t)beta * S * Hkl + kvh) * D, (uint32_t)S * kv_row_bytes);
-  const u32x4 rv = make_rsrc_words(v + ((size_t)beta * S * Hkl + kvh) * D, (uint32_t)S * kv_row_bytes);
+  const uint32_t q_row_bytes = qv.row_elems * 2, kv_row_bytes = kv.row_elems * 2;
+  uint32_t q_left, kv_left;
+  // Q of rows q0 .. (rows past the buffer's end read as zeros)
+  const rsrc_t rq =
+      make_rsrc(view_row<SH, const uint16_t>(qv, beta, q0, h, D, q_left), q_left * q_row_bytes);
+  // Local K/V: one resource per head for every tile.  Sharded: one per shard.
+  u32x4 rk = {}, rv = {};
+  if constexpr (!SH) {
+    rk = make_rsrc_words(view_row<false, const uint16_t>(kv, beta, 0, kvh, D, kv_left),
+                         kv_left * kv_row_bytes);
+    rv = make_rsrc_words(view_row<false, const uint16_t>(vv, beta, 0, kvh, D, kv_left),
+                         kv_left * kv_row_bytes);
+  }
   const uint32_t smem_lds = lds_addr_of(smem);
 
   // Q fragments (B operand of S^T = K Q^T): row `row`, e = 16s + 8hh .. +7.
   bf16x8 qf[C::NS];
 #pragma unroll
   for (int s = 0; s < C::NS; ++s)
-    qf[s] = 2 * s < D / 8 ? as_bf16x8(buf_load16(rq, (uint32_t)row * q_row_bytes + (2 * s + hh) * 16))
-                          : bf16x8{};  // columns past D
+    qf[s] = 2 * s < D / 8
+                ? as_bf16x8(buf_load16(rq, (uint32_t)(row - q0) * q_row_bytes + (2 * s + hh) * 16))
+                : bf16x8{};  // columns past D
   // Retire the Q loads before any tile copy is in flight: the compiler does
   // not count the copies, and a wait for Q inside the tile loop would also
   // drain the prefetched tiles.
@@ -115,9 +129,26 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
 #pragma unroll
   for (int i = 0; i < C::DMA_PER_WAVE; ++i)
     g_off[i] = dma_src_off<C::LW, D>((w * C::DMA_PER_WAVE + i) * 64 + lane, kv_row_bytes);
+  // Sharded: tiles are loaded in order, so the resources move to the next
+  // shard only when the tiles of the current one are used up.
+  uint32_t sh_tiles = 0, sh_base = 0;
   auto load_tile = [&](int t) {  // issue; lands asynchronously in stage t % kStages
     const uint32_t ks = smem_lds + (t % kStages) * C::STAGE_BYTES;
-    const uint32_t base = (uint32_t)(t * kBN) * kv_row_bytes;
+    uint32_t base = (uint32_t)(t * kBN) * kv_row_bytes;
+    if constexpr (SH) {
+      if (sh_tiles == 0) {  // wave-uniform; tile t is the first of its shard
+        uint32_t left;
+        rk = make_rsrc_words(view_row<true, const uint16_t>(kv, beta, t * kBN, kvh, D, left),
+                             left * kv_row_bytes);
+        rv = make_rsrc_words(view_row<true, const uint16_t>(vv, beta, t * kBN, kvh, D, left),
+                             left * kv_row_bytes);
+        sh_tiles = left / kBN;
+        sh_base = 0;
+      }
+      base = sh_base;
+      sh_base += kBN * kv_row_bytes;
+      --sh_tiles;
+    }
 #pragma unroll
     for (int i = 0; i < C::DMA_PER_WAVE; ++i) {
       const uint32_t lds_off = ks + (w * C::DMA_PER_WAVE + i) * 1024;
@@ -282,7 +313,9 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
   const float l_tot = pair_sum(l_run);
   if (row < S) {
     const float inv = 1.f / l_tot;
-    uint16_t *ob = o + ((size_t)(beta * S + row) * Hl + h) * D;
+    uint32_t o_left;
+    uint16_t *ob = view_row<SH, uint16_t>(ov, beta, q0, h, D, o_left) +
+                   (size_t)(row - q0) * ov.row_elems;
 #pragma unroll
     for (int n = 0; n < C::NE; ++n)
 #pragma unroll
@@ -299,28 +332,32 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
 
 }  // namespace
 
-hipError_t launch_attn_fwd(const void *q, const void *k, const void *v, void *o,
-                           float *lse, const AttnShape &s, hipStream_t stream) {
+hipError_t launch_attn_fwd(const RowView &q, const RowView &k, const RowView &v,
+                           const RowView &o, float *lse, const AttnShape &s, bool sharded,
+                           hipStream_t stream) {
   const int qtiles = (s.S + kBM - 1) / kBM;
   const int heads_total = s.b * s.Hl;
   const long long blocks = (long long)qtiles * heads_total;
   if (blocks == 0) return hipSuccess;
   const float c = s.scale * 1.4426950408889634f;
   const int n_rep = s.Hl / s.Hkl;
-  auto *qp = static_cast<const uint16_t *>(q);
-  auto *kp = static_cast<const uint16_t *>(k);
-  auto *vp = static_cast<const uint16_t *>(v);
-  auto *op = static_cast<uint16_t *>(o);
   auto go = [&](auto kernel) {
-    hipLaunchKernelGGL(kernel, dim3((unsigned)blocks), dim3(kThreads), 0, stream, qp, kp, vp, op,
-                       lse, s.S, s.Hl, s.Hkl, n_rep, heads_total, qtiles, c);
+    hipLaunchKernelGGL(kernel, dim3((unsigned)blocks), dim3(kThreads), 0, stream, q, k, v, o, lse,
+                       s.S, s.Hl, n_rep, heads_total, qtiles, c);
   };
-  switch (s.d) {
-    case 64: go(attn_fwd_kernel<64>); break;
-    case 80: go(attn_fwd_kernel<80>); break;
-    case 96: go(attn_fwd_kernel<96>); break;
-    default: go(attn_fwd_kernel<128>); break;
-  }
+  auto by_dim = [&](auto sh) {
+    constexpr bool SH = decltype(sh)::value;
+    switch (s.d) {
+      case 64: go(attn_fwd_kernel<64, SH>); break;
+      case 80: go(attn_fwd_kernel<80, SH>); break;
+      case 96: go(attn_fwd_kernel<96, SH>); break;
+      default: go(attn_fwd_kernel<128, SH>); break;
+    }
+  };
+  if (sharded)
+    by_dim(std::true_type{});
+  else
+    by_dim(std::false_type{});
   return hipGetLastError();
 }
 

@@ -11,6 +11,62 @@
 
 namespace basp {
 
+// n / d for 32-bit n and a divisor d fixed per launch, by multiplication
+// (Granlund and Montgomery, "Division by invariant integers using
+// multiplication", 1994: the round-up multiplier with the fix-up add).
+struct FastDiv {
+  uint32_t m, s1, s2;
+  static FastDiv make(uint32_t d) {
+    uint32_t l = 0;
+    while (l < 32 && (1ull << l) < d) ++l;  // ceil(log2 d)
+    FastDiv f;
+    f.m = (uint32_t)((((1ull << 32) * ((1ull << l) - d)) / d + 1) & 0xFFFFFFFFull);
+    f.s1 = l < 1 ? l : 1;
+    f.s2 = l > 1 ? l - 1 : 0;
+    return f;
+  }
+  __device__ __forceinline__ uint32_t div(uint32_t n) const {
+    const uint32_t t1 = __umulhi(m, n);
+    return (t1 + ((n - t1) >> s1)) >> s2;
+  }
+};
+
+// How the attention kernels find one tensor of the share.  Row r (a token
+// of the full sequence) of sequence beta lies in buffer p[r / rows], at row
+// r % rows of that buffer; a row holds row_elems elements, among them the
+// rank's heads from head0 on, d elements each:
+//   p[r / rows] + ((beta * rows + r % rows) * row_elems + (head0 + h) * d + e)
+// A head-sharded local tensor [b, S, nl, d] is the one-buffer case
+// (rows = S, row_elems = nl*d, head0 = 0).  The G sequence shards
+// [b, S/G, n, d] of the exchange are G buffers (rows = S/G, row_elems = n*d,
+// head0 = rank*n/G), so the kernels read and write them in place.
+constexpr int kMaxViewBuffers = 16;
+
+struct RowView {
+  const void *p[kMaxViewBuffers];
+  FastDiv by_rows;  // division by `rows`
+  uint32_t rows, row_elems, head0;
+};
+
+RowView local_view(const void *p, int S, int nl, int d);
+RowView shard_view(const void *const *shards, int G, int S, int n, int d, int rank);
+
+// Element pointer of row r of (beta, head h) in view v, and in `left` the
+// rows of that buffer from r on.  SH = false: v is known to be one buffer
+// (no division).  r must be wave-uniform for the pointer to stay scalar.
+template <bool SH, typename T>
+__device__ __forceinline__ T *view_row(const RowView &v, int beta, uint32_t r, int h, int d,
+                                       uint32_t &left) {
+  uint32_t j = 0, t = r;
+  if constexpr (SH) {
+    j = v.by_rows.div(r);
+    t = r - j * v.rows;
+  }
+  left = v.rows - t;
+  return static_cast<T *>(const_cast<void *>(v.p[j])) +
+         (((size_t)beta * v.rows + t) * v.row_elems + (size_t)(v.head0 + h) * d);
+}
+
 // Every permutation of the library is a batch of strided row copies: G*b
 // blocks (member j, sequence beta) of Sg rows, each row a contiguous run of
 // row_bytes.  Row t of block (j, beta) goes from
@@ -43,14 +99,18 @@ struct AttnShape {
   float scale;
 };
 
-hipError_t launch_attn_fwd(const void *q, const void *k, const void *v, void *o,
-                           float *lse, const AttnShape &s, hipStream_t stream);
+// `sharded`: the views may span several buffers (sequence shards whose row
+// count is a multiple of 256, so no workgroup tile straddles two of them).
+hipError_t launch_attn_fwd(const RowView &q, const RowView &k, const RowView &v,
+                           const RowView &o, float *lse, const AttnShape &s, bool sharded,
+                           hipStream_t stream);
 
 size_t attn_bwd_workspace_bytes(const AttnShape &s);
 
-hipError_t launch_attn_bwd(const void *q, const void *k, const void *v,
-                           const void *o, const float *lse, const void *d_o,
-                           float *dq, float *dk, float *dv, void *workspace,
-                           const AttnShape &s, hipStream_t stream);
+hipError_t launch_attn_bwd(const RowView &q, const RowView &k, const RowView &v,
+                           const RowView &o, const float *lse, const RowView &d_o,
+                           const RowView &dq, const RowView &dk, const RowView &dv,
+                           void *workspace, const AttnShape &s, bool sharded,
+                           hipStream_t stream);
 
 }  // namespace basp

@@ -41,26 +41,6 @@ __device__ __forceinline__ void nt_store(V v, V *p) {
   __builtin_nontemporal_store(v, p);
 }
 
-// n / d for 32-bit n and a divisor d fixed per launch, by multiplication
-// (Granlund and Montgomery, "Division by invariant integers using
-// multiplication", 1994: the round-up multiplier with the fix-up add).
-struct FastDiv {
-  uint32_t m, s1, s2;
-  static FastDiv make(uint32_t d) {
-    uint32_t l = 0;
-    while (l < 32 && (1ull << l) < d) ++l;  // ceil(log2 d)
-    FastDiv f;
-    f.m = (uint32_t)((((1ull << 32) * ((1ull << l) - d)) / d + 1) & 0xFFFFFFFFull);
-    f.s1 = l < 1 ? l : 1;
-    f.s2 = l > 1 ? l - 1 : 0;
-    return f;
-  }
-  __device__ __forceinline__ uint32_t div(uint32_t n) const {
-    const uint32_t t1 = __umulhi(m, n);
-    return (t1 + ((n - t1) >> s1)) >> s2;
-  }
-};
-
 // One launch's geometry in V-sized vectors.
 struct CopyGeom {
   uint32_t row_vecs;               // row_bytes / sizeof(V)

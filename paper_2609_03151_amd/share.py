@@ -17,13 +17,17 @@ shard buffers accumulate over repeated backward calls.
 
 The exchange itself (RCCL all-to-all) is outside this share: the shard
 buffers stand for the receive and send buffers of that exchange.
+
+`forward_sharded` / `backward_sharded` run the same step with no pack or
+unpack pass: attention reads the shard buffers in place and writes O, dQ,
+dK, dV straight into the send buffers (bit for bit the same results).
 """
 from __future__ import annotations
 
 import torch
 
-from . import (attn_bwd, attn_bwd_workspace_bytes, attn_fwd, heads_per_member, pack, unpack,
-               unpack_add)
+from . import (attn_bwd, attn_bwd_sharded, attn_bwd_workspace_bytes, attn_fwd,
+               attn_fwd_sharded, heads_per_member, pack, unpack, unpack_add)
 
 
 class RankShare:
@@ -100,6 +104,20 @@ class RankShare:
     def step(self):
         self.forward()
         self.backward()
+
+    # attention on the shard buffers in place
+    def forward_sharded(self):
+        attn_fwd_sharded(self.q_shards, self.k_shards, self.v_shards, self.o_shards, self.rank,
+                         scale=self.scale, lse=self.lse)
+
+    def backward_sharded(self):
+        attn_bwd_sharded(self.q_shards, self.k_shards, self.v_shards, self.o_shards, self.lse,
+                         self.do_shards, self.dq_shards, self.dk_shards, self.dv_shards,
+                         self.rank, scale=self.scale, workspace=self.workspace)
+
+    def step_sharded(self):
+        self.forward_sharded()
+        self.backward_sharded()
 
     # work counts (FlashAttention convention: causal half of S^2)
     def attn_fwd_flops(self) -> float:

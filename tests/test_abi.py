@@ -165,6 +165,32 @@ def test_shared_head_calls_reject_before_any_hip_call():
     assert L.basp_attn_bwd_workspace_bytes(1, 128, 8, 2, 128, 4) > 0
 
 
+def test_sharded_attn_rejects_before_any_hip_call():
+    """Only invalid (or empty) calls: the pointer tables hold fake values."""
+    L = basp.lib()
+    vp = ctypes.c_void_p
+    tab = lambda G, base=0x100000: (vp * G)(*[base * (j + 1) for j in range(G)])
+    f = lambda x: ctypes.c_float(x)
+    fwd = lambda *a, G=4, t=None, lse=_fake(0x40), sc=0.1: L.basp_attn_fwd_sharded(
+        *([t or tab(G)] * 4), lse, *a, f(sc), None)
+    assert fwd(1, 1024, 8, 2, 128, 4, 4) == RANK
+    assert fwd(1, 1002, 8, 2, 128, 4, 0) == SHAPE                  # S % G
+    assert fwd(1, 1536, 8, 2, 128, 4, 0) == UNSUP                  # 384 rows per shard
+    assert fwd(1, 32 * 256, 32, 32, 128, 32, 0, G=32) == UNSUP     # G > 16
+    assert fwd(1, 1024, 8, 2, 72, 4, 0) == UNSUP                   # head dim
+    assert fwd(1, 1024, 8, 2, 128, 4, 0, t=(vp * 4)(0x1000, 0, 0x3000, 0x4000)) == NULL
+    assert fwd(1, 1024, 8, 2, 128, 4, 0, t=(vp * 4)(0x1000, 0x2008, 0x3000, 0x4000)) == ALIGN
+    assert fwd(1, 1024, 8, 2, 128, 4, 0, lse=None) == NULL
+    assert fwd(0, 1024, 8, 2, 128, 4, 0) == OK                     # empty
+    bwd = lambda *a, G=4, ws=_fake(0x80), n=1 << 30: L.basp_attn_bwd_sharded(
+        *([tab(G)] * 4), _fake(0x40), *([tab(G)] * 4), ws, n, *a, f(0.1), None)
+    assert bwd(1, 1024, 8, 2, 128, 4, 1) == UNSUP                  # shared kv head (2 < 4)
+    assert bwd(1, 1024, 8, 4, 128, 4, 1, n=16) == WS
+    assert bwd(1, 1024, 8, 4, 128, 4, 1, ws=None) == NULL
+    assert bwd(1, 1024, 8, 4, 128, 4, 9) == RANK
+    assert bwd(0, 1024, 8, 4, 128, 4, 1) == OK
+
+
 def test_attn_rejects_before_any_hip_call():
     L = basp.lib()
     p = [_fake(0x10000 * (i + 1)) for i in range(10)]
