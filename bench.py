@@ -17,6 +17,7 @@ from __future__ import annotations
 
 import argparse
 import json
+import math
 import os
 import sys
 import time
@@ -89,13 +90,16 @@ def cpu_baseline(w, target_s: float):
         oracle.attn_bwd(qq, kk, vv, dd, o, lse, w.scale)
         return time.perf_counter() - t0
 
-    # Work grows with S'^2: calibrate on a prefix large enough for the
-    # quadratic term to dominate, then size the sample to the target time.
-    cal = min(2048, w.S)
-    t_cal = run(cal)
-    Sp = int(cal * (target_s / max(t_cal, 1e-6)) ** 0.5)
-    Sp = max(cal, min(w.S, (Sp // 64) * 64))
-    secs = run(Sp) if Sp != cal else t_cal
+    # Work grows about as S'^2, a little faster once rows leave the caches:
+    # time two prefixes, fit the exponent, and size the sample to the target.
+    c1, c2 = min(2048, w.S), min(4096, w.S)
+    t1 = run(c1)
+    t2 = run(c2) if c2 > c1 else t1
+    e = math.log(max(t2, 1e-6) / max(t1, 1e-6)) / math.log(c2 / c1) if c2 > c1 else 2.0
+    e = min(max(e, 2.0), 3.0)
+    Sp = int(c2 * (target_s / max(t2, 1e-6)) ** (1.0 / e))
+    Sp = max(c2, min(w.S, (Sp // 64) * 64))
+    secs = run(Sp) if Sp != c2 else t2
     flops = 3.5 * 2.0 * 1 * w.Hl * w.d * float(Sp) ** 2
     return {"value": flops / secs / 1e12, "unit": "TFLOP/s", "cores": oracle.threads(),
             "kind": "oracle",

@@ -30,6 +30,9 @@
 //     copied HBM -> LDS by buffer loads that write LDS directly (rows past S
 //     arrive as zeros) into a ring of four stages, two steps ahead; each wave
 //     waits only for its own copies and passes a fence-free barrier.
+//   * each wave raises its issue priority over the accumulating products
+//     (dV, dK, dQ), so the two waves of a SIMD drift apart and one's
+//     elementwise work overlaps the other's MFMAs.
 //   * Q, K, V, O, dO and the gradients are addressed through row views:
 //     the local head-sharded tensors, or (SH) the G sequence shards of the
 //     exchange in place (row counts multiples of 256: a workgroup's rows or
@@ -379,6 +382,9 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
         b[s2] = as_bf16x8(t4);
       }
       // dV^T += dO^T P  or  dK^T += Q^T dS: M = head dim, N = keys, K = rows.
+      // Raised priority: these products run ahead of the partner wave's
+      // elementwise work.
+      wave_priority<1>();
 #pragma unroll
       for (int n = 0; n < C::NE; ++n)
 #pragma unroll
@@ -389,6 +395,7 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
         }
       sched_reads_ahead<2 * C::NE, 2, 4>();
       __builtin_amdgcn_sched_barrier(0);  // keep the two halves apart (register pressure)
+      wave_priority<0>();
     }
   };
 
@@ -625,7 +632,8 @@ __global__ __launch_bounds__(kDqThreads, 1) void bwd_dq_kernel(
         sb[s2] = as_bf16x8(ts);
       }
       // dQ^T += K^T dS^T: M = head dim, N = rows, K = keys; K^T straight
-      // from the row-major K tile.
+      // from the row-major K tile.  Raised priority, as in bwd_kv.
+      wave_priority<1>();
 #pragma unroll
       for (int n = 0; n < C::NE; ++n)
 #pragma unroll
@@ -636,6 +644,7 @@ __global__ __launch_bounds__(kDqThreads, 1) void bwd_dq_kernel(
         }
       sched_reads_ahead<2 * C::NE, 2, 4>();
       __builtin_amdgcn_sched_barrier(0);  // keep the two halves apart (register pressure)
+      wave_priority<0>();
     }
   };
   auto step = [&](int t) __attribute__((always_inline)) {

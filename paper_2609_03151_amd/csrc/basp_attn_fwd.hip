@@ -36,6 +36,8 @@
 //     any masking code; band tiles are masked, and a wave skips band tiles
 //     past its last row.  The grid is one-dimensional, heaviest query tiles
 //     first, heads fastest, so heads sharing a kv head run side by side.
+//   * a wave raises its issue priority over the score products, so the two
+//     waves of a SIMD drift apart: one's softmax overlaps the other's MFMAs.
 //   * tensors are read and written through row views: the local
 //     head-sharded tensors, or (SH) the G sequence shards of the exchange in
 //     place, whose row counts are multiples of 256 so that a workgroup's
@@ -202,6 +204,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
     const unsigned char *Ks = smem + (t % kStages) * C::STAGE_BYTES;
     const unsigned char *Vs = Ks + C::TILE_BYTES;
 
+    wave_priority<1>();  // the score products run ahead of the partner wave's softmax
     f32x16 sacc[2];
 #pragma unroll
     for (int m = 0; m < 2; ++m) {
@@ -223,6 +226,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
       __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 2, 0);
     }
     __builtin_amdgcn_sched_group_barrier(kSchedMfma, 4, 0);
+    wave_priority<0>();
 
     // sacc[m][r] = S^T[key j0 + 32m + 8(r/4) + 4hh + r%4][query row]
     if constexpr (MASK) {

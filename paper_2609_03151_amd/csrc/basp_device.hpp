@@ -125,6 +125,19 @@ __device__ __forceinline__ float pair_sum(float x) {
   return lo + hi;
 }
 
+// Issue priority of this wave on its SIMD (s_setprio, 0 = default).  The
+// two waves that share a SIMD run the same tile loop side by side; raising
+// the priority over one block of MFMAs lets whichever wave gets there first
+// keep the matrix unit while the other does its VALU work, instead of both
+// alternating through both phases.  Scheduling barriers keep the compiler
+// from moving instructions across the switch.
+template <int P>
+__device__ __forceinline__ void wave_priority() {
+  __builtin_amdgcn_sched_barrier(0);
+  __builtin_amdgcn_s_setprio(P);
+  __builtin_amdgcn_sched_barrier(0);
+}
+
 // s_waitcnt vmcnt(n) with the other counters left alone (n < 64).
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
