@@ -25,8 +25,10 @@ struct FastDiv {
     f.s2 = l > 1 ? l - 1 : 0;
     return f;
   }
-  __device__ __forceinline__ uint32_t div(uint32_t n) const {
-    const uint32_t t1 = __umulhi(m, n);
+  // High half of m*n written as a 64-bit product, which the device compiler
+  // turns into one multiply-high; callable on the host for checking.
+  __host__ __device__ __forceinline__ uint32_t div(uint32_t n) const {
+    const uint32_t t1 = (uint32_t)(((uint64_t)m * n) >> 32);
     return (t1 + ((n - t1) >> s1)) >> s2;
   }
 };
