@@ -133,9 +133,10 @@ def sharded_step_rate(sh, steps: int, flops: float) -> dict:
 
 
 def cold_permutation_rates(sh, reps: int = 5):
-    """Each pack/unpack call timed alone with cold caches: a 1 GiB scratch
-    write (larger than L2 and the 256 MB MALL) precedes every timed call; the
-    median of `reps` runs per call.  Also a plain device-to-device copy of
+    """Each pack/unpack call of the step (the batched Q/K/V pack and gradient
+    unpack, and the O unpack and dO pack), and each single-tensor permutation,
+    timed alone with cold caches: a 1 GiB scratch write (larger than L2 and
+    the 256 MB MALL) precedes every timed call; the median of `reps` runs.  Also a plain device-to-device copy of
     the largest permutation's size under the same conditions, as the
     achievable HBM rate, and the send/receive-side permutations of the
     owner's shard (basp_a2a_pack / basp_a2a_unpack) at the same shapes."""
@@ -155,8 +156,8 @@ def cold_permutation_rates(sh, reps: int = 5):
             ts.append(e0.elapsed_time(e1))
         return statistics.median(ts)
 
-    calls = sh.permutation_calls()
-    per = {name: (cold(fn), nbytes) for name, fn, nbytes in calls}
+    per = {name: (cold(fn), nbytes) for name, fn, nbytes in sh.step_permutation_calls()}
+    each = {name: (cold(fn), nbytes) for name, fn, nbytes in sh.permutation_calls()}
     # The owner's side of the same exchanges (send pack of the own Q and K
     # shards, receive unpack of O and of fp32 dQ), outside the step.
     import paper_2609_03151_amd as basp
@@ -175,7 +176,7 @@ def cold_permutation_rates(sh, reps: int = 5):
     }
     total_ms = sum(t for t, _ in per.values())
     total_bytes = sum(b for _, b in per.values())
-    biggest = max(b for _, b in per.values()) // 2
+    biggest = max(b for _, b in each.values()) // 2
     src = torch.empty(biggest // 4, dtype=torch.float32, device="cuda").fill_(2.0)
     dst = torch.empty_like(src)
     copy_ms = cold(lambda: dst.copy_(src))
@@ -183,6 +184,8 @@ def cold_permutation_rates(sh, reps: int = 5):
     return {
         "pack_unpack_cold_gbps": round(total_bytes / (total_ms * 1e-3) / 1e9, 1),
         "pack_unpack_cold_gbps_by_call": {n: round(b / (t * 1e-3) / 1e9, 1) for n, (t, b) in per.items()},
+        "pack_unpack_cold_gbps_by_tensor": {n: round(b / (t * 1e-3) / 1e9, 1)
+                                            for n, (t, b) in each.items()},
         "hbm_copy_cold_gbps": round(2 * biggest / (copy_ms * 1e-3) / 1e9, 1),
         "a2a_cold_gbps_by_call": {n: round(b / (t * 1e-3) / 1e9, 1) for n, (t, b) in a2a.items()},
     }

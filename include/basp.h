@@ -15,6 +15,8 @@
  *   basp_attn_bwd  its backward (dQ, dK, dV in fp32)
  *   basp_unpack    head-sharded result -> the rank's head slice of G shards
  *   basp_unpack_add  the same for fp32 gradients, added into the shards
+ *   basp_pack_qkv / basp_unpack_grads   a step's three packs, or its three
+ *                  gradient unpacks, in one launch
  *   basp_attn_fwd_sharded / basp_attn_bwd_sharded   attention straight on
  *                  the shard buffers of the exchange (no pack/unpack pass)
  *   basp_a2a_pack / basp_a2a_unpack   the owner's side of the same exchanges:
@@ -133,6 +135,28 @@ int basp_unpack(const void *src, void *const *dst_shards, int b, int S,
  * fp32; shards as basp_pack with 4-byte elements.  Errors as basp_pack. */
 int basp_unpack_add(const float *src, float *const *dst_shards, int b, int S,
                     int n_heads, int d, int G, int rank, void *stream);
+
+/* The receive side of a step's first exchange in one call (Sec. II-C: Q, K
+ * and V are exchanged together): the same as basp_pack of Q (n = H), then
+ * of K and V (n = H_kv), bit for bit, with one kernel launch for all three
+ * when G <= 16 and the rows allow the same access width (small K and V packs
+ * then do not each pay a launch).  q, k, v: device [b, S, H/G, d] and
+ * [b, S, Hkl, d] (Hkl as for basp_attn_fwd).  Errors: those of the three
+ * basp_pack calls, checked before anything is launched. */
+int basp_pack_qkv(const void *const *q_shards, const void *const *k_shards,
+                  const void *const *v_shards, void *q, void *k, void *v, int b,
+                  int S, int H, int H_kv, int d, int G, int rank, int dtype,
+                  void *stream);
+
+/* The send side of the backward's last exchange in one call: basp_unpack of
+ * dQ (n = H), then of dK and dV (n = H_kv), fp32, bit for bit, as one launch
+ * under the conditions of basp_pack_qkv.  When H_kv < G the rank's kv head is
+ * shared and dK, dV are added into the shards as basp_unpack_add does (the
+ * caller clears them first).  Errors: those of the three unpacks. */
+int basp_unpack_grads(const float *dq, const float *dk, const float *dv,
+                      float *const *dq_shards, float *const *dk_shards,
+                      float *const *dv_shards, int b, int S, int H, int H_kv,
+                      int d, int G, int rank, void *stream);
 
 /* Send side of the first all-to-all, on the owner of a sequence shard
  * (Sec. II-C: every member sends each other member that member's share of

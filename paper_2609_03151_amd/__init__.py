@@ -27,7 +27,7 @@ STATUS = {
 }
 # Every symbol include/basp.h declares.
 EXPORTS = ("basp_status_str", "basp_group_of", "basp_validate", "basp_pack",
-           "basp_unpack", "basp_unpack_add", "basp_a2a_pack", "basp_a2a_unpack", "basp_attn_fwd",
+           "basp_unpack", "basp_unpack_add", "basp_pack_qkv", "basp_unpack_grads", "basp_a2a_pack", "basp_a2a_unpack", "basp_attn_fwd",
            "basp_attn_fwd_sharded", "basp_attn_bwd_workspace_bytes", "basp_attn_bwd",
            "basp_attn_bwd_sharded")
 
@@ -60,6 +60,8 @@ def lib() -> ctypes.CDLL:
     L.basp_pack.argtypes = [ctypes.POINTER(vp), vp] + [i] * 7 + [vp]
     L.basp_unpack.argtypes = [vp, ctypes.POINTER(vp)] + [i] * 7 + [vp]
     L.basp_unpack_add.argtypes = [vp, ctypes.POINTER(vp)] + [i] * 6 + [vp]
+    L.basp_pack_qkv.argtypes = [ctypes.POINTER(vp)] * 3 + [vp] * 3 + [i] * 8 + [vp]
+    L.basp_unpack_grads.argtypes = [vp] * 3 + [ctypes.POINTER(vp)] * 3 + [i] * 7 + [vp]
     L.basp_a2a_pack.argtypes = [vp, vp] + [i] * 6 + [vp]
     L.basp_a2a_unpack.argtypes = [vp, vp] + [i] * 6 + [vp]
     L.basp_attn_fwd.argtypes = [vp] * 5 + [i] * 6 + [f, vp]
@@ -169,6 +171,43 @@ def unpack_add(local: torch.Tensor, shards, rank: int):
     _check(lib().basp_unpack_add(_dev(local, "local", torch.float32), ptrs, b, Sg * G, n, d, G,
                                  rank, _stream(local)), "basp_unpack_add")
     return shards
+
+
+def pack_qkv(q_shards, k_shards, v_shards, rank: int, q=None, k=None, v=None):
+    """pack of Q, K and V in one call (one launch when G <= 16); returns (q, k, v)."""
+    G = len(q_shards)
+    b, Sg, H, d = q_shards[0].shape
+    H_kv = k_shards[0].shape[2]
+    dt = q_shards[0].dtype
+    dev = q_shards[0].device
+    if q is None:
+        q = torch.empty((b, Sg * G, heads_per_member(H, G), d), dtype=dt, device=dev)
+    if k is None:
+        k = torch.empty((b, Sg * G, heads_per_member(H_kv, G), d), dtype=dt, device=dev)
+    if v is None:
+        v = torch.empty_like(k)
+    tab = lambda xs, nm: (ctypes.c_void_p * G)(*[_dev(t, f"{nm}[{j}]", dt).value
+                                                 for j, t in enumerate(xs)])
+    _check(lib().basp_pack_qkv(tab(q_shards, "q_shards"), tab(k_shards, "k_shards"),
+                               tab(v_shards, "v_shards"), _dev(q, "q", dt), _dev(k, "k", dt),
+                               _dev(v, "v", dt), b, Sg * G, H, H_kv, d, G, rank, _dtype_code(q),
+                               _stream(q)), "basp_pack_qkv")
+    return q, k, v
+
+
+def unpack_grads(dq, dk, dv, dq_shards, dk_shards, dv_shards, rank: int):
+    """fp32 unpack of dQ, dK, dV in one call; dK, dV are added into the shards
+    when the rank's kv head is shared (H_kv < G)."""
+    G = len(dq_shards)
+    b, Sg, H, d = dq_shards[0].shape
+    H_kv = dk_shards[0].shape[2]
+    f32 = torch.float32
+    tab = lambda xs, nm: (ctypes.c_void_p * G)(*[_dev(t, f"{nm}[{j}]", f32).value
+                                                 for j, t in enumerate(xs)])
+    _check(lib().basp_unpack_grads(_dev(dq, "dq", f32), _dev(dk, "dk", f32), _dev(dv, "dv", f32),
+                                   tab(dq_shards, "dq_shards"), tab(dk_shards, "dk_shards"),
+                                   tab(dv_shards, "dv_shards"), b, Sg * G, H, H_kv, d, G, rank,
+                                   _stream(dq)), "basp_unpack_grads")
 
 
 def a2a_pack(own: torch.Tensor, G: int, out: torch.Tensor | None = None) -> torch.Tensor:

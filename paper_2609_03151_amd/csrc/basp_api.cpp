@@ -123,39 +123,51 @@ basp::PermShape perm_base(int b, int S, int n, int d, int G, uint64_t elem) {
 }
 
 // Receive-side pack (to_local) or send-side unpack of the rank's head slice;
-// `add` (fp32 only) adds the local rows into the shards instead.
-int run_pack(bool to_local, bool add, const void *const *shards, const void *local, int b, int S,
-             int n, int d, int G, int rank, int dtype, void *stream) {
+// `add` (fp32 only) adds the local rows into the shards instead.  Checks the
+// arguments and fills `pc`; `*empty` is set when there is nothing to move
+// (b*S == 0, no pointer inspected).
+int prep_pack(bool to_local, bool add, const void *const *shards, const void *local, int b, int S,
+              int n, int d, int G, int rank, int dtype, basp::PermCall *pc, bool *empty) {
   int rc = check_perm_shape(b, S, n, d, G, dtype);
   if (rc) return rc;
   if (rank < 0 || rank >= G) return BASP_ERR_RANK;
   // A head shared by several members cannot take one member's rows alone.
   if (!to_local && !add && n < G) return BASP_ERR_SHAPE;
-  // An empty problem touches no memory: its pointers are not inspected.
-  if ((long long)b * S == 0) return BASP_OK;
+  *empty = (long long)b * S == 0;
+  if (*empty) return BASP_OK;
   if (!shards || !local) return BASP_ERR_NULL;
   const uint64_t elem = dtype == BASP_BF16 ? 2 : 4;
-  basp::PermShape s = perm_base(b, S, n, d, G, elem);
-  const void *one[BASP_MAX_GROUP];
-  for (int j = 0; j < G; ++j) one[j] = local;
+  basp::PermShape &s = pc->s;
+  s = perm_base(b, S, n, d, G, elem);
   const uint64_t head0 = (uint64_t)rank * n / G;
+  for (int j = 0; j < G; ++j) {
+    if (to_local) {
+      pc->src[j] = shards[j];
+      pc->dst[j] = const_cast<void *>(local);
+    } else {
+      pc->src[j] = local;
+      pc->dst[j] = const_cast<void *>(shards[j]);
+    }
+  }
   if (to_local) {
     shard_side(S, n, d, G, elem, head0, s.src_beta, s.src_j, s.src_row, s.src_off);
     local_side(S, n, d, G, elem, s.dst_beta, s.dst_j, s.dst_row, s.dst_off);
-    rc = finish_perm(shards, const_cast<void *const *>(one), elem, &s);
-    if (rc) return rc;
-    (void)hipGetLastError();
-    return hip_status(basp::launch_permute(shards, const_cast<void *const *>(one), s,
-                                           (hipStream_t)stream));
+  } else {
+    local_side(S, n, d, G, elem, s.src_beta, s.src_j, s.src_row, s.src_off);
+    shard_side(S, n, d, G, elem, head0, s.dst_beta, s.dst_j, s.dst_row, s.dst_off);
+    if (add) s.mode = basp::PermMode::kAddDst;
   }
-  local_side(S, n, d, G, elem, s.src_beta, s.src_j, s.src_row, s.src_off);
-  shard_side(S, n, d, G, elem, head0, s.dst_beta, s.dst_j, s.dst_row, s.dst_off);
-  if (add) s.mode = basp::PermMode::kAddDst;
-  rc = finish_perm(one, const_cast<void *const *>(shards), elem, &s);
-  if (rc) return rc;
+  return finish_perm(pc->src, pc->dst, elem, &s);
+}
+
+int run_pack(bool to_local, bool add, const void *const *shards, const void *local, int b, int S,
+             int n, int d, int G, int rank, int dtype, void *stream) {
+  basp::PermCall pc;
+  bool empty = false;
+  const int rc = prep_pack(to_local, add, shards, local, b, S, n, d, G, rank, dtype, &pc, &empty);
+  if (rc || empty) return rc;
   (void)hipGetLastError();
-  return hip_status(basp::launch_permute(one, const_cast<void *const *>(shards), s,
-                                         (hipStream_t)stream));
+  return hip_status(basp::launch_permute(pc.src, pc.dst, pc.s, (hipStream_t)stream));
 }
 
 // Send-side split of the own shard (to_send) or its receive-side inverse.
@@ -316,6 +328,39 @@ int basp_unpack(const void *src, void *const *dst_shards, int b, int S, int n_he
                 int G, int rank, int dtype, void *stream) {
   return run_pack(false, false, const_cast<const void *const *>(dst_shards), src, b, S, n_heads, d, G,
                   rank, dtype, stream);
+}
+
+int basp_pack_qkv(const void *const *q_shards, const void *const *k_shards,
+                  const void *const *v_shards, void *q, void *k, void *v, int b, int S, int H,
+                  int H_kv, int d, int G, int rank, int dtype, void *stream) {
+  basp::PermCall pc[3];
+  bool empty = false;
+  int rc = prep_pack(true, false, q_shards, q, b, S, H, d, G, rank, dtype, &pc[0], &empty);
+  if (!rc) rc = prep_pack(true, false, k_shards, k, b, S, H_kv, d, G, rank, dtype, &pc[1], &empty);
+  if (!rc) rc = prep_pack(true, false, v_shards, v, b, S, H_kv, d, G, rank, dtype, &pc[2], &empty);
+  if (rc || empty) return rc;
+  (void)hipGetLastError();
+  return hip_status(basp::launch_permute_batch(pc, 3, (hipStream_t)stream));
+}
+
+int basp_unpack_grads(const float *dq, const float *dk, const float *dv, float *const *dq_shards,
+                      float *const *dk_shards, float *const *dv_shards, int b, int S, int H,
+                      int H_kv, int d, int G, int rank, void *stream) {
+  using Tab = const void *const *;
+  const bool add_kv = H_kv < G;  // a shared kv head: each member adds its part
+  basp::PermCall pc[3];
+  bool empty = false;
+  int rc = prep_pack(false, false, (Tab)dq_shards, dq, b, S, H, d, G, rank, BASP_F32, &pc[0],
+                     &empty);
+  if (!rc)
+    rc = prep_pack(false, add_kv, (Tab)dk_shards, dk, b, S, H_kv, d, G, rank, BASP_F32, &pc[1],
+                   &empty);
+  if (!rc)
+    rc = prep_pack(false, add_kv, (Tab)dv_shards, dv, b, S, H_kv, d, G, rank, BASP_F32, &pc[2],
+                   &empty);
+  if (rc || empty) return rc;
+  (void)hipGetLastError();
+  return hip_status(basp::launch_permute_batch(pc, 3, (hipStream_t)stream));
 }
 
 int basp_unpack_add(const float *src, float *const *dst_shards, int b, int S, int n_heads, int d,

@@ -96,6 +96,18 @@ struct PermShape {
 hipError_t launch_permute(const void *const *src_tab, void *const *dst_tab, const PermShape &s,
                           hipStream_t stream);
 
+// One permutation with its pointer tables, ready to launch.
+struct PermCall {
+  PermShape s;
+  const void *src[BASP_MAX_GROUP];
+  void *dst[BASP_MAX_GROUP];
+};
+
+// Up to three permutations in one launch when each has at most
+// kMaxViewBuffers members and all take the same vector width (at least 4
+// bytes); otherwise one launch each.  Results are those of launch_permute.
+hipError_t launch_permute_batch(const PermCall *calls, int n, hipStream_t stream);
+
 struct AttnShape {
   int b, S, Hl, Hkl, d;  // local heads
   float scale;

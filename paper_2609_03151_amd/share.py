@@ -10,6 +10,9 @@ once, and chains the library calls:
   forward:  pack(Q), pack(K), pack(V) -> attn_fwd -> unpack(O)
   backward: pack(dO) -> attn_bwd -> unpack(dQ), unpack(dK), unpack(dV)
 
+(the three packs and the three gradient unpacks each as one call,
+pack_qkv / unpack_grads).
+
 With fewer kv heads than members (H_kv < G, G divisible by H_kv) the rank
 holds one kv head shared by G/H_kv members, and its dK, dV are that head's
 partial gradients: they are added into the shards (unpack_add), so the dK/dV
@@ -27,7 +30,8 @@ from __future__ import annotations
 import torch
 
 from . import (attn_bwd, attn_bwd_sharded, attn_bwd_workspace_bytes, attn_fwd,
-               attn_fwd_sharded, heads_per_member, pack, unpack, unpack_add)
+               attn_fwd_sharded, heads_per_member, pack, pack_qkv, unpack, unpack_add,
+               unpack_grads)
 
 
 class RankShare:
@@ -65,9 +69,8 @@ class RankShare:
 
     # individual steps, so that callers can time them
     def pack_qkv(self):
-        pack(self.q_shards, self.rank, out=self.q)
-        pack(self.k_shards, self.rank, out=self.k)
-        pack(self.v_shards, self.rank, out=self.v)
+        pack_qkv(self.q_shards, self.k_shards, self.v_shards, self.rank, q=self.q, k=self.k,
+                 v=self.v)
 
     def attn_fwd(self):
         attn_fwd(self.q, self.k, self.v, G=self.G, scale=self.scale, out=self.o, lse=self.lse,
@@ -87,9 +90,8 @@ class RankShare:
         (unpack_add if self.shared_kv else unpack)(local, shards, self.rank)
 
     def unpack_grads(self):
-        unpack(self.dq, self.dq_shards, self.rank)
-        self._unpack_kv_grad(self.dk, self.dk_shards)
-        self._unpack_kv_grad(self.dv, self.dv_shards)
+        unpack_grads(self.dq, self.dk, self.dv, self.dq_shards, self.dk_shards, self.dv_shards,
+                     self.rank)
 
     def forward(self):
         self.pack_qkv()
@@ -126,8 +128,16 @@ class RankShare:
     def attn_bwd_flops(self) -> float:
         return 2.5 * self.attn_fwd_flops()
 
+    def step_permutation_calls(self) -> list:
+        """(name, call, bytes read + written) of the four pack/unpack calls a step makes."""
+        nb = self.pack_unpack_bytes()
+        return [("pack_qkv", self.pack_qkv, nb["pack_qkv"]),
+                ("unpack_o", self.unpack_o, nb["unpack_o"]),
+                ("pack_do", self.pack_do, nb["pack_do"]),
+                ("unpack_grads", self.unpack_grads, nb["unpack_grads"])]
+
     def permutation_calls(self) -> list:
-        """(name, call, bytes read + written) of each of the eight pack/unpack calls of a step."""
+        """(name, call, bytes read + written) of each of the eight single-tensor permutations."""
         two = lambda t: 2 * t.numel() * t.element_size()
         # an added gradient is read on both sides and written once
         kv_grad = (lambda t: 3 * t.numel() * t.element_size()) if self.shared_kv else two

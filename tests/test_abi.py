@@ -191,6 +191,32 @@ def test_sharded_attn_rejects_before_any_hip_call():
     assert bwd(0, 1024, 8, 4, 128, 4, 1) == OK
 
 
+def test_batched_permutations_reject_before_any_hip_call():
+    """basp_pack_qkv / basp_unpack_grads: any of the three tensors' errors
+    stops the call before a launch (fake pointers; only invalid or empty)."""
+    L = basp.lib()
+    vp = ctypes.c_void_p
+    tab = lambda base: (vp * 4)(*[base + 0x1000 * j for j in range(4)])
+    a, b_, c = _fake(0x100000), _fake(0x200000), _fake(0x300000)
+    pk = lambda *x, t=None: L.basp_pack_qkv(*(t or (tab(0x10000), tab(0x20000), tab(0x30000))),
+                                           a, b_, c, *x, None)
+    assert pk(1, 1024, 8, 3, 128, 4, 0, 0) == SHAPE          # 3 kv heads over 4 members
+    assert pk(1, 1022, 8, 4, 128, 4, 0, 0) == SHAPE          # S % G
+    assert pk(1, 1024, 8, 4, 128, 4, 4, 0) == RANK
+    assert pk(1, 1024, 8, 4, 128, 4, 0, 7) == UNSUP          # dtype
+    assert pk(1, 1024, 8, 4, 128, 4, 0, 0,
+              t=(tab(0x10000), (vp * 4)(0x20000, 0, 0x22000, 0x23000), tab(0x30000))) == NULL
+    assert pk(1, 1024, 8, 4, 128, 4, 0, 0,
+              t=(tab(0x10000), tab(0x20000), (vp * 4)(0x30001, 0x31000, 0x32000, 0x33000))) == ALIGN
+    assert pk(0, 1024, 8, 4, 128, 4, 0, 0) == OK             # empty
+    ug = lambda *x, t=None: L.basp_unpack_grads(a, b_, c, *(t or (tab(0x10000), tab(0x20000),
+                                                                   tab(0x30000))), *x, None)
+    assert ug(1, 1024, 8, 3, 128, 4, 0) == SHAPE
+    assert ug(1, 1024, 8, 4, 128, 4, -1) == RANK
+    assert ug(1, 1024, 8, 4, 128, 4, 0, t=(None, tab(0x20000), tab(0x30000))) == NULL
+    assert ug(0, 1024, 8, 2, 128, 4, 0) == OK
+
+
 def test_attn_rejects_before_any_hip_call():
     L = basp.lib()
     p = [_fake(0x10000 * (i + 1)) for i in range(10)]

@@ -23,6 +23,16 @@ def _bits(t: torch.Tensor) -> np.ndarray:
     return t.view(torch.int32).numpy()
 
 
+def _guards_intact(buf, sent) -> bool:
+    whole = buf.cpu().numpy()
+    s = np.array(sent).astype(whole.dtype)
+    return bool(np.all(whole[:64] == s) and np.all(whole[-64:] == s))
+
+
+def _bits_t(t: torch.Tensor) -> torch.Tensor:
+    return t.view(torch.int16) if t.dtype == torch.bfloat16 else t.view(torch.int32)
+
+
 def _guarded(shape, dtype, pad=64, dev="cuda"):
     """A tensor of `shape` inside a sentinel-filled buffer with `pad` guard
     elements on each side; returns (view, whole buffer)."""
@@ -152,3 +162,55 @@ def test_pack_unpack_full_size(name):
             del f32, acc
         del shards, glob, out
     torch.cuda.empty_cache()
+
+
+BATCH = [  # b, S, H, H_kv, d, G, rank, dtype
+    (1, 2048, 32, 8, 128, 4, 1, torch.bfloat16),
+    (2, 600, 12, 4, 64, 4, 3, torch.bfloat16),     # 150 tokens per shard
+    (1, 384, 8, 2, 80, 8, 5, torch.bfloat16),      # shared kv head (2 < 8)
+    (3, 96, 6, 3, 5, 3, 2, torch.bfloat16),        # odd head dim: 2-byte rows, separate launches
+    (1, 512, 32, 32, 128, 32, 7, torch.bfloat16),  # G > 16: separate launches
+    (1, 1024, 16, 8, 128, 8, 6, torch.float32),
+]
+
+
+@pytest.mark.parametrize("b,S,H,H_kv,d,G,rank,dtype", BATCH)
+def test_pack_qkv_equals_three_packs(b, S, H, H_kv, d, G, rank, dtype):
+    """basp_pack_qkv (one launch where it can) against three basp_pack calls
+    and the oracle, bit for bit, with sentinel guard bands."""
+    qs_h = random_shards(b, S, H, d, G, seed=S + H, dtype=dtype)
+    ks_h = random_shards(b, S, H_kv, d, G, seed=S + H_kv + 1, dtype=dtype)
+    vs_h = random_shards(b, S, H_kv, d, G, seed=S + H_kv + 2, dtype=dtype)
+    qs, ks, vs = ([x.cuda() for x in xs] for xs in (qs_h, ks_h, vs_h))
+    nq, nk = basp.heads_per_member(H, G), basp.heads_per_member(H_kv, G)
+    q, qbuf, sent = _guarded((b, S, nq, d), dtype)
+    k, kbuf, _ = _guarded((b, S, nk, d), dtype)
+    v, vbuf, _ = _guarded((b, S, nk, d), dtype)
+    basp.pack_qkv(qs, ks, vs, rank, q=q, k=k, v=v)
+    torch.cuda.synchronize()
+    for got, sh_h, sh, buf in ((q, qs_h, qs, qbuf), (k, ks_h, ks, kbuf), (v, vs_h, vs, vbuf)):
+        assert np.array_equal(_bits(got), oracle.pack(sh_h, rank).view(_bits(got).dtype))
+        assert torch.equal(_bits_t(got), _bits_t(basp.pack(sh, rank)))
+        assert _guards_intact(buf, sent)
+
+
+@pytest.mark.parametrize("b,S,H,H_kv,d,G,rank,dtype", BATCH)
+def test_unpack_grads_equals_three_unpacks(b, S, H, H_kv, d, G, rank, dtype):
+    """basp_unpack_grads against basp_unpack of dQ and basp_unpack (or
+    basp_unpack_add, for a shared kv head) of dK and dV, bit for bit."""
+    g = torch.Generator().manual_seed(b + S + G)
+    nq, nk = basp.heads_per_member(H, G), basp.heads_per_member(H_kv, G)
+    dq, dk, dv = (torch.randn(b, S, n, d, generator=g).cuda() for n in (nq, nk, nk))
+    Sg = S // G
+    base = [[torch.randn(b, Sg, n, d, generator=g).cuda() for _ in range(G)] for n in (H, H_kv, H_kv)]
+    got = [[t.clone() for t in xs] for xs in base]
+    ref = [[t.clone() for t in xs] for xs in base]
+    basp.unpack_grads(dq, dk, dv, *got, rank)
+    basp.unpack(dq, ref[0], rank)
+    kv_op = basp.unpack_add if H_kv < G else basp.unpack
+    kv_op(dk, ref[1], rank)
+    kv_op(dv, ref[2], rank)
+    torch.cuda.synchronize()
+    for xs, ys in zip(got, ref):
+        for x, y in zip(xs, ys):
+            assert torch.equal(x.view(torch.int32), y.view(torch.int32))
