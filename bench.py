@@ -272,7 +272,7 @@ def main():
         "config": {"workload": w.name, "b": w.b, "S": w.S, "H": w.H, "H_kv": w.H_kv, "d": w.d,
                    "G": w.G, "rank": w.rank, "causal": True, "inputs": "bf16 N(0,1), seeded"},
         "roofline": {
-            "kernel": ("basp_attn_bwd (bwd_pre, bwd_kv<dV>, bwd_kv<dK>, 2 x bwd_reduce, bwd_dq)"
+            "kernel": ("basp_attn_bwd (bwd_pre, bwd_kv, 2 x bwd_reduce, bwd_dq)"
                        if dom == "attn_bwd" else "basp_attn_fwd"),
             "bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),

@@ -27,6 +27,13 @@ FLAGS = [
     f"-I{os.path.join(ROOT, 'include')}",
 ]
 
+# Per-file flags.  The key-stationary backward keeps its accumulators in
+# AGPRs (inline asm); the compiler's own MFMAs there must stay in VGPR form,
+# or their results are copied out of AGPRs on every step.
+FILE_FLAGS = {
+    "basp_attn_bwd.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
+}
+
 
 def sources():
     return sorted(glob.glob(os.path.join(CSRC, "*.hip")) + glob.glob(os.path.join(CSRC, "*.cpp")))
@@ -34,7 +41,7 @@ def sources():
 
 def _compile(src: str, verbose: bool) -> str:
     obj = os.path.join(OBJDIR, os.path.basename(src) + ".o")
-    cmd = [HIPCC, *FLAGS, "-c", src, "-o", obj]
+    cmd = [HIPCC, *FLAGS, *FILE_FLAGS.get(os.path.basename(src), []), "-c", src, "-o", obj]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)

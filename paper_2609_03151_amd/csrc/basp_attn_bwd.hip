@@ -10,16 +10,14 @@
 //   dQ_i  = scale sum_{j<=i} dS_ij k_j
 // Kernels, all deterministic (no atomics):
 //   bwd_pre    per (sequence, head, row): the pair (LSE in log2 units, D)
-//   bwd_kv     key-stationary, twice (dV, then dK): a workgroup owns 256
-//              keys of one kv head and sweeps the query rows at or after
-//              them (one row chunk of them), for every query head of the
-//              GQA group, accumulating in registers
+//   bwd_kv     key-stationary, dV and dK together: a workgroup owns 128 keys
+//              of one kv head and sweeps the query rows at or after them (one
+//              row chunk of them), for every query head of the GQA group,
+//              accumulating in registers
 //   bwd_reduce sums the row-chunk partials of dK and dV in chunk order
 //   bwd_dq     query-stationary: like the forward, a workgroup owns 256
 //              rows of one query head and sweeps the keys up to the diagonal
-// gfx950 mapping shared by bwd_kv and bwd_dq
-//   * 8 waves per workgroup, one workgroup per CU (two waves per SIMD); each
-//     wave owns 32 keys (bwd_kv) or 32 rows (bwd_dq).
+// gfx950 mapping
 //   * v_mfma_f32_32x32x16_bf16 with fp32 accumulation.  The operand order
 //     puts every elementwise step (P, dS) in the accumulator layout and feeds
 //     it to the next product without a round trip through LDS.  Operands read
@@ -30,9 +28,11 @@
 //     copied HBM -> LDS by buffer loads that write LDS directly (rows past S
 //     arrive as zeros) into a ring of four stages, two steps ahead; each wave
 //     waits only for its own copies and passes a fence-free barrier.
-//   * each wave raises its issue priority over the accumulating products
-//     (dV, dK, dQ), so the two waves of a SIMD drift apart and one's
-//     elementwise work overlaps the other's MFMAs.
+//   * bwd_kv runs one wave per SIMD (4 waves, 32 keys each) and weaves its
+//     elementwise work between its own products; bwd_dq runs two waves per
+//     SIMD (8 waves, 32 rows each), which raise their issue priority over
+//     the accumulating products so that one wave's elementwise work overlaps
+//     the other's MFMAs.
 //   * Q, K, V, O, dO and the gradients are addressed through row views:
 //     the local head-sharded tensors, or (SH) the G sequence shards of the
 //     exchange in place (row counts multiples of 256: a workgroup's rows or
@@ -77,7 +77,7 @@ __device__ __forceinline__ void sched_reads_ahead() {
 // starting at their chunk's first row ("full") come first, chunk by chunk;
 // then the diagonal units (key tile inside its first chunk), longest first,
 // so the shortest work runs last.
-constexpr int kKvKeys = 256;       // keys per key-stationary workgroup
+constexpr int kKvKeys = 128;       // keys per key-stationary workgroup
 constexpr int kChunkRows = 2048;   // multiple of kKvKeys
 constexpr int kTilesPerChunk = kChunkRows / kKvKeys;
 
@@ -142,20 +142,32 @@ __global__ __launch_bounds__(kPreThreads) void bwd_pre_kernel(
   }
 }
 
-// ------------------------------------------------------ bwd_kv (dV / dK)
-// Key-stationary.  A workgroup of 8 waves owns 256 keys of one kv head (32
-// per wave) and sweeps 64-row query steps, for all query heads of the GQA
-// group.  Two instances of one kernel:
-//   kDV: S^T = K Q^T, P = exp2(S c - LSE2),   dV^T += dO^T P
-//   kDK: S^T, dP^T = V dO^T, dS = P (dP - D),   dK^T += Q^T dS
-// Keeping dV and dK in separate launches recomputes S once more, but keeps
-// each wave within two waves per SIMD of registers.
-constexpr int kKvWaves = 8;
+// ------------------------------------------------------ bwd_kv (dV and dK)
+// Key-stationary, dV and dK in one pass.  A workgroup of 4 waves (one per
+// SIMD) owns 128 keys of one kv head, 32 per wave, and sweeps 64-row query
+// steps for all query heads of the GQA group.  Per 32-row half a wave forms
+//   S^T = K Q^T and dP^T = V dO^T              (K, V of its keys in registers)
+//   P = exp2(S c - LSE2),  dS = P (dP - D)
+//   dV^T += dO^T P  and  dK^T += Q^T dS         (accumulated in registers)
+// so S is formed once for both gradients.  With one wave per SIMD the wave
+// has the register file to itself (K, V, dV, dK and two halves in flight),
+// and its own instruction stream overlaps elementwise work with products:
+// the exponentials of one half are interleaved with the products of the
+// other.
+constexpr int kKvWaves = 4;
 constexpr int kKvThreads = 64 * kKvWaves;
 constexpr int kKN = 32 * kKvWaves;  // keys per workgroup
-static_assert(kKN == kKvKeys, "work units assume 256 keys per workgroup");
+static_assert(kKN == kKvKeys, "work units assume 128 keys per workgroup");
 constexpr int kQM = 64;             // query rows per step (two 32-row halves)
-enum KvGrad { kDV = 0, kDK = 1 };
+
+// acc += A B with the accumulator held in AGPRs (issued as inline asm: the
+// compiler's own MFMA form moves a loop-carried accumulator between AGPRs and
+// VGPRs on every iteration once the VGPRs run out).  A and B are VGPRs whose
+// producers (LDS reads, waited on by the compiler, or VALU conversions issued
+// well before) are at least two wait states back.
+__device__ __forceinline__ void mfma_acc(f32x16 &acc, bf16x8 a, bf16x8 b) {
+  asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
+}
 
 template <int D>
 struct KvCfg {
@@ -170,14 +182,15 @@ struct KvCfg {
   static constexpr int DMA_PER_WAVE = kQM * CPR / kKvThreads;  // 1 KB copies per tile
 };
 
-// `outv` is the final dK/dV when there is one row chunk, else the partial
-// buffer of chunk 0 (a local view), chunk ch being ch * chunk_elems further.
-template <int D, int G, bool SH>
+// `dvv` / `dkv` are the final dV / dK when there is one row chunk, else the
+// partial buffers of chunk 0 (local views), chunk ch being ch * chunk_elems
+// further.
+template <int D, bool SH>
 __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
     const RowView qv, const RowView kv, const RowView vv, const RowView dov,
-    const f32x2 *__restrict__ ld, const RowView outv, size_t chunk_elems, int S, int Hl,
-    int Hkl, int n_rep, int kvheads_total, int ktiles, int nchunks, float c /* scale*log2e */,
-    float out_scale) {
+    const f32x2 *__restrict__ ld, const RowView dvv, const RowView dkv, size_t chunk_elems, int S,
+    int Hl, int Hkl, int n_rep, int kvheads_total, int ktiles, int nchunks,
+    float c /* scale*log2e */, float dk_scale) {
   using C = KvCfg<D>;
   using T = LdsTile<C::LW>;
   __shared__ __attribute__((aligned(16))) unsigned char smem[kStages * C::STAGE_BYTES];
@@ -209,34 +222,31 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
   const int key = wk0 + l32;
 
   const uint32_t q_row_bytes = qv.row_elems * 2, kv_row_bytes = kv.row_elems * 2;
-  // K (and V for dK) of this lane's key as B operands (B[e][j] = K[j][e]).
-  bf16x8 kf[C::NS], vf[G == kDK ? C::NS : 1];
+  // K and V of this lane's key as B operands (B[e][j] = K[j][e], V[j][e]).
+  bf16x8 kf[C::NS], vf[C::NS];
   {
     uint32_t left;
     const rsrc_t rk = make_rsrc(view_row<SH, const uint16_t>(kv, beta, k0, kvh, D, left),
                                 left * kv_row_bytes);
+    const rsrc_t rv = make_rsrc(view_row<SH, const uint16_t>(vv, beta, k0, kvh, D, left),
+                                left * kv_row_bytes);
 #pragma unroll
-    for (int s = 0; s < C::NS; ++s)
-      kf[s] = 2 * s < D / 8 ? as_bf16x8(buf_load16(rk, (uint32_t)(key - k0) * kv_row_bytes +
-                                                           (2 * s + hh) * 16))
-                            : bf16x8{};  // columns past D
-    if constexpr (G == kDK) {
-      const rsrc_t rv = make_rsrc(view_row<SH, const uint16_t>(vv, beta, k0, kvh, D, left),
-                                  left * kv_row_bytes);
-#pragma unroll
-      for (int s = 0; s < C::NS; ++s)
-        vf[s] = 2 * s < D / 8 ? as_bf16x8(buf_load16(rv, (uint32_t)(key - k0) * kv_row_bytes +
-                                                             (2 * s + hh) * 16))
-                              : bf16x8{};
+    for (int s = 0; s < C::NS; ++s) {
+      const uint32_t off = (uint32_t)(key - k0) * kv_row_bytes + (2 * s + hh) * 16;
+      kf[s] = 2 * s < D / 8 ? as_bf16x8(buf_load16(rk, off)) : bf16x8{};  // columns past D
+      vf[s] = 2 * s < D / 8 ? as_bf16x8(buf_load16(rv, off)) : bf16x8{};
     }
   }
   wait_vmcnt<0>();  // retire the tracked loads before untracked copies start
 
-  f32x16 acc[C::NE];
+  f32x16 accv[C::NE], acck[C::NE];
 #pragma unroll
   for (int n = 0; n < C::NE; ++n)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) acc[n][r] = 0.f;
+    for (int r = 0; r < 16; ++r) {
+      accv[n][r] = 0.f;
+      acck[n][r] = 0.f;
+    }
 
   const int steps_per_head = (r_hi - r_lo + kQM - 1) / kQM;
   const int nsteps = steps_per_head * n_rep;
@@ -263,6 +273,12 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
       asm volatile("" : "+v"(t_off[n][x]));
     }
 
+  // Within each head, the first nmask_ph row steps overlap some wave's keys
+  // and take the masked path; the rest need no mask in any wave.  The two
+  // kinds run in separate inner loops, so that each keeps one set of
+  // accumulator registers.
+  const int dmask = k0 + kKN - 1 - r_lo;
+  const int nmask_ph = dmask > 0 ? min(steps_per_head, (dmask + kQM - 1) / kQM) : 0;
   auto step_coords = [&](int st, int &h, int &i0) __attribute__((always_inline)) {
     const int hr = st / steps_per_head;
     h = kvh * n_rep + hr;
@@ -278,13 +294,12 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
                                      left * q_row_bytes);
     const u32x4 rd = make_rsrc_words(view_row<SH, const uint16_t>(dov, beta, i0, h, D, left),
                                      left * q_row_bytes);
-    const uint32_t base = 0;
     const uint32_t stage = smem_lds + (st % kStages) * C::STAGE_BYTES;
 #pragma unroll
     for (int i = 0; i < C::DMA_PER_WAVE; ++i) {
       const uint32_t lds = stage + (w * C::DMA_PER_WAVE + i) * 1024;
-      buf_load16_lds_async(rq, base + g_off[i], lds);
-      buf_load16_lds_async(rd, base + g_off[i], lds + C::TILE_BYTES);
+      buf_load16_lds_async(rq, g_off[i], lds);
+      buf_load16_lds_async(rd, g_off[i], lds + C::TILE_BYTES);
     }
     if (w == 0) {
       const u32x4 ra = make_rsrc_words(ld + ((size_t)beta * Hl + h) * S, (uint32_t)S * 8);
@@ -305,126 +320,208 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
     }
   };
 
-  // One 64-row step.  MASK: some row of the step precedes one of this wave's
-  // keys (P = 0 there; 32-row halves entirely before the keys are skipped).
-  auto body = [&](int st, int i0, bool MASK) __attribute__((always_inline)) {
-    const unsigned char *Qs = smem + (st % kStages) * C::STAGE_BYTES;
+  // ---- the pieces of a step (half m of the stage at Qs)
+  // S^T and dP^T of half m: 2 NS products, each with one 16-byte LDS read.
+  auto scores = [&](const unsigned char *Qs, int m, f32x16 &sacc, f32x16 &pacc)
+      __attribute__((always_inline)) {
     const unsigned char *dOs = Qs + C::TILE_BYTES;
-    const float *aux = reinterpret_cast<const float *>(dOs + C::TILE_BYTES);
-    const unsigned char *Ts = G == kDV ? dOs : Qs;  // transposed operand of the accumulation
 #pragma unroll
-    for (int m = 0; m < 2; ++m) {
-      if (MASK && i0 + 32 * m + 31 < wk0) continue;  // wave-uniform
-      // sacc[r]: row i0 + 32m + 8(r/4) + 4hh + r%4, key `key`.
-      f32x16 sacc, pacc;
-      {
-        const bf16x8 aq = *reinterpret_cast<const bf16x8 *>(Qs + a_off[0] + m * 32 * T::ROW_BYTES);
-        sacc = mfma32x32x16(aq, kf[0], f32x16{});
-        if constexpr (G == kDK) {
-          const bf16x8 ad = *reinterpret_cast<const bf16x8 *>(dOs + a_off[0] + m * 32 * T::ROW_BYTES);
-          pacc = mfma32x32x16(ad, vf[0], f32x16{});
+    for (int s = 0; s < C::NS; ++s) {
+      const bf16x8 aq = *reinterpret_cast<const bf16x8 *>(Qs + a_off[s] + m * 32 * T::ROW_BYTES);
+      const bf16x8 ad = *reinterpret_cast<const bf16x8 *>(dOs + a_off[s] + m * 32 * T::ROW_BYTES);
+      sacc = mfma32x32x16(aq, kf[s], s == 0 ? f32x16{} : sacc);
+      pacc = mfma32x32x16(ad, vf[s], s == 0 ? f32x16{} : pacc);
+    }
+  };
+  // P and dS of half m as bf16 B operands along the rows: block s2 covers rows
+  // 32m + 16*s2 .. +15, slot t <-> register 8*s2 + t.  Row 32m + 8g + 4hh + x
+  // of the step holds (LSE2, D) at aux[2 * row].  lim: rows of the half whose
+  // offset is below lim precede the key (masked); 0 for none.
+  auto elementwise = [&](const unsigned char *Qs, int m, f32x16 &sacc, const f32x16 &pacc,
+                         int lim, bf16x8 *bp, bf16x8 *bds) __attribute__((always_inline)) {
+    const float *aux = reinterpret_cast<const float *>(Qs + 2 * C::TILE_BYTES);
+    float ds[16];
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const int rr = 32 * m + 8 * g + 4 * hh;
+#pragma unroll
+      for (int x2 = 0; x2 < 2; ++x2) {
+        const f32x4 a = *reinterpret_cast<const f32x4 *>(aux + 2 * rr + 4 * x2);
+#pragma unroll
+        for (int y = 0; y < 2; ++y) {
+          const int r = 4 * g + 2 * x2 + y;
+          float p = fast_exp2(fmaf(sacc[r], c, -a[2 * y]));
+          if (8 * (r >> 2) + (r & 3) < lim) p = 0.f;
+          sacc[r] = p;
+          ds[r] = p * (pacc[r] - a[2 * y + 1]);
         }
       }
+    }
 #pragma unroll
-      for (int s = 1; s < C::NS; ++s) {
-        const bf16x8 aq = *reinterpret_cast<const bf16x8 *>(Qs + a_off[s] + m * 32 * T::ROW_BYTES);
-        sacc = mfma32x32x16(aq, kf[s], sacc);
-        if constexpr (G == kDK) {
-          const bf16x8 ad = *reinterpret_cast<const bf16x8 *>(dOs + a_off[s] + m * 32 * T::ROW_BYTES);
-          pacc = mfma32x32x16(ad, vf[s], pacc);
-        }
-      }
-      sched_reads_ahead<(G == kDK ? 2 : 1) * C::NS, 1, (G == kDK ? 4 : 2)>();
-      // Row 32m + 8g + 4hh + x of the step holds (LSE2, D) at aux[2 * row].
+    for (int s2 = 0; s2 < 2; ++s2) {
+      const int b8 = 8 * s2;
+      bp[s2] = as_bf16x8(u32x4{pack_bf16x2(sacc[b8 + 0], sacc[b8 + 1]),
+                               pack_bf16x2(sacc[b8 + 2], sacc[b8 + 3]),
+                               pack_bf16x2(sacc[b8 + 4], sacc[b8 + 5]),
+                               pack_bf16x2(sacc[b8 + 6], sacc[b8 + 7])});
+      bds[s2] = as_bf16x8(u32x4{pack_bf16x2(ds[b8 + 0], ds[b8 + 1]), pack_bf16x2(ds[b8 + 2], ds[b8 + 3]),
+                                pack_bf16x2(ds[b8 + 4], ds[b8 + 5]), pack_bf16x2(ds[b8 + 6], ds[b8 + 7])});
+    }
+  };
+  // dV^T += dO^T P and dK^T += Q^T dS over half m: 4 NE products, each with
+  // two transposed LDS reads.
+  auto accumulate = [&](const unsigned char *Qs, int m, const bf16x8 *bp, const bf16x8 *bds)
+      __attribute__((always_inline)) {
+    const unsigned char *dOs = Qs + C::TILE_BYTES;
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int rr = 32 * m + 8 * g + 4 * hh;
-#pragma unroll
-        for (int x2 = 0; x2 < 2; ++x2) {
-          const f32x4 a = *reinterpret_cast<const f32x4 *>(aux + 2 * rr + 4 * x2);
-#pragma unroll
-          for (int y = 0; y < 2; ++y) {
-            const int r = 4 * g + 2 * x2 + y;
-            sacc[r] = fast_exp2(fmaf(sacc[r], c, -a[2 * y]));
-          }
-        }
-      }
-      if (MASK) {  // wave-uniform; a real branch, taken on diagonal steps only
-        asm volatile("" ::: "memory");
-        const int lim = key - i0 - 32 * m - 4 * hh;  // row offset in the half must be >= lim
-#pragma unroll
-        for (int r = 0; r < 16; ++r)
-          if (8 * (r >> 2) + (r & 3) < lim) sacc[r] = 0.f;
-      }
-      if constexpr (G == kDK) {
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const int rr = 32 * m + 8 * g + 4 * hh;
-#pragma unroll
-          for (int x2 = 0; x2 < 2; ++x2) {
-            const f32x4 a = *reinterpret_cast<const f32x4 *>(aux + 2 * rr + 4 * x2);
-#pragma unroll
-            for (int y = 0; y < 2; ++y) {
-              const int r = 4 * g + 2 * x2 + y;
-              sacc[r] *= pacc[r] - a[2 * y + 1];
-            }
-          }
-        }
-      }
-      // P or dS as the B operand along the rows: block s2 covers rows
-      // 32m + 16*s2 .. +15, slot t <-> register 8*s2 + t.
-      bf16x8 b[2];
+    for (int n = 0; n < C::NE; ++n)
 #pragma unroll
       for (int s2 = 0; s2 < 2; ++s2) {
-        const int b8 = 8 * s2;
-        u32x4 t4 = {pack_bf16x2(sacc[b8 + 0], sacc[b8 + 1]), pack_bf16x2(sacc[b8 + 2], sacc[b8 + 3]),
-                    pack_bf16x2(sacc[b8 + 4], sacc[b8 + 5]), pack_bf16x2(sacc[b8 + 6], sacc[b8 + 7])};
-        b[s2] = as_bf16x8(t4);
+        const int ro = (2 * m + s2) * 16 * T::ROW_BYTES;
+        const bf16x8 av = tr_operand(dOs, t_off[n][0] + ro, t_off[n][1] + ro);
+        mfma_acc(accv[n], av, bp[s2]);
+        const bf16x8 ak = tr_operand(Qs, t_off[n][0] + ro, t_off[n][1] + ro);
+        mfma_acc(acck[n], ak, bds[s2]);
       }
-      // dV^T += dO^T P  or  dK^T += Q^T dS: M = head dim, N = keys, K = rows.
-      // Raised priority: these products run ahead of the partner wave's
-      // elementwise work.
-      wave_priority<1>();
+  };
+  // One step clear of the diagonal as 4 blocks of 4 NE products (2 NS = 4 NE
+  // for every head dim taken), issued one product per slot:
+  //   A: S^T, dP^T of half 0       B: S^T, dP^T of half 1 + elementwise(0)
+  //   C: accumulate(0) + elementwise(1)                D: accumulate(1)
+  // Each slot reads the operand kPf products ahead and does its share of the
+  // elementwise work; scheduling barriers keep the slots in this order.  The
+  // elementwise work of a half starts kLag slots into its block, after the
+  // products it reads have finished.
+  constexpr int kPf = 3, kLag = 2;
+  auto unmasked_step = [&](const unsigned char *Qs) __attribute__((always_inline)) {
+    constexpr int NB = 4 * C::NE;  // products per block
+    static_assert(2 * C::NS == NB, "score and accumulate blocks have equal length");
+    constexpr int NG = 4 * NB;
+    const unsigned char *dOs = Qs + C::TILE_BYTES;
+    const float *aux = reinterpret_cast<const float *>(Qs + 2 * C::TILE_BYTES);
+    bf16x8 opnd[NG];
+    auto load_opnd = [&](int g) __attribute__((always_inline)) {
+      const int blk = g / NB, j = g % NB;
+      if (blk < 2) {  // row operand of S^T (Q) or dP^T (dO), half blk, chunk pair j/2
+        opnd[g] = *reinterpret_cast<const bf16x8 *>(((j & 1) ? dOs : Qs) + a_off[j / 2] +
+                                                      blk * 32 * T::ROW_BYTES);
+      } else {  // transposed dO (for dV) or Q (for dK), half blk-2
+        const int n = j / 4, s2 = (j / 2) % 2;
+        const int ro = (2 * (blk - 2) + s2) * 16 * T::ROW_BYTES;
+        opnd[g] = tr_operand((j & 1) ? Qs : dOs, t_off[n][0] + ro, t_off[n][1] + ro);
+      }
+    };
+    f32x16 sc[2], pc[2];      // S^T and dP^T of each half
+    bf16x8 bp[2][2], bds[2][2];
+    float pv[16], dv[16];
+    f32x4 ax[8];
+    auto load_aux = [&](int me) __attribute__((always_inline)) {
 #pragma unroll
-      for (int n = 0; n < C::NE; ++n)
+      for (int q = 0; q < 8; ++q)
+        ax[q] = *reinterpret_cast<const f32x4 *>(
+            aux + 2 * (32 * me + 8 * (q >> 1) + 4 * hh) + 4 * (q & 1));
+    };
+    auto element = [&](int me, int r) __attribute__((always_inline)) {
+      const f32x4 a = ax[r / 2];
+      const int y = r & 1;
+      const float pr = fast_exp2(fmaf(sc[me][r], c, -a[2 * y]));
+      pv[r] = pr;
+      dv[r] = pr * (pc[me][r] - a[2 * y + 1]);
+      if (r & 1) {  // registers r-1, r -> dword (r % 8) / 2 of block r / 8
+        const int b = r / 8, dw = (r % 8) / 2;
+        reinterpret_cast<uint32_t *>(&bp[me][b])[dw] = pack_bf16x2(pv[r - 1], pv[r]);
+        reinterpret_cast<uint32_t *>(&bds[me][b])[dw] = pack_bf16x2(dv[r - 1], dv[r]);
+      }
+    };
 #pragma unroll
-        for (int s2 = 0; s2 < 2; ++s2) {
-          const int ro = (2 * m + s2) * 16 * T::ROW_BYTES;
-          const bf16x8 a = tr_operand(Ts, t_off[n][0] + ro, t_off[n][1] + ro);
-          acc[n] = mfma32x32x16(a, b[s2], acc[n]);
+    for (int g = 0; g < kPf; ++g) load_opnd(g);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int g = 0; g < NG; ++g) {
+      const int blk = g / NB, j = g % NB;
+      if (g + kPf < NG) load_opnd(g + kPf);
+      if (blk < 2) {
+        const int s = j / 2;
+        if (j & 1) pc[blk] = mfma32x32x16(opnd[g], vf[s], s == 0 ? f32x16{} : pc[blk]);
+        else sc[blk] = mfma32x32x16(opnd[g], kf[s], s == 0 ? f32x16{} : sc[blk]);
+      } else {
+        const int n = j / 4, s2 = (j / 2) % 2, mh = blk - 2;
+        if (j & 1) mfma_acc(acck[n], opnd[g], bds[mh][s2]);
+        else mfma_acc(accv[n], opnd[g], bp[mh][s2]);
+      }
+      if (blk == 1 || blk == 2) {  // elementwise of half blk-1
+        const int me = blk - 1;
+        if (j == 0) load_aux(me);
+        if (j >= kLag) {
+#pragma unroll
+          for (int r = (j - kLag) * 16 / (NB - kLag); r < (j - kLag + 1) * 16 / (NB - kLag); ++r)
+            element(me, r);
         }
-      sched_reads_ahead<2 * C::NE, 2, 4>();
-      __builtin_amdgcn_sched_barrier(0);  // keep the two halves apart (register pressure)
-      wave_priority<0>();
+      }
+      __builtin_amdgcn_sched_barrier(0);
     }
   };
 
   for (int st = 0; st < 2 && st < nsteps; ++st) load_step(st);
-  for (int st = 0; st < nsteps; ++st) {
-    // Stage (st+2) % 4 last held step st-2, finished by every wave before
-    // the barrier of step st-1.
+  // Stage (st+2) % 4 last held step st-2, finished by every wave before the
+  // barrier of step st-1.
+  auto begin_step = [&](int st) __attribute__((always_inline)) {
     if (st + 2 < nsteps) load_step(st + 2);
     wait_step(min(2, nsteps - 1 - st));
     barrier_no_fence();
-    int h_unused, i0;
-    step_coords(st, h_unused, i0);
-    if (i0 + kQM - 1 < wk0) continue;          // wave-uniform: all rows before the keys
-    body(st, i0, i0 < wk0 + 31);  // mask when rows and keys overlap
+  };
+  int st = 0;
+  for (int hr = 0; hr < n_rep; ++hr) {
+    for (int t = 0; t < nmask_ph; ++t, ++st) {
+      begin_step(st);
+      const int i0 = r_lo + t * kQM;
+      const unsigned char *Qs = smem + (st % kStages) * C::STAGE_BYTES;
+      // Halves in turn, masked; halves entirely before the keys skipped
+      // (wave-uniform).
+#pragma unroll
+      for (int m = 0; m < 2; ++m) {
+        if (i0 + 32 * m + 31 < wk0) continue;
+        f32x16 sacc, pacc;
+        bf16x8 bp[2], bds[2];
+        scores(Qs, m, sacc, pacc);
+        sched_reads_ahead<2 * C::NS, 1, 4>();
+        __builtin_amdgcn_sched_barrier(0);
+        elementwise(Qs, m, sacc, pacc, key - i0 - 32 * m - 4 * hh, bp, bds);
+        __builtin_amdgcn_sched_barrier(0);
+        asm volatile("s_nop 1");
+        accumulate(Qs, m, bp, bds);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+    // The accumulators may be moved between the loops: cover the latency of
+    // the last products before anything reads them.
+    asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
+    for (int t = nmask_ph; t < steps_per_head; ++t, ++st) {
+      begin_step(st);
+      unmasked_step(smem + (st % kStages) * C::STAGE_BYTES);
+    }
+    asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
   }
 
+  // The last products' results are read below: cover their latency.
+  asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
   // acc[n][r] = (dV or dK)^T[e = 32n + 8(r/4) + 4hh + r%4][key]
   if (key < S) {
     uint32_t left;
-    float *o = view_row<true, float>(outv, beta, k0, kvh, D, left) + (size_t)ch * chunk_elems +
-               (size_t)(key - k0) * outv.row_elems;
+    float *ov = view_row<true, float>(dvv, beta, k0, kvh, D, left) + (size_t)ch * chunk_elems +
+                (size_t)(key - k0) * dvv.row_elems;
+    float *ok = view_row<true, float>(dkv, beta, k0, kvh, D, left) + (size_t)ch * chunk_elems +
+                (size_t)(key - k0) * dkv.row_elems;
 #pragma unroll
     for (int n = 0; n < C::NE; ++n)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         if (32 * n + 8 * g >= D) continue;  // padding columns
-        f32x4 a = {acc[n][4 * g] * out_scale, acc[n][4 * g + 1] * out_scale,
-                   acc[n][4 * g + 2] * out_scale, acc[n][4 * g + 3] * out_scale};
-        *reinterpret_cast<f32x4 *>(o + 32 * n + 8 * g + 4 * hh) = a;
+        *reinterpret_cast<f32x4 *>(ov + 32 * n + 8 * g + 4 * hh) =
+            f32x4{accv[n][4 * g], accv[n][4 * g + 1], accv[n][4 * g + 2], accv[n][4 * g + 3]};
+        *reinterpret_cast<f32x4 *>(ok + 32 * n + 8 * g + 4 * hh) =
+            f32x4{acck[n][4 * g] * dk_scale, acck[n][4 * g + 1] * dk_scale,
+                  acck[n][4 * g + 2] * dk_scale, acck[n][4 * g + 3] * dk_scale};
       }
   }
 }
@@ -708,12 +805,9 @@ hipError_t launch_bwd_d(const RowView &q, const RowView &k, const RowView &v, co
     dv_out = local_view(dv_part, s.S, s.Hkl, D);
     dk_out = local_view(dk_part, s.S, s.Hkl, D);
   }
-  hipLaunchKernelGGL((bwd_kv_kernel<D, kDV, SH>), kv_grid, dim3(kKvThreads), 0, stream, q, k, v,
-                     d_o, ld, dv_out, chunk_elems, s.S, s.Hl, s.Hkl, n_rep, kvheads_total, ktiles,
-                     ck.n, c, 1.f);
-  hipLaunchKernelGGL((bwd_kv_kernel<D, kDK, SH>), kv_grid, dim3(kKvThreads), 0, stream, q, k, v,
-                     d_o, ld, dk_out, chunk_elems, s.S, s.Hl, s.Hkl, n_rep, kvheads_total, ktiles,
-                     ck.n, c, s.scale);
+  hipLaunchKernelGGL((bwd_kv_kernel<D, SH>), kv_grid, dim3(kKvThreads), 0, stream, q, k, v, d_o,
+                     ld, dv_out, dk_out, chunk_elems, s.S, s.Hl, s.Hkl, n_rep, kvheads_total,
+                     ktiles, ck.n, c, s.scale);
   if (ck.n > 1) {
     const uint32_t row_quads = (uint32_t)(s.Hkl * D / 4);
     const uint32_t seq_quads = (uint32_t)s.S * row_quads;
