@@ -70,16 +70,10 @@ __device__ __forceinline__ void sched_reads_ahead() {
 // Workspace: LD [b][Hl][S] of (LSE * log2(e), D), then, when the key
 // passes are chunked, the dV and dK partial sums [chunk][b][S][H_kv/G][d].
 //
-// Work units of the key-stationary passes.  The rows a key tile needs,
-// [k0, S), are cut at multiples of kChunkRows; a unit is one (key tile, row
-// chunk) pair and writes its own partial sum (slice `chunk` of the partial
-// buffer), so no unit holds more than kChunkRows rows per query head.  Units
-// starting at their chunk's first row ("full") come first, chunk by chunk;
-// then the diagonal units (key tile inside its first chunk), longest first,
-// so the shortest work runs last.
-constexpr int kKvKeys = 128;       // keys per key-stationary workgroup
-constexpr int kChunkRows = 2048;   // multiple of kKvKeys
-constexpr int kTilesPerChunk = kChunkRows / kKvKeys;
+// Work units of the key-stationary pass: see kv_unit.  kChunkRows is the
+// chunk of rows per unit, kTilesPerChunk the key tiles in one chunk.
+constexpr int kChunkRows = kKvChunkRows;
+constexpr int kTilesPerChunk = kKvTilesPerChunk;
 
 struct BwdChunks {
   int n;      // row chunks
@@ -91,7 +85,7 @@ BwdChunks bwd_chunks(const AttnShape &s) {
   BwdChunks ck;
   ck.n = (s.S + kChunkRows - 1) / kChunkRows;
   if (ck.n < 1) ck.n = 1;
-  ck.units = kTilesPerChunk * ck.n * (ck.n - 1) / 2 + ck.n + ck.n * (kTilesPerChunk - 1);
+  ck.units = kv_units(ck.n);
   const size_t ld_floats = 2 * (size_t)s.b * s.Hl * s.S;
   ck.part_offset_floats = (ld_floats + 63) & ~(size_t)63;  // 256-byte aligned
   return ck;
@@ -199,20 +193,11 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int l32 = lane & 31, hh = lane >> 5;
   // Work unit (key tile kt, row chunk ch) of sequence x kv head hb; the
-  // order of units is described with kChunkRows.
+  // order of units is described with kv_unit.
   const int L = blockIdx.x;
   const int hb = L % kvheads_total;
-  int u = L / kvheads_total, ch = 0, kt;
-  while (ch < nchunks && u >= ch * kTilesPerChunk + 1) {  // full units of chunk ch
-    u -= ch * kTilesPerChunk + 1;
-    ++ch;
-  }
-  if (ch < nchunks) {
-    kt = u;
-  } else {  // diagonal units, j-th key tile of its chunk
-    ch = u % nchunks;
-    kt = ch * kTilesPerChunk + u / nchunks + 1;
-  }
+  int kt, ch;
+  kv_unit(L / kvheads_total, nchunks, kt, ch);
   if (kt >= ktiles) return;  // workgroup-uniform
   const int beta = hb / Hkl, kvh = hb % Hkl;
   const int k0 = kt * kKN;
@@ -277,8 +262,7 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
   // and take the masked path; the rest need no mask in any wave.  The two
   // kinds run in separate inner loops, so that each keeps one set of
   // accumulator registers.
-  const int dmask = k0 + kKN - 1 - r_lo;
-  const int nmask_ph = dmask > 0 ? min(steps_per_head, (dmask + kQM - 1) / kQM) : 0;
+  const int nmask_ph = kv_masked_steps(k0, r_lo, steps_per_head, kQM);
   auto step_coords = [&](int st, int &h, int &i0) __attribute__((always_inline)) {
     const int hr = st / steps_per_head;
     h = kvh * n_rep + hr;

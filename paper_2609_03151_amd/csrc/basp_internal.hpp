@@ -33,6 +33,49 @@ struct FastDiv {
   }
 };
 
+// Work schedule of the key-stationary backward pass (dV and dK).  A key
+// tile is kKvKeys keys; the rows it needs, [k0, S), are cut at multiples of
+// kKvChunkRows, and a unit is one (key tile kt, row chunk ch) pair that
+// writes its own partial sum.  Per (sequence, kv head) there are kv_units(n)
+// units for n row chunks: first the units that start at their chunk's first
+// row ("full"), chunk by chunk (chunk ch has tiles 0 .. ch*T of them, T =
+// tiles per chunk); then the diagonal units (key tile inside its first chunk
+// but not at its start), longest first (exactly so when S fills whole
+// chunks; a partial last chunk's are shorter).  Units whose tile lies past S, or
+// whose rows are empty, do nothing.  Host-callable for checking.
+constexpr int kKvKeys = 128;
+constexpr int kKvChunkRows = 2048;
+constexpr int kKvTilesPerChunk = kKvChunkRows / kKvKeys;
+
+__host__ __device__ inline int kv_units(int nchunks) {
+  const int T = kKvTilesPerChunk;
+  return T * nchunks * (nchunks - 1) / 2 + nchunks + nchunks * (T - 1);
+}
+__host__ __device__ inline void kv_unit(int u, int nchunks, int &kt, int &ch) {
+  const int T = kKvTilesPerChunk;
+  ch = 0;
+  while (ch < nchunks && u >= ch * T + 1) {  // full units of chunk ch
+    u -= ch * T + 1;
+    ++ch;
+  }
+  if (ch < nchunks) {
+    kt = u;
+  } else {  // diagonal units, j-th key tile of its chunk
+    ch = u % nchunks;
+    kt = ch * T + u / nchunks + 1;
+  }
+}
+// Row steps of `step_rows` at the start of a unit's rows r_lo.. that overlap
+// some key of its tile [k0, k0 + kKvKeys) in a wave's 32-key block: the
+// masked steps, at most ceil((k0 + kKvKeys - 1 - r_lo) / step_rows).  Every
+// later step starts at or after k0 + kKvKeys - 1.
+__host__ __device__ inline int kv_masked_steps(int k0, int r_lo, int steps, int step_rows) {
+  const int dm = k0 + kKvKeys - 1 - r_lo;
+  if (dm <= 0) return 0;
+  const int n = (dm + step_rows - 1) / step_rows;
+  return n < steps ? n : steps;
+}
+
 // How the attention kernels find one tensor of the share.  Row r (a token
 // of the full sequence) of sequence beta lies in buffer p[r / rows], at row
 // r % rows of that buffer; a row holds row_elems elements, among them the
