@@ -58,6 +58,8 @@ SMALL = [  # b, S, Hl, Hkl, d
     (1, 1000, 4, 1, 96),     # d = 96, ragged tail
     (2, 300, 3, 3, 80),      # d = 80 (Table II: 2560 / 32), computed at 96, ragged
     (1, 2500, 2, 1, 80),     # d = 80, 2 chunks, ragged tail
+    (2, 2112, 4, 2, 128),    # 2 chunks, the second one 64-row step; GQA 2, b = 2
+    (1, 4160, 7, 1, 64),     # 3 chunks (4160 = 2*2048 + 64), GQA 7, d = 64
 ]
 
 
