@@ -8,7 +8,8 @@
   LSE = ln(i+1), run-to-run bitwise determinism;
 * full workload sizes, in the launch configuration the benchmark times:
   sampled rows of O, LSE, dQ, the last keys' dK and dV, and the invariants
-  sum_j dK_j = 0 and sum_j dV_j = sum of dO over the group's heads.
+  sum_j dK_j = 0 and sum_j dV_j = sum of dO over the group's heads; and, for
+  one kv head, every row and key against a plain fp64 torch computation.
 Bar: max |err| <= 2e-2 and mean |err| <= 2e-3 per tensor (LSE max 1e-3)."""
 import math
 
@@ -199,6 +200,63 @@ def test_attention_full_size_sampled(name):
     log(f"  sum dV vs sum dO: rel {rel:.2e}")
     assert rel < 1e-3
     del sh
+    torch.cuda.empty_cache()
+
+
+def _fp64_kv_head(ql, kl, vl, dl, n_rep, scale, block=2048):
+    """O, dQ of query heads 0 .. n_rep-1 and dK, dV of kv head 0 (sequence 0)
+    in plain fp64 torch on the GPU: per block of query rows, the dense masked
+    score block, its softmax, and the gradients of sum(O * dO) from the
+    definition (D = rowsum(dO * O), dS = P (dP - D))."""
+    S, d = ql.shape[1], ql.shape[3]
+    K, V = kl[0, :, 0].cuda().double(), vl[0, :, 0].cuda().double()
+    rO = torch.empty(S, n_rep, d, dtype=torch.float64, device="cuda")
+    rdQ = torch.empty_like(rO)
+    rdK = torch.zeros(S, d, dtype=torch.float64, device="cuda")
+    rdV = torch.zeros_like(rdK)
+    for h in range(n_rep):
+        Q, dO = ql[0, :, h].cuda().double(), dl[0, :, h].cuda().double()
+        for r0 in range(0, S, block):
+            r1 = min(S, r0 + block)
+            s = (Q[r0:r1] @ K[:r1].T) * scale
+            keys = torch.arange(r1, device="cuda")[None, :]
+            rows = torch.arange(r0, r1, device="cuda")[:, None]
+            s.masked_fill_(keys > rows, float("-inf"))
+            p = torch.softmax(s, dim=1)
+            del s
+            ob = p @ V[:r1]
+            rO[r0:r1, h] = ob
+            ds = p * (dO[r0:r1] @ V[:r1].T - (dO[r0:r1] * ob).sum(1, keepdim=True))
+            rdV[:r1] += p.T @ dO[r0:r1]
+            del p
+            rdQ[r0:r1, h] = scale * (ds @ K[:r1])
+            rdK[:r1] += scale * (ds.T @ Q[r0:r1])
+            del ds
+    return rO, rdQ, rdK, rdV
+
+
+@pytest.mark.parametrize("name", ["llama3_8b_s32k", "qwen25_7b_s64k", "llama3_70b_s128k"])
+def test_attention_full_size_kv_head_fp64(name):
+    """Every row and key of one kv head at full size (sequence 0, kv head 0 and
+    its query heads) against an independent fp64 computation in plain torch on
+    the GPU; the oracle's sampled rows and tails above pin the same outputs."""
+    w = WORKLOADS[name]
+    log(f"[attn full fp64] {name}")
+    q, k, v, do = workload_inputs(name)
+    sh = RankShare(device_shards(q, w), device_shards(k, w), device_shards(v, w),
+                   device_shards(do, w), G=w.G, rank=w.rank, scale=w.scale)
+    sh.step()
+    torch.cuda.synchronize()
+    ql, kl, vl, dl = (local_heads(x, w, n).contiguous()
+                      for x, n in ((q, w.H), (k, w.H_kv), (v, w.H_kv), (do, w.H)))
+    n_rep = w.Hl // w.Hkl
+    rO, rdQ, rdK, rdV = _fp64_kv_head(ql, kl, vl, dl, n_rep, w.scale)
+    torch.cuda.synchronize()
+    log("  fp64 reference done")
+    for nm, got, ref in (("O", sh.o[0, :, :n_rep], rO), ("dQ", sh.dq[0, :, :n_rep], rdQ),
+                         ("dK", sh.dk[0, :, 0], rdK), ("dV", sh.dv[0, :, 0], rdV)):
+        check_close(nm + " (fp64 torch)", got.double().cpu().numpy(), ref.cpu().numpy())
+    del sh, rO, rdQ, rdK, rdV
     torch.cuda.empty_cache()
 
 
