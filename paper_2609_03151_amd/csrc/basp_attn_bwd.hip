@@ -70,12 +70,10 @@ __device__ __forceinline__ void sched_reads_ahead() {
 // Workspace: LD [b][Hl][S] of (LSE * log2(e), D), then, when the key
 // passes are chunked, the dV and dK partial sums [chunk][b][S][H_kv/G][d].
 //
-// Work units of the key-stationary pass: see kv_unit.  kChunkRows is the
-// chunk of rows per unit, kTilesPerChunk the key tiles in one chunk.
-constexpr int kChunkRows = kKvChunkRows;
-constexpr int kTilesPerChunk = kKvTilesPerChunk;
-
+// Work units of the key-stationary pass: see kv_unit.
 struct BwdChunks {
+  int rows;   // rows per chunk (a multiple of kKvKeys)
+  int T;      // key tiles per chunk
   int n;      // row chunks
   int units;  // work units per (sequence, kv head)
   size_t part_offset_floats;
@@ -83,9 +81,11 @@ struct BwdChunks {
 
 BwdChunks bwd_chunks(const AttnShape &s) {
   BwdChunks ck;
-  ck.n = (s.S + kChunkRows - 1) / kChunkRows;
+  ck.rows = kv_chunk_rows(s.S);
+  ck.T = ck.rows / kKvKeys;
+  ck.n = (s.S + ck.rows - 1) / ck.rows;
   if (ck.n < 1) ck.n = 1;
-  ck.units = kv_units(ck.n);
+  ck.units = kv_units(ck.n, ck.T);
   const size_t ld_floats = 2 * (size_t)s.b * s.Hl * s.S;
   ck.part_offset_floats = (ld_floats + 63) & ~(size_t)63;  // 256-byte aligned
   return ck;
@@ -183,7 +183,7 @@ template <int D, bool SH>
 __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
     const RowView qv, const RowView kv, const RowView vv, const RowView dov,
     const f32x2 *__restrict__ ld, const RowView dvv, const RowView dkv, size_t chunk_elems, int S,
-    int Hl, int Hkl, int n_rep, int kvheads_total, int ktiles, int nchunks,
+    int Hl, int Hkl, int n_rep, int kvheads_total, int ktiles, int nchunks, int chunk_tiles,
     float c /* scale*log2e */, float dk_scale) {
   using C = KvCfg<D>;
   using T = LdsTile<C::LW>;
@@ -197,11 +197,12 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
   const int L = blockIdx.x;
   const int hb = L % kvheads_total;
   int kt, ch;
-  kv_unit(L / kvheads_total, nchunks, kt, ch);
+  kv_unit(L / kvheads_total, nchunks, chunk_tiles, kt, ch);
   if (kt >= ktiles) return;  // workgroup-uniform
   const int beta = hb / Hkl, kvh = hb % Hkl;
   const int k0 = kt * kKN;
-  const int r_lo = max(k0, ch * kChunkRows), r_hi = min(S, (ch + 1) * kChunkRows);
+  const int chunk_rows = chunk_tiles * kKvKeys;
+  const int r_lo = max(k0, ch * chunk_rows), r_hi = min(S, (ch + 1) * chunk_rows);
   if (r_lo >= r_hi) return;
   const int wk0 = k0 + 32 * w;
   const int key = wk0 + l32;
@@ -519,13 +520,13 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
 __global__ __launch_bounds__(kPreThreads) void bwd_reduce_kernel(
     const float *__restrict__ part, const RowView outv, uint32_t row_quads /* Hkl*D/4 */,
     FastDiv by_row_quads, uint32_t seq_quads /* S*row_quads */, size_t slice /* b*S*Hkl*D */,
-    int d, int nchunks) {
+    int d, int nchunks, int chunk_tiles) {
   const uint32_t i = blockIdx.x * kPreThreads + threadIdx.x;
   if (i >= seq_quads) return;
   const int beta = blockIdx.y;
   const uint32_t key = by_row_quads.div(i), cq = i - key * row_quads;
   const size_t e = ((size_t)beta * seq_quads + i) * 4;
-  const int first = (int)(key / kKN) / kTilesPerChunk;  // first chunk the key tile wrote
+  const int first = (int)(key / kKN) / chunk_tiles;  // first chunk the key tile wrote
   f32x4 acc = *reinterpret_cast<const f32x4 *>(part + (size_t)first * slice + e);
   for (int ch = first + 1; ch < nchunks; ++ch) {
     const f32x4 x = *reinterpret_cast<const f32x4 *>(part + (size_t)ch * slice + e);
@@ -791,16 +792,16 @@ hipError_t launch_bwd_d(const RowView &q, const RowView &k, const RowView &v, co
   }
   hipLaunchKernelGGL((bwd_kv_kernel<D, SH>), kv_grid, dim3(kKvThreads), 0, stream, q, k, v, d_o,
                      ld, dv_out, dk_out, chunk_elems, s.S, s.Hl, s.Hkl, n_rep, kvheads_total,
-                     ktiles, ck.n, c, s.scale);
+                     ktiles, ck.n, ck.T, c, s.scale);
   if (ck.n > 1) {
     const uint32_t row_quads = (uint32_t)(s.Hkl * D / 4);
     const uint32_t seq_quads = (uint32_t)s.S * row_quads;
     const dim3 rg((seq_quads + kPreThreads - 1) / kPreThreads, (unsigned)s.b);
     const FastDiv by_rq = FastDiv::make(row_quads);
     hipLaunchKernelGGL(bwd_reduce_kernel, rg, dim3(kPreThreads), 0, stream, dv_part, dv,
-                       row_quads, by_rq, seq_quads, chunk_elems, D, ck.n);
+                       row_quads, by_rq, seq_quads, chunk_elems, D, ck.n, ck.T);
     hipLaunchKernelGGL(bwd_reduce_kernel, rg, dim3(kPreThreads), 0, stream, dk_part, dk,
-                       row_quads, by_rq, seq_quads, chunk_elems, D, ck.n);
+                       row_quads, by_rq, seq_quads, chunk_elems, D, ck.n, ck.T);
   }
 
   const int qtiles = (s.S + kDQM - 1) / kDQM;

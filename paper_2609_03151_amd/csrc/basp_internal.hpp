@@ -35,24 +35,29 @@ struct FastDiv {
 
 // Work schedule of the key-stationary backward pass (dV and dK).  A key
 // tile is kKvKeys keys; the rows it needs, [k0, S), are cut at multiples of
-// kKvChunkRows, and a unit is one (key tile kt, row chunk ch) pair that
-// writes its own partial sum.  Per (sequence, kv head) there are kv_units(n)
-// units for n row chunks: first the units that start at their chunk's first
-// row ("full"), chunk by chunk (chunk ch has tiles 0 .. ch*T of them, T =
-// tiles per chunk); then the diagonal units (key tile inside its first chunk
-// but not at its start), longest first (exactly so when S fills whole
-// chunks; a partial last chunk's are shorter).  Units whose tile lies past S, or
-// whose rows are empty, do nothing.  Host-callable for checking.
+// the chunk (kv_chunk_rows(S), T key tiles long), and a unit is one (key
+// tile kt, row chunk ch) pair that writes its own partial sum.  Per
+// (sequence, kv head) there are kv_units(n, T) units for n row chunks: first
+// the units that start at their chunk's first row ("full"), chunk by chunk
+// (chunk ch has tiles 0 .. ch*T of them); then the diagonal units (key tile
+// inside its first chunk but not at its start), longest first (exactly so
+// when S fills whole chunks; a partial last chunk's are shorter).  Units
+// whose tile lies past S, or whose rows are empty, do nothing.  Longer chunks
+// mean fewer partial sums to write and add, shorter ones more, smaller units
+// to balance; a quarter of the sequence, between 2048 and 8192 rows,
+// measured best.  Host-callable for checking.
 constexpr int kKvKeys = 128;
-constexpr int kKvChunkRows = 2048;
-constexpr int kKvTilesPerChunk = kKvChunkRows / kKvKeys;
 
-__host__ __device__ inline int kv_units(int nchunks) {
-  const int T = kKvTilesPerChunk;
+__host__ __device__ inline int kv_chunk_rows(int S) {
+  int rows = (S / 4) / kKvKeys * kKvKeys;
+  if (rows < 2048) rows = 2048;
+  if (rows > 8192) rows = 8192;
+  return rows;
+}
+__host__ __device__ inline int kv_units(int nchunks, int T) {
   return T * nchunks * (nchunks - 1) / 2 + nchunks + nchunks * (T - 1);
 }
-__host__ __device__ inline void kv_unit(int u, int nchunks, int &kt, int &ch) {
-  const int T = kKvTilesPerChunk;
+__host__ __device__ inline void kv_unit(int u, int nchunks, int T, int &kt, int &ch) {
   ch = 0;
   while (ch < nchunks && u >= ch * T + 1) {  // full units of chunk ch
     u -= ch * T + 1;

@@ -7,10 +7,10 @@
   their neighbours, shard row counts, and random divisors up to 2^32 - 1,
   with edge dividends, random ones and multiples +-1.
 * The work schedule of the key-stationary backward pass: a host build of the
-  library's own kv_unit / kv_masked_steps, checked for coverage (every
+  library's own kv_chunk_rows / kv_unit / kv_masked_steps, checked for coverage (every
   (key tile, row chunk) pair with rows exactly once), order, the first chunk
   a tile writes, and that the steps after the masked ones need no mask, at 66
-  sequence lengths."""
+  sequence lengths, each with the chunk the library picks and five others."""
 import os
 import shutil
 import subprocess
