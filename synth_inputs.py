@@ -90,13 +90,16 @@ WORKLOADS = {
                                 G=4, rank=0, seed=4, b_total=2, seq_offset=0),
     "llama3_70b_s128k": Workload("llama3_70b_s128k", b=1, S=131072, H=64, H_kv=8,
                                  d=128, G=8, rank=5, seed=5),
-    # Two Table II models whose hidden size / heads give the other head dims,
-    # in the paper's training setup (sequence 16K, batch 2 on 8 GPUs: groups
-    # of 4, one sequence each).  The paper gives no kv-head count; 8 is used.
+    # Three Table II models whose hidden size / heads give the other head
+    # dims, in the paper's training setup (sequence 16K, batch 2 on 8 GPUs:
+    # groups of 4, one sequence each).  The paper gives no kv-head count; 8
+    # is used.
     "llama32_3b_s16k": Workload("llama32_3b_s16k", b=1, S=16384, H=32, H_kv=8, d=96,
                                 G=4, rank=1, seed=6),
     "qwen25_3b_s16k": Workload("qwen25_3b_s16k", b=1, S=16384, H=32, H_kv=8, d=80,
                                G=4, rank=2, seed=7),
+    "llama32_1b_s16k": Workload("llama32_1b_s16k", b=1, S=16384, H=32, H_kv=8, d=64,
+                                G=4, rank=3, seed=9),
     # Fewer kv heads than group members: Llama-3-8B under one group of 16
     # (two 8-GPU nodes, micro-batch 1); each kv head is shared by 2 members.
     "llama3_8b_g16_s64k": Workload("llama3_8b_g16_s64k", b=1, S=65536, H=32, H_kv=8,

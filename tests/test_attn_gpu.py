@@ -142,7 +142,8 @@ def test_bitwise_deterministic():
 
 
 FULL = ["llama3_8b_s32k", "qwen25_7b_s64k", "ulysses_g8_b2_s64k", "basp_g4_b1_s64k",
-        "llama3_70b_s128k", "llama32_3b_s16k", "qwen25_3b_s16k", "llama3_8b_g16_s64k"]
+        "llama3_70b_s128k", "llama32_3b_s16k", "qwen25_3b_s16k", "llama32_1b_s16k",
+        "llama3_8b_g16_s64k"]
 
 
 def _sample_rows(S, rng, n=40):
