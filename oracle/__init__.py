@@ -60,9 +60,13 @@ def lib():
     L.oracle_attn_bwd.argtypes = [vp] * 9 + [c_long] * 5 + [c_double, c_long]
     L.oracle_attn_rows.argtypes = ([vp] * 4 + [c_long] * 5 + [c_double, c_long]
                                    + [vp] * 6)
+    L.oracle_set_threads.argtypes = [c_int]
+    L.oracle_set_threads.restype = None
+    L.oracle_attn_keys.argtypes = ([vp] * 6 + [c_long] * 5 + [c_double, c_long]
+                                   + [vp] * 5)
     for f in ("oracle_group_of", "oracle_seq_partition", "oracle_pack",
               "oracle_unpack", "oracle_attn_fwd", "oracle_attn_bwd",
-              "oracle_attn_rows", "oracle_threads"):
+              "oracle_attn_rows", "oracle_attn_keys", "oracle_threads"):
         getattr(L, f).restype = c_int
     _lib = L
     return L
@@ -79,6 +83,11 @@ def _check(rc: int, what: str):
 
 def threads() -> int:
     return lib().oracle_threads()
+
+
+def set_threads(n: int) -> None:
+    """Run the oracle's parallel loops on n threads (n < 1: all processors)."""
+    lib().oracle_set_threads(int(n))
 
 
 def _np(x) -> np.ndarray:
@@ -121,8 +130,10 @@ def seq_partition(L: int, K: int, global_rank: int):
 
 
 # ------------------------------------------------------------ permutations
-def pack(shards, rank: int) -> np.ndarray:
-    """G shards [b, S/G, n, d] -> head-sharded local [b, S, n/G, d] (raw bytes)."""
+def pack(shards, rank: int, out: np.ndarray | None = None) -> np.ndarray:
+    """G shards [b, S/G, n, d] -> head-sharded local [b, S, n/G, d] (raw bytes).
+
+    ``out``: optional C-contiguous destination of that shape and dtype."""
     arrs = [_np(s) for s in shards]
     G = len(arrs)
     b, Sg, n, d = arrs[0].shape
@@ -130,7 +141,11 @@ def pack(shards, rank: int) -> np.ndarray:
         if a.shape != arrs[0].shape or a.dtype != arrs[0].dtype:
             raise OracleError("shards differ in shape or dtype")
     nl = n // G if n % G == 0 else (1 if (n < G and G % n == 0) else 0)
-    out = np.empty((b, Sg * G, nl, d), dtype=arrs[0].dtype)
+    shape = (b, Sg * G, nl, d)
+    if out is None:
+        out = np.empty(shape, dtype=arrs[0].dtype)
+    elif (out.shape != shape or out.dtype != arrs[0].dtype or not out.flags.c_contiguous):
+        raise OracleError("out must be a C-contiguous array of the packed shape and dtype")
     ptrs = (ctypes.c_void_p * G)(*[a.ctypes.data for a in arrs])
     rc = lib().oracle_pack(ptrs, _ptr(out), b, Sg * G, n, d, G, rank,
                            arrs[0].dtype.itemsize)
@@ -253,3 +268,26 @@ def attn_rows(q, k, v, do, scale: float, beta, head, row):
                                 _ptr(row), _ptr(o), _ptr(lse), _ptr(dq))
     _check(rc, "attn_rows")
     return o, lse, dq
+
+
+def attn_keys(q, k, v, do, o, lse, scale: float, beta, kvhead, key):
+    """dK_j and dV_j (summed over the kv head's query heads) at the sampled
+    (beta, kv head, key) triples; o [b,S,Hl,d] and lse [b,Hl,S] are every row
+    of ``attn_fwd``."""
+    q, k, v, do = _f64(q), _f64(k), _f64(v), _f64(do)
+    o, lse = _f64(o), _f64(lse)
+    b, S, Hl, d = q.shape
+    Hkl = k.shape[2]
+    if o.shape != (b, S, Hl, d) or lse.shape != (b, Hl, S):
+        raise OracleError("o/lse must cover every row")
+    beta = np.ascontiguousarray(beta, dtype=np.int64)
+    kvhead = np.ascontiguousarray(kvhead, dtype=np.int64)
+    key = np.ascontiguousarray(key, dtype=np.int64)
+    n = len(key)
+    dk = np.empty((n, d))
+    dv = np.empty((n, d))
+    rc = lib().oracle_attn_keys(_ptr(q), _ptr(k), _ptr(v), _ptr(do), _ptr(o), _ptr(lse),
+                                b, S, Hl, Hkl, d, scale, n, _ptr(beta), _ptr(kvhead),
+                                _ptr(key), _ptr(dk), _ptr(dv))
+    _check(rc, "attn_keys")
+    return dk, dv

@@ -46,6 +46,15 @@ int oracle_threads(void) {
 #endif
 }
 
+/* Threads of the parallel loops from now on (n < 1: every available one). */
+void oracle_set_threads(int n) {
+#ifdef _OPENMP
+  omp_set_num_threads(n >= 1 ? n : omp_get_num_procs());
+#else
+  (void)n;
+#endif
+}
+
 /* ---------------------------------------------------------------- Alg. 1 */
 int oracle_group_of(long world, long micro_batch, long global_rank,
                     long *group, long *local_rank, long *group_size) {
@@ -106,10 +115,12 @@ int oracle_pack(const void *const *src, void *dst, long b, long S, long n,
   int rc = perm_args_ok(b, S, n, d, G, rank, elem);
   if (rc) return rc;
   if (!src || !dst) return ORC_ERR_NULL;
+  for (long j = 0; j < G; ++j)
+    if (!src[j]) return ORC_ERR_NULL;
   long Sg = S / G, nl = heads_per_member(n, G), h0 = first_head(n, G, rank);
   for (long j = 0; j < G; ++j) {
     const unsigned char *s = (const unsigned char *)src[j];
-    if (!s) return ORC_ERR_NULL;
+#pragma omp parallel for collapse(2)
     for (long beta = 0; beta < b; ++beta)
       for (long t = 0; t < Sg; ++t)
         for (long h = 0; h < nl; ++h)
@@ -129,10 +140,12 @@ int oracle_unpack(const void *src, void *const *dst, long b, long S, long n,
   if (rc) return rc;
   if (!src || !dst) return ORC_ERR_NULL;
   if (n < G) return ORC_ERR_SHAPE; /* a shared head takes oracle_unpack_add */
+  for (long j = 0; j < G; ++j)
+    if (!dst[j]) return ORC_ERR_NULL;
   long Sg = S / G, nl = n / G;
   for (long j = 0; j < G; ++j) {
     unsigned char *o = (unsigned char *)dst[j];
-    if (!o) return ORC_ERR_NULL;
+#pragma omp parallel for collapse(2)
     for (long beta = 0; beta < b; ++beta)
       for (long t = 0; t < Sg; ++t)
         for (long h = 0; h < nl; ++h)
@@ -151,10 +164,12 @@ int oracle_unpack_add(const float *src, float *const *dst, long b, long S, long 
   int rc = perm_args_ok(b, S, n, d, G, rank, 4);
   if (rc) return rc;
   if (!src || !dst) return ORC_ERR_NULL;
+  for (long j = 0; j < G; ++j)
+    if (!dst[j]) return ORC_ERR_NULL;
   long Sg = S / G, nl = heads_per_member(n, G), h0 = first_head(n, G, rank);
   for (long j = 0; j < G; ++j) {
     float *o = dst[j];
-    if (!o) return ORC_ERR_NULL;
+#pragma omp parallel for collapse(2)
     for (long beta = 0; beta < b; ++beta)
       for (long t = 0; t < Sg; ++t)
         for (long h = 0; h < nl; ++h)
@@ -363,6 +378,50 @@ int oracle_attn_bwd(const double *q, const double *k, const double *v,
           }
       }
   free(D);
+  return ORC_OK;
+}
+
+/* Key-local gradients for sampled (beta, kv head, key) triples: dK_j and
+ * dV_j of the definition above, summed over the query heads sharing the kv
+ * head and over every row i >= j.  o/lse are all rows [0, S) of the
+ * forward; D_i is formed from them row by row. */
+int oracle_attn_keys(const double *q, const double *k, const double *v,
+                     const double *dout, const double *o, const double *lse,
+                     long b, long S, long Hl, long Hkl, long d, double scale,
+                     long nsamp, const long *beta, const long *kvhead,
+                     const long *key, double *dk_out, double *dv_out) {
+  int rc = attn_args_ok(b, S, Hl, Hkl, d);
+  if (rc) return rc;
+  if (nsamp < 0) return ORC_ERR_RANGE;
+  if (!q || !k || !v || !dout || !o || !lse || !beta || !kvhead || !key ||
+      !dk_out || !dv_out)
+    return ORC_ERR_NULL;
+  for (long n = 0; n < nsamp; ++n)
+    if (beta[n] < 0 || beta[n] >= b || kvhead[n] < 0 || kvhead[n] >= Hkl ||
+        key[n] < 0 || key[n] >= S)
+      return ORC_ERR_RANGE;
+  long n_rep = Hl / Hkl;
+#pragma omp parallel for schedule(dynamic, 1)
+  for (long n = 0; n < nsamp; ++n) {
+    long bt = beta[n], kvh = kvhead[n], j = key[n];
+    const double *kj = k + ((bt * S + j) * Hkl + kvh) * d;
+    const double *vj = v + ((bt * S + j) * Hkl + kvh) * d;
+    double *dkj = dk_out + n * d, *dvj = dv_out + n * d;
+    for (long e = 0; e < d; ++e) dkj[e] = dvj[e] = 0.0;
+    for (long h = kvh * n_rep; h < (kvh + 1) * n_rep; ++h)
+      for (long i = j; i < S; ++i) {
+        const double *qi = q + ((bt * S + i) * Hl + h) * d;
+        const double *doi = dout + ((bt * S + i) * Hl + h) * d;
+        const double *oi = o + ((bt * S + i) * Hl + h) * d;
+        double Di = dot(doi, oi, d);
+        double p = exp(scale * dot(qi, kj, d) - lse[(bt * Hl + h) * S + i]);
+        double ds = p * (dot(doi, vj, d) - Di);
+        for (long e = 0; e < d; ++e) {
+          dvj[e] += p * doi[e];
+          dkj[e] += scale * ds * qi[e];
+        }
+      }
+  }
   return ORC_OK;
 }
 

@@ -93,8 +93,21 @@ int oracle_attn_rows(const double *q, const double *k, const double *v,
                      const long *head, const long *row, double *o_out,
                      double *lse_out, double *dq_out);
 
+/* Key-local results for a list of (beta, kv head, key) samples: dK_j and
+ * dV_j summed over the query heads of the kv head and over every row i >= j.
+ * o [b,S,Hl,d] and lse [b,Hl,S] are all rows of oracle_attn_fwd.
+ * dk_out/dv_out [n, d]. */
+int oracle_attn_keys(const double *q, const double *k, const double *v,
+                     const double *dout, const double *o, const double *lse,
+                     long b, long S, long Hl, long Hkl, long d, double scale,
+                     long nsamp, const long *beta, const long *kvhead,
+                     const long *key, double *dk_out, double *dv_out);
+
 /* Number of OpenMP threads the oracle runs with. */
 int oracle_threads(void);
+
+/* Set the number of OpenMP threads (n < 1: all available processors). */
+void oracle_set_threads(int n);
 
 #ifdef __cplusplus
 }

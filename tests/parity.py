@@ -50,3 +50,37 @@ def local_heads(x: torch.Tensor, w, n: int):
 
 def device_shards(x: torch.Tensor, w, dev="cuda"):
     return [s.to(dev) for s in shards_of(x, w)]
+
+
+def fp64_kv_head(ql, kl, vl, dl, n_rep, scale, block=2048, device="cuda"):
+    """O, dQ of query heads 0 .. n_rep-1 and dK, dV of kv head 0 (sequence 0)
+    in plain fp64 torch on ``device``: per block of query rows, the dense
+    masked score block, its softmax, and the gradients of sum(O * dO) from
+    the definition (D = rowsum(dO * O), dS = P (dP - D)).  A second
+    reference for full-size shapes the CPU oracle cannot finish in a test;
+    a CPU test ties it to the oracle on small shapes."""
+    S, d = ql.shape[1], ql.shape[3]
+    K, V = kl[0, :, 0].to(device).double(), vl[0, :, 0].to(device).double()
+    rO = torch.empty(S, n_rep, d, dtype=torch.float64, device=device)
+    rdQ = torch.empty_like(rO)
+    rdK = torch.zeros(S, d, dtype=torch.float64, device=device)
+    rdV = torch.zeros_like(rdK)
+    for h in range(n_rep):
+        Q, dO = ql[0, :, h].to(device).double(), dl[0, :, h].to(device).double()
+        for r0 in range(0, S, block):
+            r1 = min(S, r0 + block)
+            s = (Q[r0:r1] @ K[:r1].T) * scale
+            keys = torch.arange(r1, device=device)[None, :]
+            rows = torch.arange(r0, r1, device=device)[:, None]
+            s.masked_fill_(keys > rows, float("-inf"))
+            p = torch.softmax(s, dim=1)
+            del s
+            ob = p @ V[:r1]
+            rO[r0:r1, h] = ob
+            ds = p * (dO[r0:r1] @ V[:r1].T - (dO[r0:r1] * ob).sum(1, keepdim=True))
+            rdV[:r1] += p.T @ dO[r0:r1]
+            del p
+            rdQ[r0:r1, h] = scale * (ds @ K[:r1])
+            rdK[:r1] += scale * (ds.T @ Q[r0:r1])
+            del ds
+    return rO, rdQ, rdK, rdV

@@ -198,3 +198,54 @@ def test_bwd_invariants():
     np.testing.assert_allclose(dk.sum(axis=1), 0.0, atol=1e-12)   # shift invariance
     dosum = do.reshape(b, S, Hkl, Hl // Hkl, d).sum(axis=(1, 3))
     np.testing.assert_allclose(dv.sum(axis=1), dosum, rtol=0, atol=1e-11)  # rows of P sum to 1
+
+
+@pytest.mark.parametrize("b,S,Hl,Hkl,d", [(2, 29, 4, 2, 16), (1, 40, 7, 1, 8)])
+def test_key_samples_match_autograd(b, S, Hl, Hkl, d):
+    """The key-local dK_j, dV_j (summed over the kv head's query heads) equal
+    torch fp64 autograd at every key, and the full backward's rows."""
+    q, k, v, do = _case(b, S, Hl, Hkl, d, seed=7 * S)
+    c = 1.0 / math.sqrt(d)
+    o, lse = oracle.attn_fwd(q, k, v, c)
+    _, tk, tv = _torch_grads(q, k, v, do, c)
+    _, dk, dv = oracle.attn_bwd(q, k, v, do, o, lse, c)
+    beta, kvh, key = zip(*[(bt, g, j) for bt in range(b) for g in range(Hkl) for j in range(S)])
+    sk, sv = oracle.attn_keys(q, k, v, do, o, lse, c, beta, kvh, key)
+    for n, (bt, g, j) in enumerate(zip(beta, kvh, key)):
+        np.testing.assert_allclose(sk[n], tk[bt, j, g], rtol=0, atol=1e-12)
+        np.testing.assert_allclose(sv[n], tv[bt, j, g], rtol=0, atol=1e-12)
+        np.testing.assert_allclose(sk[n], dk[bt, j, g], rtol=0, atol=1e-13)
+        np.testing.assert_allclose(sv[n], dv[bt, j, g], rtol=0, atol=1e-13)
+
+
+def test_key_samples_closed_form_zero_keys():
+    """K = 0: dV_j = sum_h sum_{i>=j} dO_i / (i+1) and dK_j = c sum_h sum_{i>=j}
+    dS_ij q_i with P_ij = 1/(i+1), dS_ij = (dO_i.v_j - D_i)/(i+1)."""
+    b, S, Hl, Hkl, d = 1, 33, 4, 2, 8
+    q, k, v, do = _case(b, S, Hl, Hkl, d, seed=77)
+    k[:] = 0.0
+    c = 0.5
+    o, lse = oracle.attn_fwd(q, k, v, c)
+    n_rep = Hl // Hkl
+    key = [0, 5, 32]
+    for g in range(Hkl):
+        sk, sv = oracle.attn_keys(q, k, v, do, o, lse, c, [0] * 3, [g] * 3, key)
+        for n, j in enumerate(key):
+            ev = np.zeros(d)
+            ek = np.zeros(d)
+            for h in range(g * n_rep, (g + 1) * n_rep):
+                for i in range(j, S):
+                    prefix = v[0, :i + 1, g].mean(axis=0)          # O_i: mean of v_0..v_i
+                    Di = do[0, i, h] @ prefix
+                    ev += do[0, i, h] / (i + 1)
+                    ek += c * (do[0, i, h] @ v[0, j, g] - Di) / (i + 1) * q[0, i, h]
+            np.testing.assert_allclose(sv[n], ev, rtol=0, atol=1e-12)
+            np.testing.assert_allclose(sk[n], ek, rtol=0, atol=1e-12)
+
+
+def test_key_samples_reject_bad_indices():
+    q, k, v, do = _case(1, 8, 2, 1, 4, seed=1)
+    o, lse = oracle.attn_fwd(q, k, v, 0.5)
+    for bad in (([1], [0], [0]), ([0], [1], [0]), ([0], [0], [8]), ([0], [0], [-1])):
+        with pytest.raises(oracle.OracleError):
+            oracle.attn_keys(q, k, v, do, o, lse, 0.5, *bad)
