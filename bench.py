@@ -4,11 +4,17 @@ A step is one pass of the whole share over one batch of synthetic inputs
 already resident in HBM:
   pack(Q, K, V) -> causal GQA attention fwd -> unpack(O)
   pack(dO) -> attention bwd -> unpack(dQ, dK, dV)
+The default workload is the largest single-GPU share: Llama-3-70B shapes at
+S = 128K (b = 1, 64 query / 8 kv heads, d = 128, G = 8, rank 5).
 The reported value is attention FLOPs (fwd + bwd, causal half of S^2,
-bwd = 2.5 x fwd) divided by the whole step's time, in TFLOP/s; the pack and
+bwd = 2.5 x fwd) divided by the median step time, in TFLOP/s; the pack and
 unpack permutations are inside the step and also reported as GB/s, both as
 timed in the step and with cold caches (each call alone after a 1 GiB
-scratch write), next to a plain device copy under the same conditions.
+scratch write).  Achievable peaks measured on the same GPU (back-to-back bf16
+MFMAs, a 1 GiB streaming copy) are reported as second denominators next to
+the published ones.  The CPU oracle is timed on a bounded sample of the
+same workload: fp64 attention on all host cores, and the step's
+permutations on one core and on all cores.
 
 Prints one JSON line.  With --gpus N > 1 it exits: this build runs one rank's
 share on one GPU (the exchange between ranks is not part of it).
@@ -34,26 +40,31 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
+# Sources of the attention-backward kernels (the dominant call): the counter
+# summary under profiles/ stays valid while these hash to what it records.
+BWD_KERNEL_SOURCES = ("paper_2609_03151_amd/csrc/basp_attn_bwd.hip",
+                      "paper_2609_03151_amd/csrc/basp_device.hpp",
+                      "paper_2609_03151_amd/csrc/basp_internal.hpp")
+
+
 def kernel_source_sha256() -> str:
-    """Hash of the HIP sources and the C ABI header (matches profiles/traffic_*.txt)."""
-    import glob
+    """Hash of the attention-backward kernel sources (matches profiles/traffic_*.txt)."""
     import hashlib
     h = hashlib.sha256()
-    paths = sorted(glob.glob(os.path.join(ROOT, "paper_2609_03151_amd", "csrc", "*")))
-    paths.append(os.path.join(ROOT, "include", "basp.h"))
-    for p in paths:
-        if p.endswith((".hip", ".hpp", ".cpp", ".h")):
-            with open(p, "rb") as f:
-                h.update(f.read())
+    for p in BWD_KERNEL_SOURCES:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
     return h.hexdigest()
 
 
 def recorded_traffic(workload: str):
-    """HBM traffic per attention-backward launch from the committed counter
-    summary, or None when the kernels changed since those counters were taken."""
-    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.txt")
+    """(bytes, source) of HBM traffic per attention-backward launch, from the
+    committed rocprofv3 FETCH_SIZE/WRITE_SIZE summary of this workload, or
+    (None, reason) when there is none or the kernels changed since."""
+    rel = os.path.join("profiles", f"traffic_{workload}.txt")
+    path = os.path.join(ROOT, rel)
     if not os.path.exists(path):
-        return None
+        return None, f"no counter summary {rel}"
     kv = {}
     with open(path) as f:
         for ln in f:
@@ -61,21 +72,94 @@ def recorded_traffic(workload: str):
                 a, b = ln.split("=", 1)
                 kv[a.strip()] = b.strip()
     if kv.get("source_sha256") != kernel_source_sha256():
-        return None
-    return int(kv["traffic_bytes"])
+        return None, f"{rel} was taken on other kernel sources"
+    return int(kv["traffic_bytes"]), f"recorded: {rel} (rocprofv3 FETCH_SIZE + WRITE_SIZE)"
 
 
-def cpu_baseline(w, target_s: float):
+def cpu_info() -> dict:
+    """Host CPU model and the cores this process may run on."""
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for ln in f:
+                if ln.startswith("model name"):
+                    model = ln.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"model": model, "cores_available": len(os.sched_getaffinity(0))}
+
+
+def cpu_pack_unpack_baseline(w, q, k, v, do) -> dict:
+    """The step's eight permutations (pack Q, K, V, unpack O, pack dO, unpack
+    fp32 dQ, dK, dV) of the whole workload by the oracle's index loops, on one
+    core and on all cores, in GB/s under the GPU's byte convention (each moved
+    element read once and written once; an added gradient read twice)."""
+    import numpy as np
+    import oracle
+    import torch
+    from synth_inputs import shards_of
+
+    bits = lambda x: [s.view(torch.int16).numpy() for s in shards_of(x, w)]
+    qs, ks, vs, ds = bits(q), bits(k), bits(v), bits(do)
+    b, Sg, G, r = w.b, w.S // w.G, w.G, w.rank
+    shared = w.H_kv < w.G
+
+    def shard_bufs(n, dtype):
+        return [np.zeros((b, Sg, n, w.d), dtype=dtype) + 0 for _ in range(G)]
+
+    o_sh = shard_bufs(w.H, np.int16)
+    dq_sh, dk_sh, dv_sh = (shard_bufs(w.H, np.float32), shard_bufs(w.H_kv, np.float32),
+                           shard_bufs(w.H_kv, np.float32))
+    dq_l = np.ones((b, w.S, w.Hl, w.d), dtype=np.float32)
+    dk_l = np.ones((b, w.S, w.Hkl, w.d), dtype=np.float32)
+
+    # Destinations allocated and touched once, outside the timed calls.
+    ql, dl = (np.zeros((b, w.S, w.Hl, w.d), dtype=np.int16) + 0 for _ in range(2))
+    kl, vl = (np.zeros((b, w.S, w.Hkl, w.d), dtype=np.int16) + 0 for _ in range(2))
+
+    def run():
+        t0 = time.perf_counter()
+        oracle.pack(qs, r, out=ql)
+        oracle.pack(ks, r, out=kl)
+        oracle.pack(vs, r, out=vl)
+        oracle.unpack(ql, o_sh, r)          # O stand-in: a local tensor of O's shape
+        oracle.pack(ds, r, out=dl)
+        oracle.unpack(dq_l, dq_sh, r)
+        if shared:
+            oracle.unpack_add(dk_l, dk_sh, r)
+            oracle.unpack_add(dk_l, dv_sh, r)
+        else:
+            oracle.unpack(dk_l, dk_sh, r)
+            oracle.unpack(dk_l, dv_sh, r)
+        nbytes = (2 * (ql.nbytes + kl.nbytes + vl.nbytes) + 2 * ql.nbytes + 2 * ql.nbytes
+                  + 2 * dq_l.nbytes + (3 if shared else 2) * 2 * dk_l.nbytes)
+        return nbytes, time.perf_counter() - t0
+
+    oracle.set_threads(0)
+    run()                                  # first touch of every buffer, untimed
+    nb, t_all = run()
+    cores = oracle.threads()
+    oracle.set_threads(1)
+    _, t_one = run()
+    oracle.set_threads(0)
+    return {"value": round(nb / t_all / 1e9, 3), "unit": "GB/s", "cores": cores,
+            "kind": "oracle", "value_1core": round(nb / t_one / 1e9, 3),
+            "sample": f"the step's 8 permutations of the whole workload ({nb / 2**20:.0f} MiB "
+                      f"moved): {t_all:.2f} s on {cores} cores, {t_one:.2f} s on 1 core",
+            "seconds": round(t_all + t_one, 3)}
+
+
+def cpu_baseline(w, target_s: float, q, k, v, do):
     """Time the oracle (fp64, OpenMP) on a bounded prefix of the workload.
 
     Sample: sequence 0 of the share, every local head, the first S' tokens,
     full forward and backward of causal attention restricted to them; S' is
     chosen from a short calibration run so the sample takes ~target_s."""
     import oracle
-    import torch
-    from synth_inputs import global_tensors, shards_of
 
-    q, k, v, do = global_tensors(w)
+    oracle.set_threads(0)
+
     def loc(x, n):
         h0, nl = w.first_head(n), (n // w.G if n >= w.G else 1)
         return x[w.seq_offset:w.seq_offset + 1, :, h0:h0 + nl]
@@ -176,19 +260,21 @@ def cold_permutation_rates(sh, reps: int = 5):
     }
     total_ms = sum(t for t, _ in per.values())
     total_bytes = sum(b for _, b in per.values())
-    biggest = max(b for _, b in each.values()) // 2
-    src = torch.empty(biggest // 4, dtype=torch.float32, device="cuda").fill_(2.0)
-    dst = torch.empty_like(src)
-    copy_ms = cold(lambda: dst.copy_(src))
-    del scratch, src, dst, send_q, send_k, own_dq, recv_dq
+    del scratch, send_q, send_k, own_dq, recv_dq
     return {
         "pack_unpack_cold_gbps": round(total_bytes / (total_ms * 1e-3) / 1e9, 1),
         "pack_unpack_cold_gbps_by_call": {n: round(b / (t * 1e-3) / 1e9, 1) for n, (t, b) in per.items()},
         "pack_unpack_cold_gbps_by_tensor": {n: round(b / (t * 1e-3) / 1e9, 1)
                                             for n, (t, b) in each.items()},
-        "hbm_copy_cold_gbps": round(2 * biggest / (copy_ms * 1e-3) / 1e9, 1),
         "a2a_cold_gbps_by_call": {n: round(b / (t * 1e-3) / 1e9, 1) for n, (t, b) in a2a.items()},
     }
+
+
+def measured_peaks() -> dict:
+    """Achievable peaks of this GPU: bf16 MFMA issue rate and a 1 GiB copy."""
+    from paper_2609_03151_amd import peak
+    return {"mfma_bf16_tflops": round(peak.mfma_bf16_tflops(), 1),
+            "hbm_copy_gbps": round(peak.copy_gbps(1 << 30), 1)}
 
 
 def main():
@@ -196,7 +282,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="llama3_8b_s32k")
+    ap.add_argument("--workload", default="llama3_70b_s128k")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     args = ap.parse_args()
@@ -219,7 +305,6 @@ def main():
     q, k, v, do = global_tensors(w)
     dev = lambda x: [s.cuda() for s in shards_of(x, w)]
     sh = RankShare(dev(q), dev(k), dev(v), dev(do), G=w.G, rank=w.rank, scale=w.scale)
-    del q, k, v, do
     log("[bench] inputs on device")
 
     for _ in range(args.warmup):
@@ -241,11 +326,14 @@ def main():
             e[i + 1].record()
     stop.record()
     torch.cuda.synchronize()
+    import statistics
     total_ms = start.elapsed_time(stop)
-    ms_step = total_ms / args.steps
+    ms_mean = total_ms / args.steps
+    ms_step = statistics.median(ev[s][0].elapsed_time(ev[s][-1]) for s in range(args.steps))
     phase_ms = {ph: sum(ev[s][i].elapsed_time(ev[s][i + 1]) for s in range(args.steps)) / args.steps
                 for i, ph in enumerate(phases)}
-    log(f"[bench] {args.steps} steps, {ms_step:.3f} ms/step; phases {phase_ms}")
+    log(f"[bench] {args.steps} steps, median {ms_step:.3f} ms/step (mean {ms_mean:.3f}); "
+        f"phases {phase_ms}")
 
     fwd_f, bwd_f = sh.attn_fwd_flops(), sh.attn_bwd_flops()
     value = (fwd_f + bwd_f) / (ms_step * 1e-3) / 1e12
@@ -264,6 +352,7 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms_step, 4),
+        "ms_per_step_mean": round(ms_mean, 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -276,7 +365,7 @@ def main():
                        if dom == "attn_bwd" else "basp_attn_fwd"),
             "bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-            "traffic": recorded_traffic(w.name) if dom == "attn_bwd" else None,
+            "traffic": None,
         },
         "attn_fwd_tflops": round(fwd_tf, 2),
         "attn_bwd_tflops": round(bwd_tf, 2),
@@ -288,13 +377,26 @@ def main():
         "phase_ms": {p: round(t, 4) for p, t in phase_ms.items()},
         "cpu_baseline": None,
     }
+    if dom == "attn_bwd":
+        traffic, src = recorded_traffic(w.name)
+        out["roofline"]["traffic"] = traffic
+        out["roofline"]["traffic_source"] = src
     out.update(sharded_step_rate(sh, args.steps, fwd_f + bwd_f))
     out.update(cold_permutation_rates(sh))
-    log(f"[bench] cold permutations {out['pack_unpack_cold_gbps']} GB/s, "
-        f"device copy {out['hbm_copy_cold_gbps']} GB/s")
+    del sh
+    torch.cuda.empty_cache()
+    pk = measured_peaks()
+    out["peak_measured"] = pk
+    out["roofline"]["frac_of_measured_peak"] = round(achieved / pk["mfma_bf16_tflops"], 4)
+    out["attn_fwd_frac_of_measured_peak"] = round(fwd_tf / pk["mfma_bf16_tflops"], 4)
+    out["pack_unpack_cold_frac_of_measured_copy"] = round(
+        out["pack_unpack_cold_gbps"] / pk["hbm_copy_gbps"], 4)
+    log(f"[bench] cold permutations {out['pack_unpack_cold_gbps']} GB/s; measured peaks {pk}")
     if not args.no_cpu_baseline:
-        log("[bench] timing the CPU oracle sample")
-        out["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
+        out["cpu"] = cpu_info()
+        log("[bench] timing the CPU oracle samples")
+        out["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds, q, k, v, do)
+        out["cpu_baseline_pack_unpack"] = cpu_pack_unpack_baseline(w, q, k, v, do)
     print(json.dumps(out), flush=True)
 
 

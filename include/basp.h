@@ -80,12 +80,23 @@ typedef enum basp_status {
   BASP_ERR_DP_FALLBACK = 8  /* micro-batch larger than the world (plain DP)  */
 } basp_status;
 
-typedef enum basp_dtype { BASP_BF16 = 0, BASP_F32 = 1 } basp_dtype;
+/* Element type of a permuted tensor.  Values other than the two listed are
+ * rejected with BASP_ERR_UNSUPPORTED (the last enumerator only keeps the
+ * type as wide as int, so that any int a caller passes is representable). */
+typedef enum basp_dtype {
+  BASP_BF16 = 0,
+  BASP_F32 = 1,
+  BASP_DTYPE_INT_RANGE_ = 0x7fffffff
+} basp_dtype;
 
 /* Largest group size the permutation kernels accept. */
 #define BASP_MAX_GROUP 128
 
-/* Human-readable name of a status code (static string, never NULL). */
+/* Human-readable name of a status code (static string, never NULL).  The
+ * codes report, before any device work, the conditions the method requires
+ * of its sizes: the group-formation assert N mod B = 0 of Alg. 1 and the
+ * equal token chunks L/K of Alg. 2 are BASP_ERR_SHAPE, B > N (Sec. IV-A's
+ * fall-back to data parallelism) is BASP_ERR_DP_FALLBACK. */
 const char *basp_status_str(int status);
 
 /* Batch-aware group formation (Alg. 1) and rank placement (Alg. 2):
@@ -97,8 +108,12 @@ int basp_group_of(int world, int micro_batch, int global_rank, int *group,
                   int *local_rank, int *group_size);
 
 /* Check a share's parameters (b, S, H, H_kv, d, G, rank) without touching
- * the GPU.  Returns BASP_OK or the code the other entry points would give
- * for the same shape (UNSUPPORTED when d is not 64, 80, 96 or 128). */
+ * the GPU: the sequence splits into G equal contiguous chunks (Alg. 2,
+ * S % G == 0), the query heads into G equal blocks (Sec. II-C head split,
+ * H % G == 0), the kv heads into G blocks or G/H_kv members per kv head
+ * (Sec. II-A GQA), H % H_kv == 0, and 0 <= rank < G.  Returns BASP_OK or the
+ * code the other entry points would give for the same shape (UNSUPPORTED
+ * when d is not 64, 80, 96 or 128). */
 int basp_validate(int b, int S, int H, int H_kv, int d, int G, int rank);
 
 /* Receive side of the head-parallel all-to-all (Sec. II-C, Sec. IV-C):
@@ -112,7 +127,7 @@ int basp_validate(int b, int S, int H, int H_kv, int d, int G, int rank);
  * RANK, UNSUPPORTED (dtype, G > BASP_MAX_GROUP, (S/G)*nl*d >= 2^31 elements,
  * or b*G > 65535), ALIGN, HIP. */
 int basp_pack(const void *const *src_shards, void *dst, int b, int S,
-              int n_heads, int d, int G, int rank, int dtype, void *stream);
+              int n_heads, int d, int G, int rank, basp_dtype dtype, void *stream);
 
 /* Send side, the inverse on the rank's head slice (Sec. II-C: the second
  * all-to-all returns the attention output to the sequence owners):
@@ -121,7 +136,7 @@ int basp_pack(const void *const *src_shards, void *dst, int b, int S,
  * untouched.  Arguments and errors as basp_pack, plus SHAPE when n < G (a
  * shared head takes basp_unpack_add). */
 int basp_unpack(const void *src, void *const *dst_shards, int b, int S,
-                int n_heads, int d, int G, int rank, int dtype, void *stream);
+                int n_heads, int d, int G, int rank, basp_dtype dtype, void *stream);
 
 /* Gradient form of basp_unpack, fp32 only: the rank's rows are added into
  * the shards instead of written,
@@ -145,7 +160,7 @@ int basp_unpack_add(const float *src, float *const *dst_shards, int b, int S,
  * basp_pack calls, checked before anything is launched. */
 int basp_pack_qkv(const void *const *q_shards, const void *const *k_shards,
                   const void *const *v_shards, void *q, void *k, void *v, int b,
-                  int S, int H, int H_kv, int d, int G, int rank, int dtype,
+                  int S, int H, int H_kv, int d, int G, int rank, basp_dtype dtype,
                   void *stream);
 
 /* The send side of the backward's last exchange in one call: basp_unpack of
@@ -171,7 +186,7 @@ int basp_unpack_grads(const float *dq, const float *dk, const float *dv,
  * (send [G, b, S/G, 1, d]).  dtype as basp_pack; values copied bit for bit.
  * Errors: NULL, SHAPE (as basp_pack), UNSUPPORTED (as basp_pack), ALIGN, HIP. */
 int basp_a2a_pack(const void *own, void *send, int b, int S, int n_heads, int d,
-                  int G, int dtype, void *stream);
+                  int G, basp_dtype dtype, void *stream);
 
 /* Receive side of the second all-to-all (the attention output returns to
  * the sequence owners): block j, received from member j and holding heads
@@ -184,7 +199,7 @@ int basp_a2a_pack(const void *own, void *send, int b, int S, int n_heads, int d,
  * Arguments and errors as basp_a2a_pack, plus UNSUPPORTED for a bf16 tensor
  * with n < G. */
 int basp_a2a_unpack(const void *recv, void *own, int b, int S, int n_heads, int d,
-                    int G, int dtype, void *stream);
+                    int G, basp_dtype dtype, void *stream);
 
 /* Causal GQA scaled dot-product attention (Sec. II-A) over the full sequence
  * for the rank's H/G query heads:
@@ -225,11 +240,22 @@ int basp_attn_fwd_sharded(const void *const *q_shards,
                           float *lse, int b, int S, int H, int H_kv, int d,
                           int G, int rank, float scale, void *stream);
 
-/* Bytes of device workspace basp_attn_bwd needs for this shape. */
+/* Bytes of device workspace basp_attn_bwd (and basp_attn_bwd_sharded) needs
+ * for this share of the Sec. II-A attention backward: the per-row pair
+ * (LSE, D_i = dO_i . O_i) of every local query head, and, when S is longer
+ * than one row chunk of the key pass (a quarter of S, 2048 to 8192 rows),
+ * fp32 partial sums of dK and dV per chunk.  0 for an invalid shape. */
 size_t basp_attn_bwd_workspace_bytes(int b, int S, int H, int H_kv, int d,
                                      int G);
 
-/* Backward of basp_attn_fwd for the loss sum(O * dO): inputs q, k, v, o, d_o
+/* Backward of basp_attn_fwd (the Sec. II-A scaled dot-product attention;
+ * the paper states the forward, and the gradients follow from it):
+ *   P_ij = exp(scale q_i.k_j - LSE_i),  D_i = dO_i . O_i,
+ *   dS_ij = P_ij (dO_i . v_j - D_i),
+ *   dQ_i = scale sum_{j<=i} dS_ij k_j,
+ *   dK_j = scale sum_{h} sum_{i>=j} dS_ij q_i,  dV_j = sum_{h} sum_{i>=j} P_ij dO_i
+ * (h over the local query heads of kv head j's group), for the loss
+ * sum(O * dO): inputs q, k, v, o, d_o
  * (bf16, layouts as above) and lse from the forward; outputs
  * dq [b,S,H/G,d], dk/dv [b,S,Hkl,d] in fp32, each fully overwritten
  * (dk/dv sum over the rank's query heads sharing a kv head; with a kv head

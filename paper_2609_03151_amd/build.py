@@ -1,7 +1,8 @@
 """Build libbasp.so (HIP for gfx950) in-tree with hipcc.
 
 Every translation unit under csrc/ is compiled to an object, then linked into
-paper_2609_03151_amd/libbasp.so.  Always recompiles (a few seconds per file).
+paper_2609_03151_amd/libbasp.so.  The benchmark's peak probes (peak/) become
+paper_2609_03151_amd/libbasp_peak.so.  Always recompiles (a few seconds per file).
 """
 from __future__ import annotations
 
@@ -15,6 +16,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libbasp.so")
+PEAK_SRC = os.path.join(HERE, "peak", "basp_peak.hip")
+PEAK_LIB = os.path.join(HERE, "libbasp_peak.so")
 OBJDIR = os.path.join(HERE, "_build")
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
@@ -66,7 +69,22 @@ def build(verbose: bool = False) -> str:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
     os.replace(tmp, LIB)
+    build_peak(verbose)
     return LIB
+
+
+def build_peak(verbose: bool = False) -> str:
+    """libbasp_peak.so: the benchmark's achievable-peak probes (not libbasp)."""
+    tmp = PEAK_LIB + ".tmp"
+    cmd = [HIPCC, *FLAGS, "-shared", PEAK_SRC, "-o", tmp]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        sys.stderr.write(r.stdout + r.stderr)
+        raise RuntimeError("hipcc failed on basp_peak.hip")
+    os.replace(tmp, PEAK_LIB)
+    return PEAK_LIB
 
 
 if __name__ == "__main__":

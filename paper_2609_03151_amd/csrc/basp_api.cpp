@@ -320,19 +320,19 @@ int basp_validate(int b, int S, int H, int H_kv, int d, int G, int rank) {
 }
 
 int basp_pack(const void *const *src_shards, void *dst, int b, int S, int n_heads, int d,
-              int G, int rank, int dtype, void *stream) {
+              int G, int rank, basp_dtype dtype, void *stream) {
   return run_pack(true, false, src_shards, dst, b, S, n_heads, d, G, rank, dtype, stream);
 }
 
 int basp_unpack(const void *src, void *const *dst_shards, int b, int S, int n_heads, int d,
-                int G, int rank, int dtype, void *stream) {
+                int G, int rank, basp_dtype dtype, void *stream) {
   return run_pack(false, false, const_cast<const void *const *>(dst_shards), src, b, S, n_heads, d, G,
                   rank, dtype, stream);
 }
 
 int basp_pack_qkv(const void *const *q_shards, const void *const *k_shards,
                   const void *const *v_shards, void *q, void *k, void *v, int b, int S, int H,
-                  int H_kv, int d, int G, int rank, int dtype, void *stream) {
+                  int H_kv, int d, int G, int rank, basp_dtype dtype, void *stream) {
   basp::PermCall pc[3];
   bool empty = false;
   int rc = prep_pack(true, false, q_shards, q, b, S, H, d, G, rank, dtype, &pc[0], &empty);
@@ -370,12 +370,12 @@ int basp_unpack_add(const float *src, float *const *dst_shards, int b, int S, in
 }
 
 int basp_a2a_pack(const void *own, void *send, int b, int S, int n_heads, int d, int G,
-                  int dtype, void *stream) {
+                  basp_dtype dtype, void *stream) {
   return run_a2a(true, own, send, b, S, n_heads, d, G, dtype, stream);
 }
 
 int basp_a2a_unpack(const void *recv, void *own, int b, int S, int n_heads, int d, int G,
-                    int dtype, void *stream) {
+                    basp_dtype dtype, void *stream) {
   return run_a2a(false, recv, own, b, S, n_heads, d, G, dtype, stream);
 }
 

@@ -8,7 +8,8 @@
   LSE = ln(i+1), run-to-run bitwise determinism;
 * full workload sizes, in the launch configuration the benchmark times:
   sampled rows of O, LSE, dQ, the last keys' dK and dV, and the invariants
-  sum_j dK_j = 0 and sum_j dV_j = sum of dO over the group's heads; and, for
+  sum_j dK_j = 0 and sum_j dV_j = sum of dO over the group's heads; keys in
+  every row chunk of the backward's key pass against the oracle; and, for
   one kv head, every row and key against a plain fp64 torch computation.
 Bar: max |err| <= 2e-2 and mean |err| <= 2e-3 per tensor (LSE max 1e-3)."""
 import math
@@ -20,7 +21,7 @@ import torch
 import oracle
 import paper_2609_03151_amd as basp
 from paper_2609_03151_amd.share import RankShare
-from parity import (LSE_MAX_ABS, check_close, device_shards, local_heads, log,
+from parity import (LSE_MAX_ABS, check_close, device_shards, fp64_kv_head, local_heads, log,
                     workload_inputs)
 from synth_inputs import WORKLOADS, Workload, global_tensors
 
@@ -204,43 +205,61 @@ def test_attention_full_size_sampled(name):
     torch.cuda.empty_cache()
 
 
-def _fp64_kv_head(ql, kl, vl, dl, n_rep, scale, block=2048):
-    """O, dQ of query heads 0 .. n_rep-1 and dK, dV of kv head 0 (sequence 0)
-    in plain fp64 torch on the GPU: per block of query rows, the dense masked
-    score block, its softmax, and the gradients of sum(O * dO) from the
-    definition (D = rowsum(dO * O), dS = P (dP - D))."""
-    S, d = ql.shape[1], ql.shape[3]
-    K, V = kl[0, :, 0].cuda().double(), vl[0, :, 0].cuda().double()
-    rO = torch.empty(S, n_rep, d, dtype=torch.float64, device="cuda")
-    rdQ = torch.empty_like(rO)
-    rdK = torch.zeros(S, d, dtype=torch.float64, device="cuda")
-    rdV = torch.zeros_like(rdK)
-    for h in range(n_rep):
-        Q, dO = ql[0, :, h].cuda().double(), dl[0, :, h].cuda().double()
-        for r0 in range(0, S, block):
-            r1 = min(S, r0 + block)
-            s = (Q[r0:r1] @ K[:r1].T) * scale
-            keys = torch.arange(r1, device="cuda")[None, :]
-            rows = torch.arange(r0, r1, device="cuda")[:, None]
-            s.masked_fill_(keys > rows, float("-inf"))
-            p = torch.softmax(s, dim=1)
-            del s
-            ob = p @ V[:r1]
-            rO[r0:r1, h] = ob
-            ds = p * (dO[r0:r1] @ V[:r1].T - (dO[r0:r1] * ob).sum(1, keepdim=True))
-            rdV[:r1] += p.T @ dO[r0:r1]
-            del p
-            rdQ[r0:r1, h] = scale * (ds @ K[:r1])
-            rdK[:r1] += scale * (ds.T @ Q[r0:r1])
-            del ds
-    return rO, rdQ, rdK, rdV
+KEY_WORKLOADS = ["llama3_8b_s32k", "llama32_3b_s16k", "qwen25_3b_s16k", "llama32_1b_s16k"]
 
 
-@pytest.mark.parametrize("name", ["llama3_8b_s32k", "qwen25_7b_s64k", "llama3_70b_s128k"])
+def _keys_in_every_quarter(S, rng, per=6):
+    """Keys spread over the four quarters of the sequence: every quarter's first
+    and last key, keys at and beside 128-key tile edges, and random keys."""
+    q4 = S // 4
+    keys = {0, 1, 127, 128, S - 1}
+    for c in range(4):
+        lo = c * q4
+        keys.update({lo, lo + 1, lo + q4 - 1, lo + 127, lo + 128})
+        keys.update(rng.integers(lo, lo + q4, size=per).tolist())
+    return sorted(k for k in keys if 0 <= k < S)
+
+
+@pytest.mark.parametrize("name", KEY_WORKLOADS)
+def test_attention_full_size_keys_every_chunk(name):
+    """dK and dV at full size, in the benchmark's launch configuration, for keys
+    in every quarter of the sequence -- the backward's key pass cuts the rows at
+    a quarter of S (8192 rows at the Llama-3-8B share: 4 chunks), so key 0 sums
+    the partials of every chunk and a key in the last quarter has one -- against
+    the oracle's key-local gradients of kv head 0 (summed over its query heads;
+    LSE and D from the oracle's own forward of every row)."""
+    w = WORKLOADS[name]
+    log(f"[attn full keys] {name}: b={w.b} S={w.S} Hl={w.Hl} Hkl={w.Hkl}")
+    q, k, v, do = workload_inputs(name)
+    sh = RankShare(device_shards(q, w), device_shards(k, w), device_shards(v, w),
+                   device_shards(do, w), G=w.G, rank=w.rank, scale=w.scale)
+    sh.step()
+    torch.cuda.synchronize()
+    n_rep = w.Hl // w.Hkl
+    ql, kl, vl, dl = (local_heads(x, w, n)[:1, :, :nh].contiguous()
+                      for x, n, nh in ((q, w.H, n_rep), (k, w.H_kv, 1), (v, w.H_kv, 1),
+                                       (do, w.H, n_rep)))
+    ql64, kl64, vl64, dl64 = (x.double().numpy() for x in (ql, kl, vl, dl))
+    ro, rl = oracle.attn_fwd(ql64, kl64, vl64, w.scale)
+    log("  oracle forward of every row done")
+    keys = _keys_in_every_quarter(w.S, np.random.default_rng(w.seed + 100))
+    rdk, rdv = oracle.attn_keys(ql64, kl64, vl64, dl64, ro, rl, w.scale,
+                                [0] * len(keys), [0] * len(keys), keys)
+    kt = torch.tensor(keys, device="cuda")
+    check_close("dK keys", sh.dk[0, kt, 0].double().cpu().numpy(), rdk)
+    check_close("dV keys", sh.dv[0, kt, 0].double().cpu().numpy(), rdv)
+    check_close("O kv head 0", _f64(sh.o[:1, :, :n_rep]), ro)
+    del sh
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("name", ["llama3_8b_s32k", "qwen25_7b_s64k", "ulysses_g8_b2_s64k",
+                                  "basp_g4_b1_s64k", "llama3_70b_s128k"])
 def test_attention_full_size_kv_head_fp64(name):
     """Every row and key of one kv head at full size (sequence 0, kv head 0 and
     its query heads) against an independent fp64 computation in plain torch on
-    the GPU; the oracle's sampled rows and tails above pin the same outputs."""
+    the GPU (``fp64_kv_head``, tied to the oracle by a CPU test); the oracle's
+    sampled rows and keys pin the same outputs."""
     w = WORKLOADS[name]
     log(f"[attn full fp64] {name}")
     q, k, v, do = workload_inputs(name)
@@ -251,7 +270,7 @@ def test_attention_full_size_kv_head_fp64(name):
     ql, kl, vl, dl = (local_heads(x, w, n).contiguous()
                       for x, n in ((q, w.H), (k, w.H_kv), (v, w.H_kv), (do, w.H)))
     n_rep = w.Hl // w.Hkl
-    rO, rdQ, rdK, rdV = _fp64_kv_head(ql, kl, vl, dl, n_rep, w.scale)
+    rO, rdQ, rdK, rdV = fp64_kv_head(ql, kl, vl, dl, n_rep, w.scale)
     torch.cuda.synchronize()
     log("  fp64 reference done")
     for nm, got, ref in (("O", sh.o[0, :, :n_rep], rO), ("dQ", sh.dq[0, :, :n_rep], rdQ),

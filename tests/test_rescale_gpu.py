@@ -1,0 +1,110 @@
+"""Parity of the attention forward when a row's maximum logit keeps growing.
+
+The forward keeps, per query row, an exponent reference that starts at the
+largest logit of the first key tile and moves only when a later 64-key tile
+holds a logit more than 8 above it (in log2 units); moving it rescales the
+running sum, the output accumulator and, through them, the LSE the backward
+uses.  With N(0,1) inputs at scale 1/sqrt(d) a row's maximum hardly grows
+after the first tile, so these tests use ``ramped_local`` inputs, whose
+logits rise along the sequence (Sec. II-A's softmax over long rows with a
+recency bias), and check on the host, from the inputs alone, that a stated
+fraction of (row, later tile) pairs crosses the threshold.  O, LSE, dQ, dK and
+dV are then compared element by element with the fp64 oracle at the usual
+bar, on small shapes and on one S = 4096 shape whose key pass runs in two
+row chunks (GQA 4).
+"""
+import math
+
+import pytest
+import torch
+
+import oracle
+import paper_2609_03151_amd as basp
+from parity import LSE_MAX_ABS, check_close, log
+from synth_inputs import ramped_local
+
+pytestmark = pytest.mark.gpu
+
+TILE = 64          # keys per tile of the forward
+SLACK_LOG2 = 8.0   # the reference moves when a tile's maximum exceeds it by this
+
+
+def reference_moves(q, k, scale):
+    """(moves, pairs, rows moved twice or more) over every (sequence, head, row):
+    replays the reference rule on fp64 logits of the bf16 inputs, tile by tile."""
+    b, S, Hl, d = q.shape
+    n_rep = Hl // k.shape[2]
+    c = scale / math.log(2.0)
+    ntiles = (S + TILE - 1) // TILE
+    moves = pairs = multi = 0
+    keys = torch.arange(ntiles * TILE)
+    for bt in range(b):
+        for h in range(Hl):
+            Q = q[bt, :, h].double()
+            K = torch.zeros(ntiles * TILE, d, dtype=torch.float64)
+            K[:S] = k[bt, :, h // n_rep].double()
+            s = (Q @ K.T) * c
+            s.masked_fill_(keys[None, :] > torch.arange(S)[:, None], float("-inf"))
+            tmax = s.reshape(S, ntiles, TILE).max(dim=2).values
+            ref = tmax[:, 0].clone()
+            count = torch.zeros(S, dtype=torch.int64)
+            for t in range(1, ntiles):
+                live = torch.arange(S) >= t * TILE
+                grow = live & (tmax[:, t] > ref + SLACK_LOG2)
+                ref = torch.where(grow, tmax[:, t], ref)
+                count += grow.long()
+                pairs += int(live.sum())
+            moves += int(count.sum())
+            multi += int((count >= 2).sum())
+    return moves, pairs, multi
+
+
+CASES = [  # b, S, Hl, Hkl, d, least fraction of (row, later tile) pairs that move
+    (1, 1000, 4, 2, 128, 0.05),   # ragged tail, GQA 2 (8.1% move)
+    (2, 777, 2, 1, 64, 0.10),     # d = 64, b = 2, ragged (15.6%)
+    (1, 1200, 3, 1, 96, 0.05),    # d = 96, GQA 3 (8.6%)
+    (1, 4096, 4, 1, 128, 0.015),  # key pass in two row chunks, GQA 4 (2.1%)
+]
+
+
+@pytest.mark.parametrize("b,S,Hl,Hkl,d,frac", CASES)
+def test_moving_reference_matches_oracle(b, S, Hl, Hkl, d, frac):
+    log(f"[rescale] b={b} S={S} Hl={Hl} Hkl={Hkl} d={d}")
+    q, k, v, do = ramped_local(b, S, Hl, Hkl, d, seed=S + d)
+    scale = 1.0 / math.sqrt(d)
+    moves, pairs, multi = reference_moves(q, k, scale)
+    log(f"  reference moves: {moves} of {pairs} (row, later tile) pairs "
+        f"({moves / pairs:.3%}); rows moved at least twice: {multi}")
+    assert moves >= frac * pairs, "inputs do not exercise the moving reference"
+    assert multi > 0
+    qd, kd, vd, dod = (x.cuda() for x in (q, k, v, do))
+    o, lse = basp.attn_fwd(qd, kd, vd, G=1, scale=scale)
+    dq, dk, dv = basp.attn_bwd(qd, kd, vd, o, lse, dod, G=1, scale=scale)
+    torch.cuda.synchronize()
+    ro, rl = oracle.attn_fwd(q, k, v, scale)
+    rdq, rdk, rdv = oracle.attn_bwd(q, k, v, do, ro, rl, scale)
+    f64 = lambda t: t.double().cpu().numpy()
+    check_close("O", f64(o), ro)
+    check_close("LSE", f64(lse), rl, max_abs=LSE_MAX_ABS, mean_abs=LSE_MAX_ABS)
+    check_close("dQ", f64(dq), rdq)
+    check_close("dK", f64(dk), rdk)
+    check_close("dV", f64(dv), rdv)
+
+
+def test_moving_reference_in_place_path_is_bitwise_the_same():
+    """The in-place forward (shard buffers, G = 4) on ramped inputs gives the
+    composed path's O and LSE bit for bit."""
+    b, S, Hl, Hkl, d, G, rank = 1, 2048, 2, 1, 128, 4, 1
+    q, k, v, do = ramped_local(b, S, Hl * G, Hkl * G, d, seed=99)
+    scale = 1.0 / math.sqrt(d)
+    chunks = lambda x: [c.contiguous().cuda() for c in torch.chunk(x, G, dim=1)]
+    qs, ks, vs = chunks(q), chunks(k), chunks(v)
+    o_sh = [torch.zeros_like(s) for s in qs]
+    lse_a = basp.attn_fwd_sharded(qs, ks, vs, o_sh, rank, scale=scale)
+    ql = basp.pack(qs, rank)
+    kl, vl = basp.pack(ks, rank), basp.pack(vs, rank)
+    o, lse_b = basp.attn_fwd(ql, kl, vl, G=G, scale=scale, H_kv=Hkl * G)
+    torch.cuda.synchronize()
+    o_cat = torch.cat([s[:, :, rank * Hl:(rank + 1) * Hl] for s in o_sh], dim=1)
+    assert torch.equal(o_cat.view(torch.int16), o.view(torch.int16))
+    assert torch.equal(lse_a, lse_b)
