@@ -158,16 +158,19 @@ def small_workload(b=1, S=384, H=8, H_kv=2, d=128, G=2, rank=1, seed=11, name=No
                     b=b, S=S, H=H, H_kv=H_kv, d=d, G=G, rank=rank, seed=seed)
 
 
-def ramped_local(b, S, Hl, Hkl, d, seed, lift=12.0, ramp=12.0):
+def ramped_local(b, S, Hl, Hkl, d, seed, lift=12.0, ramp=12.0, do_std=0.25):
     """Local (head-sharded) Q, K, V, dO whose attention logits grow along the sequence.
 
     Q ``[b,S,Hl,d]``, K and V ``[b,S,Hkl,d]``, dO as Q, drawn in that order
     from one seeded generator as float32 standard normals; every element of Q
     is then shifted by ``lift/sqrt(d)`` and every element of K at position j
-    by ``ramp*(j/S)/sqrt(d)``, and all four are rounded to bfloat16 (round to
-    nearest even).  The shifts add ``lift*ramp*j/S`` to the dot product of any
-    query with key j, so a row's largest logit keeps rising over its later
-    keys (a recency-biased attention pattern)."""
+    by ``ramp*(j/S)/sqrt(d)``, dO is multiplied by ``do_std``, and all four
+    are rounded to bfloat16 (round to nearest even).  The shifts add
+    ``lift*ramp*j/S`` to the dot product of any query with key j, so a row's
+    largest logit keeps rising over its later keys (a recency-biased
+    attention pattern).  Such attention concentrates on few keys, which makes
+    dK and dV larger than under N(0,1) inputs; the smaller incoming gradient
+    keeps them in the same range (|dK|, |dV| up to about 2-3)."""
     gen = torch.Generator(device="cpu")
     gen.manual_seed(seed)
     q = torch.randn(b, S, Hl, d, generator=gen, dtype=torch.float32)
@@ -175,6 +178,7 @@ def ramped_local(b, S, Hl, Hkl, d, seed, lift=12.0, ramp=12.0):
     v = torch.randn(b, S, Hkl, d, generator=gen, dtype=torch.float32)
     do = torch.randn(b, S, Hl, d, generator=gen, dtype=torch.float32)
     q += lift / d ** 0.5
+    do *= do_std
     pos = torch.arange(S, dtype=torch.float32) / S
     k += (ramp / d ** 0.5) * pos[None, :, None, None]
     bf = torch.bfloat16

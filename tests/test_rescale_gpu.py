@@ -7,7 +7,9 @@ running sum, the output accumulator and, through them, the LSE the backward
 uses.  With N(0,1) inputs at scale 1/sqrt(d) a row's maximum hardly grows
 after the first tile, so these tests use ``ramped_local`` inputs, whose
 logits rise along the sequence (Sec. II-A's softmax over long rows with a
-recency bias), and check on the host, from the inputs alone, that a stated
+recency bias; the incoming gradient dO at a quarter of unit scale keeps dK
+and dV, which such concentrated attention enlarges, in the range of the other
+tests), and check on the host, from the inputs alone, that a stated
 fraction of (row, later tile) pairs crosses the threshold.  O, LSE, dQ, dK and
 dV are then compared element by element with the fp64 oracle at the usual
 bar, on small shapes and on one S = 4096 shape whose key pass runs in two
