@@ -81,12 +81,13 @@ typedef enum basp_status {
 } basp_status;
 
 /* Element type of a permuted tensor.  Values other than the two listed are
- * rejected with BASP_ERR_UNSUPPORTED (the last enumerator only keeps the
- * type as wide as int, so that any int a caller passes is representable). */
+ * rejected with BASP_ERR_UNSUPPORTED (the last two enumerators only make the
+ * type span every int, so that any int a caller passes is representable). */
 typedef enum basp_dtype {
   BASP_BF16 = 0,
   BASP_F32 = 1,
-  BASP_DTYPE_INT_RANGE_ = 0x7fffffff
+  BASP_DTYPE_INT_MAX_ = 0x7fffffff,
+  BASP_DTYPE_INT_MIN_ = -0x7fffffff - 1
 } basp_dtype;
 
 /* Largest group size the permutation kernels accept. */
@@ -244,7 +245,8 @@ int basp_attn_fwd_sharded(const void *const *q_shards,
  * for this share of the Sec. II-A attention backward: the per-row pair
  * (LSE, D_i = dO_i . O_i) of every local query head, and, when S is longer
  * than one row chunk of the key pass (a quarter of S, 2048 to 8192 rows),
- * fp32 partial sums of dK and dV per chunk.  0 for an invalid shape. */
+ * fp32 partial sums of dK and dV per chunk.  0 for an invalid shape, and
+ * for an empty one (b == 0 or S == 0), which needs none. */
 size_t basp_attn_bwd_workspace_bytes(int b, int S, int H, int H_kv, int d,
                                      int G);
 

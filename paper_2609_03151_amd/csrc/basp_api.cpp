@@ -311,12 +311,14 @@ int basp_group_of(int world, int micro_batch, int global_rank, int *group, int *
 }
 
 int basp_validate(int b, int S, int H, int H_kv, int d, int G, int rank) {
-  int rc = check_share(b, S, H, H_kv, d, G);
+  // The attention limits (head dims, 32-bit row indices), then the rank, then
+  // the permutation limits of the share's Q (n = H) and K, V (n = H_kv).
+  int rc = check_attn(b, S, H, H_kv, d, G, 1.f);
   if (rc) return rc;
   if (rank < 0 || rank >= G) return BASP_ERR_RANK;
-  if (d != 64 && d != 80 && d != 96 && d != 128) return BASP_ERR_UNSUPPORTED;
-  if (G > BASP_MAX_GROUP) return BASP_ERR_UNSUPPORTED;
-  return BASP_OK;
+  rc = check_perm_shape(b, S, H, d, G, BASP_BF16);
+  if (!rc) rc = check_perm_shape(b, S, H_kv, d, G, BASP_BF16);
+  return rc;
 }
 
 int basp_pack(const void *const *src_shards, void *dst, int b, int S, int n_heads, int d,

@@ -67,30 +67,6 @@ __device__ __forceinline__ void sched_reads_ahead() {
   __builtin_amdgcn_sched_group_barrier(kSchedMfma, A / R, 0);
 }
 
-// Workspace: LD [b][Hl][S] of (LSE * log2(e), D), then, when the key
-// passes are chunked, the dV and dK partial sums [chunk][b][S][H_kv/G][d].
-//
-// Work units of the key-stationary pass: see kv_unit.
-struct BwdChunks {
-  int rows;   // rows per chunk (a multiple of kKvKeys)
-  int T;      // key tiles per chunk
-  int n;      // row chunks
-  int units;  // work units per (sequence, kv head)
-  size_t part_offset_floats;
-};
-
-BwdChunks bwd_chunks(const AttnShape &s) {
-  BwdChunks ck;
-  ck.rows = kv_chunk_rows(s.S);
-  ck.T = ck.rows / kKvKeys;
-  ck.n = (s.S + ck.rows - 1) / ck.rows;
-  if (ck.n < 1) ck.n = 1;
-  ck.units = kv_units(ck.n, ck.T);
-  const size_t ld_floats = 2 * (size_t)s.b * s.Hl * s.S;
-  ck.part_offset_floats = (ld_floats + 63) & ~(size_t)63;  // 256-byte aligned
-  return ck;
-}
-
 // ---------------------------------------------------------------- bwd_pre
 // One group of D/8 lanes per (beta, row, head); 16-byte loads of O and dO.
 template <int D, bool SH>
@@ -813,13 +789,6 @@ hipError_t launch_bwd_d(const RowView &q, const RowView &k, const RowView &v, co
 }
 
 }  // namespace
-
-size_t attn_bwd_workspace_bytes(const AttnShape &s) {
-  const BwdChunks ck = bwd_chunks(s);
-  size_t floats = ck.part_offset_floats;
-  if (ck.n > 1) floats += 2 * (size_t)ck.n * s.b * s.Hkl * s.S * s.d;
-  return floats * sizeof(float);
-}
 
 hipError_t launch_attn_bwd(const RowView &q, const RowView &k, const RowView &v,
                            const RowView &o, const float *lse, const RowView &d_o,

@@ -167,7 +167,35 @@ hipError_t launch_attn_fwd(const RowView &q, const RowView &k, const RowView &v,
                            const RowView &o, float *lse, const AttnShape &s, bool sharded,
                            hipStream_t stream);
 
-size_t attn_bwd_workspace_bytes(const AttnShape &s);
+// Workspace of the backward: LD [b][Hl][S] of (LSE * log2(e), D), then, when
+// the key pass runs in more than one row chunk, the dV and dK partial sums
+// [chunk][b][S][Hkl][d] (fp32).  Host-callable.
+struct BwdChunks {
+  int rows;   // rows per chunk (a multiple of kKvKeys)
+  int T;      // key tiles per chunk
+  int n;      // row chunks
+  int units;  // work units per (sequence, kv head)
+  size_t part_offset_floats;
+};
+
+inline BwdChunks bwd_chunks(const AttnShape &s) {
+  BwdChunks ck;
+  ck.rows = kv_chunk_rows(s.S);
+  ck.T = ck.rows / kKvKeys;
+  ck.n = (s.S + ck.rows - 1) / ck.rows;
+  if (ck.n < 1) ck.n = 1;
+  ck.units = kv_units(ck.n, ck.T);
+  const size_t ld_floats = 2 * (size_t)s.b * s.Hl * s.S;
+  ck.part_offset_floats = (ld_floats + 63) & ~(size_t)63;  // 256-byte aligned
+  return ck;
+}
+
+inline size_t attn_bwd_workspace_bytes(const AttnShape &s) {
+  const BwdChunks ck = bwd_chunks(s);
+  size_t floats = ck.part_offset_floats;
+  if (ck.n > 1) floats += 2 * (size_t)ck.n * s.b * s.Hkl * s.S * s.d;
+  return floats * sizeof(float);
+}
 
 hipError_t launch_attn_bwd(const RowView &q, const RowView &k, const RowView &v,
                            const RowView &o, const float *lse, const RowView &d_o,
