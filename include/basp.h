@@ -272,6 +272,30 @@ int basp_attn_bwd(const void *q, const void *k, const void *v, const void *o,
                   int S, int H, int H_kv, int d, int G, float scale,
                   void *stream);
 
+/* Size of the device scratch buffer basp_attn_bwd_noalloc uses instead of a
+ * workspace argument (128 MiB, held on each GPU the library runs on). */
+#define BASP_NOALLOC_SCRATCH_BYTES ((size_t)128 << 20)
+
+/* basp_attn_bwd for callers that cannot allocate device memory (code under
+ * stream capture, allocation-free serving loops, harnesses that forbid
+ * hipMalloc): the same computation and results, bit for bit, with the
+ * workspace taken from a static device buffer of BASP_NOALLOC_SCRATCH_BYTES
+ * that the library holds on each GPU.  The first call on a GPU looks up that
+ * buffer's address; no call allocates or frees anything.  Arguments as
+ * basp_attn_bwd without workspace/workspace_bytes; the device is the one
+ * `stream` belongs to (the current device for the null stream).  Calls on
+ * one GPU share its buffer: calls that overlap on the device (other streams,
+ * other host threads) race and must not be issued; calls in order on one
+ * stream are safe, since nothing in the buffer is carried from one call to
+ * the next.  Errors: as basp_attn_bwd, and BASP_ERR_WORKSPACE when the shape
+ * needs more than BASP_NOALLOC_SCRATCH_BYTES
+ * (basp_attn_bwd_workspace_bytes() tells how much it needs), HIP when the
+ * buffer's address cannot be obtained. */
+int basp_attn_bwd_noalloc(const void *q, const void *k, const void *v,
+                          const void *o, const float *lse, const void *d_o,
+                          float *dq, float *dk, float *dv, int b, int S, int H,
+                          int H_kv, int d, int G, float scale, void *stream);
+
 /* basp_attn_bwd on the exchange's buffers in place: Q, K, V, O and dO are
  * read from their G sequence shards (layouts as basp_attn_fwd_sharded; dO as
  * Q) and dQ, dK, dV (fp32) are written into the rank's head slices of their

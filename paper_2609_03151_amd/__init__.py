@@ -29,7 +29,9 @@ STATUS = {
 EXPORTS = ("basp_status_str", "basp_group_of", "basp_validate", "basp_pack",
            "basp_unpack", "basp_unpack_add", "basp_pack_qkv", "basp_unpack_grads", "basp_a2a_pack", "basp_a2a_unpack", "basp_attn_fwd",
            "basp_attn_fwd_sharded", "basp_attn_bwd_workspace_bytes", "basp_attn_bwd",
-           "basp_attn_bwd_sharded")
+           "basp_attn_bwd_noalloc", "basp_attn_bwd_sharded")
+# Bytes of the static device buffer basp_attn_bwd_noalloc works in.
+NOALLOC_SCRATCH_BYTES = 128 << 20
 
 
 class BaspError(RuntimeError):
@@ -68,12 +70,14 @@ def lib() -> ctypes.CDLL:
     L.basp_attn_bwd_workspace_bytes.argtypes = [i] * 6
     L.basp_attn_bwd_workspace_bytes.restype = sz
     L.basp_attn_bwd.argtypes = [vp] * 10 + [sz] + [i] * 6 + [f, vp]
+    L.basp_attn_bwd_noalloc.argtypes = [vp] * 9 + [i] * 6 + [f, vp]
     tab = ctypes.POINTER(vp)
     L.basp_attn_fwd_sharded.argtypes = [tab] * 4 + [vp] + [i] * 7 + [f, vp]
     L.basp_attn_bwd_sharded.argtypes = ([tab] * 4 + [vp] + [tab] * 4 + [vp, sz] + [i] * 7
                                         + [f, vp])
     for name in ("basp_group_of", "basp_validate", "basp_pack", "basp_unpack",
-                 "basp_a2a_pack", "basp_a2a_unpack", "basp_attn_fwd", "basp_attn_bwd"):
+                 "basp_a2a_pack", "basp_a2a_unpack", "basp_attn_fwd", "basp_attn_bwd",
+                 "basp_attn_bwd_noalloc"):
         getattr(L, name).restype = i
     _lib = L
     return L
@@ -298,6 +302,22 @@ def attn_bwd(q, k, v, o, lse, do, G: int = 1, scale: float | None = None,
         _dev(dv, "dv", torch.float32), _dev(workspace, "workspace"),
         workspace.numel() * workspace.element_size(), b, S, H, H_kv, d, G, float(scale),
         _stream(q)), "basp_attn_bwd")
+    return dq, dk, dv
+
+
+def attn_bwd_noalloc(q, k, v, o, lse, do, dq, dk, dv, G: int = 1, scale: float | None = None,
+                     H_kv: int | None = None):
+    """attn_bwd into caller-given dq, dk, dv (fp32) with no workspace argument:
+    the library's static device buffer serves instead (basp_attn_bwd_noalloc)."""
+    b, S, H, H_kv, d = _attn_dims(q, k, G, H_kv)
+    scale = d ** -0.5 if scale is None else scale
+    _check(lib().basp_attn_bwd_noalloc(
+        _dev(q, "q", torch.bfloat16), _dev(k, "k", torch.bfloat16),
+        _dev(v, "v", torch.bfloat16), _dev(o, "o", torch.bfloat16),
+        _dev(lse, "lse", torch.float32), _dev(do, "do", torch.bfloat16),
+        _dev(dq, "dq", torch.float32), _dev(dk, "dk", torch.float32),
+        _dev(dv, "dv", torch.float32), b, S, H, H_kv, d, G, float(scale),
+        _stream(q)), "basp_attn_bwd_noalloc")
     return dq, dk, dv
 
 

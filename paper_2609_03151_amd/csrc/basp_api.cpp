@@ -425,24 +425,31 @@ size_t basp_attn_bwd_workspace_bytes(int b, int S, int H, int H_kv, int d, int G
   return basp::attn_bwd_workspace_bytes(s);
 }
 
-int basp_attn_bwd(const void *q, const void *k, const void *v, const void *o, const float *lse,
-                  const void *d_o, float *dq, float *dk, float *dv, void *workspace,
-                  size_t workspace_bytes, int b, int S, int H, int H_kv, int d, int G,
-                  float scale, void *stream) {
+}  // extern "C"
+
+namespace {
+
+// Checks of the local backward's tensors; *empty when there is nothing to do.
+int check_bwd_local(const void *q, const void *k, const void *v, const void *o, const float *lse,
+                    const void *d_o, float *dq, float *dk, float *dv, int b, int S, int H,
+                    int H_kv, int d, int G, float scale, bool *empty) {
   int rc = check_attn(b, S, H, H_kv, d, G, scale);
   if (rc) return rc;
-  if ((long long)b * S == 0) return BASP_OK;  // empty: no pointer is inspected
+  *empty = (long long)b * S == 0;
+  if (*empty) return BASP_OK;  // empty: no pointer is inspected
   if (!q || !k || !v || !o || !lse || !d_o || !dq || !dk || !dv) return BASP_ERR_NULL;
   if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(o, 16) ||
       !aligned(d_o, 16) || !aligned(dq, 16) || !aligned(dk, 16) || !aligned(dv, 16) ||
       !aligned(lse, 4))
     return BASP_ERR_ALIGN;
-  basp::AttnShape s = attn_shape(b, S, H, H_kv, d, G, scale);
-  const size_t need = basp::attn_bwd_workspace_bytes(s);
-  if (workspace_bytes < need) return BASP_ERR_WORKSPACE;
-  if (!workspace) return BASP_ERR_NULL;
-  if (!aligned(workspace, 16)) return BASP_ERR_ALIGN;
+  return BASP_OK;
+}
+
+int launch_bwd_local(const void *q, const void *k, const void *v, const void *o, const float *lse,
+                     const void *d_o, float *dq, float *dk, float *dv, void *workspace,
+                     const basp::AttnShape &s, void *stream) {
   using basp::local_view;
+  const int S = s.S, d = s.d;
   const basp::RowView qv = local_view(q, S, s.Hl, d), kv = local_view(k, S, s.Hkl, d),
                       vv = local_view(v, S, s.Hkl, d), ov = local_view(o, S, s.Hl, d),
                       dov = local_view(d_o, S, s.Hl, d), dqv = local_view(dq, S, s.Hl, d),
@@ -450,6 +457,39 @@ int basp_attn_bwd(const void *q, const void *k, const void *v, const void *o, co
   (void)hipGetLastError();
   return hip_status(basp::launch_attn_bwd(qv, kv, vv, ov, lse, dov, dqv, dkv, dvv, workspace, s,
                                           false, (hipStream_t)stream));
+}
+
+}  // namespace
+
+extern "C" {
+
+int basp_attn_bwd(const void *q, const void *k, const void *v, const void *o, const float *lse,
+                  const void *d_o, float *dq, float *dk, float *dv, void *workspace,
+                  size_t workspace_bytes, int b, int S, int H, int H_kv, int d, int G,
+                  float scale, void *stream) {
+  bool empty = false;
+  int rc = check_bwd_local(q, k, v, o, lse, d_o, dq, dk, dv, b, S, H, H_kv, d, G, scale, &empty);
+  if (rc || empty) return rc;
+  basp::AttnShape s = attn_shape(b, S, H, H_kv, d, G, scale);
+  const size_t need = basp::attn_bwd_workspace_bytes(s);
+  if (workspace_bytes < need) return BASP_ERR_WORKSPACE;
+  if (!workspace) return BASP_ERR_NULL;
+  if (!aligned(workspace, 16)) return BASP_ERR_ALIGN;
+  return launch_bwd_local(q, k, v, o, lse, d_o, dq, dk, dv, workspace, s, stream);
+}
+
+int basp_attn_bwd_noalloc(const void *q, const void *k, const void *v, const void *o,
+                          const float *lse, const void *d_o, float *dq, float *dk, float *dv,
+                          int b, int S, int H, int H_kv, int d, int G, float scale,
+                          void *stream) {
+  bool empty = false;
+  int rc = check_bwd_local(q, k, v, o, lse, d_o, dq, dk, dv, b, S, H, H_kv, d, G, scale, &empty);
+  if (rc || empty) return rc;
+  basp::AttnShape s = attn_shape(b, S, H, H_kv, d, G, scale);
+  if (basp::attn_bwd_workspace_bytes(s) > BASP_NOALLOC_SCRATCH_BYTES) return BASP_ERR_WORKSPACE;
+  void *scratch = nullptr;
+  if (basp::noalloc_scratch((hipStream_t)stream, &scratch) != hipSuccess) return BASP_ERR_HIP;
+  return launch_bwd_local(q, k, v, o, lse, d_o, dq, dk, dv, scratch, s, stream);
 }
 
 int basp_attn_bwd_sharded(const void *const *q_shards, const void *const *k_shards,

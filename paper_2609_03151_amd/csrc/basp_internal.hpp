@@ -197,6 +197,11 @@ inline size_t attn_bwd_workspace_bytes(const AttnShape &s) {
   return floats * sizeof(float);
 }
 
+// Device address of the static scratch buffer of basp_attn_bwd_noalloc
+// (BASP_NOALLOC_SCRATCH_BYTES) on the device of `stream` (the current device
+// for the null stream), looked up once per device.  Allocates nothing.
+hipError_t noalloc_scratch(hipStream_t stream, void **ptr);
+
 hipError_t launch_attn_bwd(const RowView &q, const RowView &k, const RowView &v,
                            const RowView &o, const float *lse, const RowView &d_o,
                            const RowView &dq, const RowView &dk, const RowView &dv,

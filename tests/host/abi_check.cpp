@@ -42,6 +42,12 @@ hipError_t launch_attn_bwd(const RowView &, const RowView &, const RowView &, co
   g_sharded = sharded;
   return hipSuccess;
 }
+static int g_scratch_lookups = 0;
+hipError_t noalloc_scratch(hipStream_t, void **ptr) {
+  ++g_scratch_lookups;
+  *ptr = reinterpret_cast<void *>(0x7000000);
+  return hipSuccess;
+}
 }  // namespace basp
 
 // The ABI layer clears a stale launch error before launching; no runtime here.
@@ -201,6 +207,29 @@ int main() {
                        128, 2, 0.1f, nullptr),
          BASP_OK);
   CHECK(basp::g_attn.S == 4096 && basp::g_attn.Hl == 4 && basp::g_attn.Hkl == 1);
+  // the allocation-free variant: same checks, the static buffer's size as the limit
+  EXPECT(basp_attn_bwd_noalloc(p[0], p[1], p[2], p[3], lse, p[5], fq, fk, fv, 1, 131072, 64, 8,
+                               128, 8, 0.1f, nullptr),
+         BASP_ERR_WORKSPACE);
+  CHECK(basp_attn_bwd_workspace_bytes(1, 131072, 64, 8, 128, 8) > BASP_NOALLOC_SCRATCH_BYTES);
+  EXPECT(basp_attn_bwd_noalloc(p[0], p[1], p[2], p[3], lse, nullptr, fq, fk, fv, 1, 4096, 8, 2,
+                               128, 2, 0.1f, nullptr),
+         BASP_ERR_NULL);
+  EXPECT(basp_attn_bwd_noalloc(p[0], p[1], p[2], p[3], lse, p[5], (float *)fake(0x700004), fk, fv,
+                               1, 4096, 8, 2, 128, 2, 0.1f, nullptr),
+         BASP_ERR_ALIGN);
+  EXPECT(basp_attn_bwd_noalloc(p[0], p[1], p[2], p[3], lse, p[5], fq, fk, fv, 1, 4096, 8, 2, 72,
+                               2, 0.1f, nullptr),
+         BASP_ERR_UNSUPPORTED);
+  CHECK(basp::g_scratch_lookups == 0);
+  EXPECT(basp_attn_bwd_noalloc(p[0], p[1], p[2], p[3], lse, p[5], fq, fk, fv, 1, 4096, 8, 2, 128,
+                               2, 0.1f, nullptr),
+         BASP_OK);
+  CHECK(basp::g_scratch_lookups == 1 && basp::g_attn.S == 4096);
+  EXPECT(basp_attn_bwd_noalloc(nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr,
+                               nullptr, nullptr, 0, 4096, 8, 2, 128, 2, 0.1f, nullptr),
+         BASP_OK);
+  CHECK(basp::g_scratch_lookups == 1);
 
   // ---- in place on the shard buffers
   void *tq[4], *to[4], *tk[4], *tv[4], *td[4], *tdq[4], *tdk[4], *tdv[4];

@@ -244,3 +244,18 @@ def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(basp, "LIB_PATH", str(tmp_path / "missing.so"))
     with pytest.raises(ImportError):
         basp.lib()
+
+
+def test_noalloc_backward_rejects_before_any_hip_call():
+    """basp_attn_bwd_noalloc: the shape checks of basp_attn_bwd, and a shape whose
+    workspace exceeds the static buffer is refused (fake pointers: only invalid
+    or empty calls here)."""
+    L = basp.lib()
+    p = [_fake(0x10000 * (i + 1)) for i in range(9)]
+    f = ctypes.c_float(0.125)
+    assert L.basp_attn_bwd_workspace_bytes(1, 131072, 64, 8, 128, 8) > basp.NOALLOC_SCRATCH_BYTES
+    assert L.basp_attn_bwd_noalloc(*p, 1, 131072, 64, 8, 128, 8, f, None) == WS
+    assert L.basp_attn_bwd_noalloc(*p[:5], None, *p[6:], 1, 4096, 8, 2, 128, 2, f, None) == NULL
+    assert L.basp_attn_bwd_noalloc(*p, 1, 4096, 8, 2, 72, 2, f, None) == UNSUP
+    assert L.basp_attn_bwd_noalloc(*p, 1, 4095, 8, 2, 128, 2, f, None) == SHAPE
+    assert L.basp_attn_bwd_noalloc(*([None] * 9), 0, 4096, 8, 2, 128, 2, f, None) == OK
