@@ -25,7 +25,7 @@ def lib():
         L.basp_peak_mfma_bf16.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_void_p,
                                           ctypes.c_void_p]
         L.basp_peak_copy.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
-                                     ctypes.c_int, ctypes.c_void_p]
+                                     ctypes.c_int, ctypes.c_int, ctypes.c_void_p]
         L.basp_peak_mfma_bf16.restype = ctypes.c_int
         L.basp_peak_copy.restype = ctypes.c_int
         _lib = L
@@ -62,18 +62,25 @@ def mfma_bf16_tflops(iters: int = 20000, reps: int = 5) -> float:
     return flops / (ms * 1e-3) / 1e12
 
 
-def copy_gbps(nbytes: int = 1 << 30, reps: int = 5) -> float:
-    """Median rate (bytes read + written) of a streaming copy of nbytes."""
+# Launch shapes tried by copy_gbps: (workgroups, vectors in flight per thread).
+COPY_SHAPES = ((8192, 4), (16384, 4), (32768, 4), (32768, 8), (8192, 8))
+
+
+def copy_gbps(nbytes: int = 1 << 30, reps: int = 5, shapes=COPY_SHAPES) -> float:
+    """Best over launch shapes of the median rate (bytes read + written) of a
+    streaming copy of nbytes."""
     src = torch.empty(nbytes // 4, dtype=torch.float32, device="cuda").fill_(1.0)
     dst = torch.empty_like(src)
-    cus = torch.cuda.get_device_properties(0).multi_processor_count
-    call = lambda: lib().basp_peak_copy(ctypes.c_void_p(src.data_ptr()),
-                                        ctypes.c_void_p(dst.data_ptr()), nbytes, cus * 8,
-                                        _stream())
-    assert call() == 0
-    ms = _time(call, reps)
-    ok = bool(torch.equal(src, dst))
+    best = 0.0
+    for blocks, unroll in shapes:
+        dst.zero_()
+        call = lambda: lib().basp_peak_copy(ctypes.c_void_p(src.data_ptr()),
+                                            ctypes.c_void_p(dst.data_ptr()), nbytes, blocks,
+                                            unroll, _stream())
+        assert call() == 0
+        ms = _time(call, reps)
+        if not bool(torch.equal(src, dst)):
+            raise RuntimeError("peak copy produced a wrong result")
+        best = max(best, 2.0 * nbytes / (ms * 1e-3) / 1e9)
     del src, dst
-    if not ok:
-        raise RuntimeError("peak copy produced a wrong result")
-    return 2.0 * nbytes / (ms * 1e-3) / 1e9
+    return best

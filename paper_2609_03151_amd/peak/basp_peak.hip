@@ -43,20 +43,30 @@ __global__ __launch_bounds__(512) void mfma_peak_kernel(int iters, float *__rest
 }
 
 constexpr int kCopyThreads = 256;
-constexpr int kCopyUnroll = 8;
 
+// Each pass of a workgroup moves 256*U consecutive 16-byte vectors (thread t
+// takes t, t + 256, ...: every load instruction of a wave is one contiguous
+// 1 KiB run); the workgroups then step over the buffer in passes of
+// gridDim.x*256*U vectors.  U vectors are in flight per thread.
+template <int U>
 __global__ __launch_bounds__(kCopyThreads) void copy_kernel(const u32x4 *__restrict__ src,
                                                             u32x4 *__restrict__ dst, size_t n16) {
-  const size_t stride = (size_t)gridDim.x * kCopyThreads;
-  size_t i = (size_t)blockIdx.x * kCopyThreads + threadIdx.x;
-  for (; i + (kCopyUnroll - 1) * stride < n16; i += kCopyUnroll * stride) {
-    u32x4 v[kCopyUnroll];
+  const size_t step = (size_t)gridDim.x * kCopyThreads * U;
+  for (size_t b0 = (size_t)blockIdx.x * kCopyThreads * U; b0 < n16; b0 += step) {
+    const size_t i0 = b0 + threadIdx.x;
+    if (b0 + (size_t)kCopyThreads * U <= n16) {
+      u32x4 v[U];
 #pragma unroll
-    for (int u = 0; u < kCopyUnroll; ++u) v[u] = __builtin_nontemporal_load(src + i + u * stride);
+      for (int u = 0; u < U; ++u) v[u] = __builtin_nontemporal_load(src + i0 + u * kCopyThreads);
 #pragma unroll
-    for (int u = 0; u < kCopyUnroll; ++u) __builtin_nontemporal_store(v[u], dst + i + u * stride);
+      for (int u = 0; u < U; ++u) __builtin_nontemporal_store(v[u], dst + i0 + u * kCopyThreads);
+    } else {
+      for (int u = 0; u < U; ++u) {
+        const size_t i = i0 + (size_t)u * kCopyThreads;
+        if (i < n16) __builtin_nontemporal_store(__builtin_nontemporal_load(src + i), dst + i);
+      }
+    }
   }
-  for (; i < n16; i += stride) __builtin_nontemporal_store(__builtin_nontemporal_load(src + i), dst + i);
 }
 
 }  // namespace
@@ -72,14 +82,23 @@ int basp_peak_mfma_bf16(int blocks, int iters, float *out, void *stream) {
   return hipGetLastError() == hipSuccess ? 0 : 7;
 }
 
-// dst[0, bytes) = src[0, bytes); both 16-byte aligned, bytes a multiple of 16.
-int basp_peak_copy(const void *src, void *dst, size_t bytes, int blocks, void *stream) {
+// dst[0, bytes) = src[0, bytes); both 16-byte aligned, bytes a multiple of 16;
+// `blocks` workgroups, `unroll` (4, 8 or 16) vectors in flight per thread.
+int basp_peak_copy(const void *src, void *dst, size_t bytes, int blocks, int unroll,
+                   void *stream) {
   if (!src || !dst || (bytes & 15) || ((uintptr_t)src & 15) || ((uintptr_t)dst & 15) ||
-      blocks < 1)
+      blocks < 1 || (unroll != 4 && unroll != 8 && unroll != 16))
     return 2;
   if (bytes == 0) return 0;
-  hipLaunchKernelGGL(copy_kernel, dim3(blocks), dim3(kCopyThreads), 0, (hipStream_t)stream,
-                     (const u32x4 *)src, (u32x4 *)dst, bytes / 16);
+  const hipStream_t st = (hipStream_t)stream;
+  const u32x4 *s = (const u32x4 *)src;
+  u32x4 *d = (u32x4 *)dst;
+  if (unroll == 4)
+    hipLaunchKernelGGL(copy_kernel<4>, dim3(blocks), dim3(kCopyThreads), 0, st, s, d, bytes / 16);
+  else if (unroll == 8)
+    hipLaunchKernelGGL(copy_kernel<8>, dim3(blocks), dim3(kCopyThreads), 0, st, s, d, bytes / 16);
+  else
+    hipLaunchKernelGGL(copy_kernel<16>, dim3(blocks), dim3(kCopyThreads), 0, st, s, d, bytes / 16);
   return hipGetLastError() == hipSuccess ? 0 : 7;
 }
 
