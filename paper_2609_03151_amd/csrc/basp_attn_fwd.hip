@@ -23,12 +23,18 @@
 //     in exactly the key order the accumulator holds P in.
 //   * K/V tiles of 64 keys are copied HBM -> LDS by buffer loads that write
 //     LDS directly (no register staging; rows past S arrive as zeros) into a
-//     ring of four stages, two tiles ahead of the one being consumed.  Tiles
-//     are stored row-major with an XOR swizzle that is conflict-free for both
-//     read patterns.  Each wave waits only for its own copies of the tile it
-//     needs next and then passes a fence-free barrier, so later tiles stay in
-//     flight.  The LDS operand reads are scheduled one step ahead of the
-//     MFMAs that consume them.
+//     ring of four stages.  Tiles are stored row-major with an XOR swizzle
+//     that is conflict-free for both read patterns.  Each wave waits only for
+//     its own copies of the tile it needs next, passes a fence-free barrier,
+//     and then issues the copies of the tile three ahead into the stage every
+//     wave has just finished with, so two later tiles stay in flight.
+//   * tiles left of the diagonal band are software-pipelined inside each
+//     wave: the score products of tile t+1 are issued between the
+//     exponentials of tile t, and the row sum of t and row maxima of t+1
+//     between the P V products of t, one product per slot with its operand
+//     read two slots ahead.  Every stretch of a wave's instruction stream
+//     thus mixes matrix and vector work; the arithmetic and its order per
+//     tile are unchanged (bit-identical results).
 //   * the running maximum used as the exponent reference only moves when a
 //     row's maximum grows by more than 8 (in log2 units): P <= 2^8 stays exact
 //     in bf16's relative precision and O is rescaled only on those tiles.
@@ -36,8 +42,9 @@
 //     any masking code; band tiles are masked, and a wave skips band tiles
 //     past its last row.  The grid is one-dimensional, heaviest query tiles
 //     first, heads fastest, so heads sharing a kv head run side by side.
-//   * a wave raises its issue priority over the score products, so the two
-//     waves of a SIMD drift apart: one's softmax overlaps the other's MFMAs.
+//   * in the diagonal band a wave raises its issue priority over the score
+//     products, so the two waves of a SIMD drift apart: one's softmax
+//     overlaps the other's MFMAs.
 //   * tensors are read and written through row views: the local
 //     head-sharded tensors, or (SH) the G sequence shards of the exchange in
 //     place, whose row counts are multiples of 256 so that a workgroup's
@@ -57,10 +64,11 @@ constexpr int kThreads = 512;
 constexpr int kWaves = 8;
 constexpr int kBM = 32 * kWaves;   // query rows per workgroup
 constexpr int kStages = 4;
-constexpr int kPD = 2;            // tiles prefetched ahead
+constexpr int kPD = 2;            // tiles in flight behind the one being read
 constexpr int kBN = 64;           // keys per tile
 constexpr float kRescaleSlack = 8.f;  // log2 headroom before the reference max moves
 // Instruction classes of __builtin_amdgcn_sched_group_barrier.
+constexpr int kSchedValu = 0x002;
 constexpr int kSchedMfma = 0x008;
 constexpr int kSchedDsRead = 0x100;
 
@@ -194,7 +202,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
     for (int r = 0; r < 16; ++r) oacc[n][r] = 0.f;
   float m_ref = -INFINITY, l_run = 0.f;
 
-  for (int t = 0; t < kPD && t < nt; ++t) load_tile(t);
+  for (int t = 0; t <= kPD && t < nt; ++t) load_tile(t);
 
   // One tile: scores, softmax update, P V.  MASK only for tiles that can
   // hold keys past some row of the workgroup (the diagonal band).
@@ -296,20 +304,203 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
     }
     __builtin_amdgcn_sched_group_barrier(kSchedMfma, 2, 0);
   };
-  auto step = [&](int t) {
-    // Stage (t+kPD) % 4 last held tile t-2, finished before this wave passed
-    // the barrier of iteration t-1.
-    if (t + kPD < nt) load_tile(t + kPD);
-    wait_tile(min(kPD, nt - 1 - t));
+  // Ring discipline: tiles 0 .. kPD are issued up front, then iteration t
+  // (of either loop below) issues tile t + kPD + 1 into the stage of tile
+  // t - 1, after a barrier that every wave passes only once it has finished
+  // with tile t - 1.  Before the barrier a wave waits for its own copies of
+  // the tile it is about to read, with `ahead` later tiles left in flight.
+  auto make_visible = [&](int ahead, int issue) __attribute__((always_inline)) {
+    wait_tile(ahead);
     barrier_no_fence();
+    if (issue < nt) load_tile(issue);
   };
-  const int t_mask = min(nt, q0 / kBN);  // tiles before t_mask need no mask
-  for (int t = 0; t < t_mask; ++t) {
-    step(t);
-    tile(t, std::false_type{});
+
+  // Tiles before t_mask need no mask.  They run software-pipelined: while
+  // the softmax of tile t (exponentials, conversions, row sum) is computed,
+  // the score products of tile t+1 are issued, and while P V of tile t runs,
+  // the row maxima of tile t+1 are formed, so that every stretch of the
+  // wave's instruction stream mixes matrix and vector work.  The arithmetic
+  // and its order per tile are those of `tile`: bit-identical results.
+  const int t_mask = min(nt, q0 / kBN);
+  auto scores = [&](int t, f32x16 (&sc)[2]) __attribute__((always_inline)) {
+    const unsigned char *Ks = smem + (t % kStages) * C::STAGE_BYTES;
+#pragma unroll
+    for (int m = 0; m < 2; ++m) {
+      const bf16x8 a = *reinterpret_cast<const bf16x8 *>(Ks + k_off[0] + m * 32 * T::ROW_BYTES);
+      sc[m] = mfma32x32x16(a, qf[0], f32x16{});
+    }
+#pragma unroll
+    for (int s2 = 1; s2 < C::NS; ++s2)
+#pragma unroll
+      for (int m = 0; m < 2; ++m) {
+        const bf16x8 a = *reinterpret_cast<const bf16x8 *>(Ks + k_off[s2] + m * 32 * T::ROW_BYTES);
+        sc[m] = mfma32x32x16(a, qf[s2], sc[m]);
+      }
+  };
+  auto row_max = [&](const f32x16 (&sc)[2]) __attribute__((always_inline)) {
+    float mx = -INFINITY;
+#pragma unroll
+    for (int m = 0; m < 2; ++m)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sc[m][r]);
+    return pair_max(mx) * c;
+  };
+  auto move_reference = [&](float mx) __attribute__((always_inline)) {
+    const bool grow = mx > m_ref + kRescaleSlack;
+    if (__builtin_amdgcn_ballot_w64(grow)) {  // wave-uniform, rare after the first tiles
+      asm volatile("" ::: "memory");
+      const float m_new = grow ? mx : m_ref;
+      const float alpha = fast_exp2(m_ref - m_new);
+      m_ref = m_new;
+      l_run *= alpha;
+#pragma unroll
+      for (int n = 0; n < C::NE; ++n)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) oacc[n][r] *= alpha;
+    }
+  };
+  auto exps = [&](f32x16 (&sc)[2], bf16x8 (&pf)[kBN / 16]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int m = 0; m < 2; ++m)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) sc[m][r] = fast_exp2(fmaf(sc[m][r], c, -m_ref));
+#pragma unroll
+    for (int s2 = 0; s2 < kBN / 16; ++s2) {
+      const int m = s2 >> 1, b8 = (s2 & 1) * 8;
+      pf[s2] = as_bf16x8(u32x4{pack_bf16x2(sc[m][b8 + 0], sc[m][b8 + 1]),
+                               pack_bf16x2(sc[m][b8 + 2], sc[m][b8 + 3]),
+                               pack_bf16x2(sc[m][b8 + 4], sc[m][b8 + 5]),
+                               pack_bf16x2(sc[m][b8 + 6], sc[m][b8 + 7])});
+    }
+  };
+  auto row_sum = [&](const f32x16 (&sc)[2]) __attribute__((always_inline)) {
+    float psum = 0.f;
+#pragma unroll
+    for (int m = 0; m < 2; ++m)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) psum += sc[m][r];
+    l_run += psum;
+  };
+  auto pv = [&](int t, const bf16x8 (&pf)[kBN / 16]) __attribute__((always_inline)) {
+    const unsigned char *Vs = smem + (t % kStages) * C::STAGE_BYTES + C::TILE_BYTES;
+#pragma unroll
+    for (int n = 0; n < C::NE; ++n)
+#pragma unroll
+      for (int s2 = 0; s2 < kBN / 16; ++s2) {
+        const bf16x8 a = tr_operand(Vs, v_off[n][0] + s2 * 16 * T::ROW_BYTES,
+                                    v_off[n][1] + s2 * 16 * T::ROW_BYTES);
+        oacc[n] = mfma32x32x16(a, pf[s2], oacc[n]);
+      }
+  };
+  // Iteration t of the pipelined loop, tile t+1 unmasked: `cur` holds the
+  // scores of tile t (reference already moved for them); the scores of tile
+  // t+1 go to `nxt`.  Each block is a sequence of slots of one product each,
+  // fenced by scheduling barriers: the slot's share of the vector work, and
+  // the operand read for the product kPf slots later.
+  constexpr int kPf = 2;
+  auto pipelined = [&](int t, f32x16 (&cur)[2], f32x16 (&nxt)[2]) __attribute__((always_inline)) {
+    make_visible(min(1, nt - 2 - t), t + kPD + 1);  // tile t+1 readable, t+2 in flight
+    asm volatile("" : "+v"(m_ref));  // keep the exponent arguments here
+    bf16x8 pf[kBN / 16];
+    // Block X: scores of tile t+1 (16 products), exponentials of tile t.
+    {
+      constexpr int NG = 2 * C::NS;
+      const unsigned char *Ks = smem + ((t + 1) % kStages) * C::STAGE_BYTES;
+      bf16x8 op[NG];
+      auto read = [&](int g) __attribute__((always_inline)) {
+        op[g] = *reinterpret_cast<const bf16x8 *>(Ks + k_off[g / 2] + (g % 2) * 32 * T::ROW_BYTES);
+      };
+#pragma unroll
+      for (int g = 0; g < kPf; ++g) read(g);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int g = 0; g < NG; ++g) {
+        if (g + kPf < NG) read(g + kPf);
+        const int m = g % 2, s2 = g / 2;
+        nxt[m] = mfma32x32x16(op[g], qf[s2], s2 == 0 ? f32x16{} : nxt[m]);
+        // 32 exponentials over the 16 slots; each full group of 8 converted
+#pragma unroll
+        for (int e = 32 * g / NG; e < 32 * (g + 1) / NG; ++e) {
+          const int mm = e / 16, r = e % 16;
+          cur[mm][r] = fast_exp2(fmaf(cur[mm][r], c, -m_ref));
+          if (r % 8 == 7) {
+            const int b8 = r - 7;
+            pf[2 * mm + b8 / 8] = as_bf16x8(u32x4{pack_bf16x2(cur[mm][b8 + 0], cur[mm][b8 + 1]),
+                                                  pack_bf16x2(cur[mm][b8 + 2], cur[mm][b8 + 3]),
+                                                  pack_bf16x2(cur[mm][b8 + 4], cur[mm][b8 + 5]),
+                                                  pack_bf16x2(cur[mm][b8 + 6], cur[mm][b8 + 7])});
+          }
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+    // Block Y: P V of tile t (16 products), row sum of t, row maxima of t+1.
+    float psum = 0.f, mx = -INFINITY;
+    {
+      constexpr int NG = C::NE * (kBN / 16);
+      const unsigned char *Vs = smem + (t % kStages) * C::STAGE_BYTES + C::TILE_BYTES;
+      bf16x8 op[NG];
+      auto read = [&](int g) __attribute__((always_inline)) {
+        const int n = g / (kBN / 16), s2 = g % (kBN / 16);
+        op[g] = tr_operand(Vs, v_off[n][0] + s2 * 16 * T::ROW_BYTES,
+                           v_off[n][1] + s2 * 16 * T::ROW_BYTES);
+      };
+#pragma unroll
+      for (int g = 0; g < kPf; ++g) read(g);
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int g = 0; g < NG; ++g) {
+        if (g + kPf < NG) read(g + kPf);
+        const int n = g / (kBN / 16), s2 = g % (kBN / 16);
+        oacc[n] = mfma32x32x16(op[g], pf[s2], oacc[n]);
+#pragma unroll
+        for (int e = 32 * g / NG; e < 32 * (g + 1) / NG; ++e) psum += cur[e / 16][e % 16];
+#pragma unroll
+        for (int e = 32 * g / NG; e < 32 * (g + 1) / NG; ++e) mx = fmaxf(mx, nxt[e / 16][e % 16]);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+    l_run += psum;
+    move_reference(pair_max(mx) * c);  // after P V of tile t, before the exponentials of t+1
+  };
+  // The last unmasked tile t: no scores to start.
+  auto pipelined_last = [&](int t, f32x16 (&cur)[2]) __attribute__((always_inline)) {
+    make_visible(min(1, nt - 2 - t), t + kPD + 1);  // tile t+1 (the first masked one)
+    asm volatile("" : "+v"(m_ref));
+    bf16x8 pf[kBN / 16];
+    exps(cur, pf);
+    __builtin_amdgcn_sched_barrier(0);
+    pv(t, pf);
+    row_sum(cur);
+    __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 4, 0);
+#pragma unroll
+    for (int i = 0; i < C::NE * (kBN / 16) - 2; ++i) {
+      __builtin_amdgcn_sched_group_barrier(kSchedMfma, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(kSchedDsRead, 2, 0);
+      __builtin_amdgcn_sched_group_barrier(kSchedValu, 2, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(kSchedMfma, 2, 0);
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  if (t_mask > 0) {
+    f32x16 sa[2], sb[2];
+    make_visible(min(kPD, nt - 1), nt);  // tile 0; tile kPD + 1 is issued by iteration 0
+    scores(0, sa);
+    move_reference(row_max(sa));
+    int t = 0;
+    for (; t + 2 < t_mask; t += 2) {
+      pipelined(t, sa, sb);
+      pipelined(t + 1, sb, sa);
+    }
+    if (t + 1 < t_mask) {
+      pipelined(t, sa, sb);
+      pipelined_last(t + 1, sb);
+    } else {
+      pipelined_last(t, sa);
+    }
   }
-  for (int t = t_mask; t < nt; ++t) {
-    step(t);
+  for (int t = t_mask; t < nt; ++t) {  // the diagonal band, masked
+    make_visible(min(kPD, nt - 1 - t), t + kPD + 1);
     if (t * kBN <= wrow0 + 31) tile(t, std::true_type{});  // wave-uniform
   }
 

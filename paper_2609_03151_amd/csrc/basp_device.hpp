@@ -147,18 +147,22 @@ __device__ __forceinline__ void wait_vmcnt() {
 
 // ------------------------------------------------------------- LDS tiles
 // A [rows][D] bf16 tile stored row-major without padding, its 16-byte chunks
-// permuted by an XOR of the row.  The permutation makes both access patterns
-// of the attention kernels free of bank conflicts:
-//   * 16 lanes reading one chunk of 16 consecutive rows (MFMA operand rows);
-//   * ds_read_b64_tr_b16 over 4 consecutive rows starting at a multiple of 4,
-//     each lane group touching two adjacent chunks (even first) of every row.
+// permuted by an XOR of the row (a key that depends on the row modulo 16).
+// With LDS serving 256 bytes per cycle, the permutation makes both access
+// patterns of the attention kernels free of bank conflicts:
+//   * 16 lanes reading one chunk of 16 consecutive rows (MFMA operand rows):
+//     the key is a bijection on the 16 rows;
+//   * 32 lanes of ds_read_b64_tr_b16 reading 4 consecutive rows, starting at
+//     a multiple of 4, at 4 consecutive chunks starting at a multiple of 4:
+//     the keys of those rows differ in their upper bits, so the 16 chunk
+//     slots they touch are distinct.
 template <int D>
 struct LdsTile;
 
 template <>
 struct LdsTile<128> {
   static constexpr int ROW_BYTES = 256;
-  __device__ static __forceinline__ int swz(int r) { return ((r & 7) << 1) | ((r >> 3) & 1); }
+  __device__ static __forceinline__ int swz(int r) { return ((r & 3) << 2) | ((r >> 2) & 3); }
   __device__ static __forceinline__ int off(int r, int chunk) {
     return r * ROW_BYTES + ((chunk ^ swz(r)) << 4);
   }
@@ -168,7 +172,7 @@ template <>
 struct LdsTile<64> {
   static constexpr int ROW_BYTES = 128;
   __device__ static __forceinline__ int swz(int r) {
-    return (((r >> 1) & 3) << 1) | ((r >> 3) & 1);
+    return (((r >> 1) & 1) << 2) | ((r >> 2) & 3);
   }
   __device__ static __forceinline__ int off(int r, int chunk) {
     return r * ROW_BYTES + ((chunk ^ swz(r)) << 4);
