@@ -301,11 +301,26 @@ int basp_attn_bwd_noalloc(const void *q, const void *k, const void *v,
  * Q) and dQ, dK, dV (fp32) are written into the rank's head slices of their
  * G shard buffers ([b, S/G, H, d] for dQ, [b, S/G, H_kv, d] for dK and dV);
  * other heads are untouched.  The result is bit for bit that of basp_pack
- * (of dO), basp_attn_bwd and basp_unpack of each gradient.  lse and the
- * workspace (same size as basp_attn_bwd's) as there.
- * Errors: as basp_attn_fwd_sharded, plus WORKSPACE, and UNSUPPORTED when
- * H_kv < G (members sharing a kv head would overwrite each other's partial
- * gradients: use basp_attn_bwd and basp_unpack_add). */
+ * (of dO), basp_attn_bwd and basp_unpack of each gradient.  lse as there;
+ * workspace of basp_attn_bwd_sharded_workspace_bytes(), 16-byte aligned
+ * (the rank's heads of Q and dO are first packed into it: the key pass
+ * streams those rows many times, and local rows stream faster than rows a
+ * whole shard row apart).
+ * With a kv head shared by G/H_kv members (H_kv < G, Sec. II-A GQA under the
+ * head split of Sec. II-C) each member holds only a partial dK, dV of that
+ * head, which the reverse exchange must sum: dk_shards and dv_shards are
+ * then G send blocks, block j [b, S/G, 1, d] receiving this member's partial
+ * gradient of member j's tokens (bit for bit rows j*S/G .. of basp_attn_bwd's
+ * dk, dv); member j sums the blocks of the sharing members in member order
+ * (basp_a2a_unpack does this).
+ * Errors: as basp_attn_fwd_sharded, plus WORKSPACE. */
+/* Bytes of device workspace basp_attn_bwd_sharded needs: local copies of
+ * the rank's heads of Q and dO (each [b, S, H/G, d] bf16, rounded up to 256
+ * bytes), then basp_attn_bwd_workspace_bytes().  0 for an invalid or empty
+ * shape. */
+size_t basp_attn_bwd_sharded_workspace_bytes(int b, int S, int H, int H_kv,
+                                             int d, int G);
+
 int basp_attn_bwd_sharded(const void *const *q_shards,
                           const void *const *k_shards,
                           const void *const *v_shards,

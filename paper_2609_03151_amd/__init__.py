@@ -29,7 +29,8 @@ STATUS = {
 EXPORTS = ("basp_status_str", "basp_group_of", "basp_validate", "basp_pack",
            "basp_unpack", "basp_unpack_add", "basp_pack_qkv", "basp_unpack_grads", "basp_a2a_pack", "basp_a2a_unpack", "basp_attn_fwd",
            "basp_attn_fwd_sharded", "basp_attn_bwd_workspace_bytes", "basp_attn_bwd",
-           "basp_attn_bwd_noalloc", "basp_attn_bwd_sharded")
+           "basp_attn_bwd_noalloc", "basp_attn_bwd_sharded_workspace_bytes",
+           "basp_attn_bwd_sharded")
 # Bytes of the static device buffer basp_attn_bwd_noalloc works in.
 NOALLOC_SCRATCH_BYTES = 128 << 20
 
@@ -69,6 +70,8 @@ def lib() -> ctypes.CDLL:
     L.basp_attn_fwd.argtypes = [vp] * 5 + [i] * 6 + [f, vp]
     L.basp_attn_bwd_workspace_bytes.argtypes = [i] * 6
     L.basp_attn_bwd_workspace_bytes.restype = sz
+    L.basp_attn_bwd_sharded_workspace_bytes.argtypes = [i] * 6
+    L.basp_attn_bwd_sharded_workspace_bytes.restype = sz
     L.basp_attn_bwd.argtypes = [vp] * 10 + [sz] + [i] * 6 + [f, vp]
     L.basp_attn_bwd_noalloc.argtypes = [vp] * 9 + [i] * 6 + [f, vp]
     tab = ctypes.POINTER(vp)
@@ -280,6 +283,10 @@ def attn_bwd_workspace_bytes(b, S, H, H_kv, d, G) -> int:
     return int(lib().basp_attn_bwd_workspace_bytes(b, S, H, H_kv, d, G))
 
 
+def attn_bwd_sharded_workspace_bytes(b, S, H, H_kv, d, G) -> int:
+    return int(lib().basp_attn_bwd_sharded_workspace_bytes(b, S, H, H_kv, d, G))
+
+
 def attn_bwd(q, k, v, o, lse, do, G: int = 1, scale: float | None = None,
              dq=None, dk=None, dv=None, workspace=None, H_kv: int | None = None):
     """Backward of attn_fwd: returns (dq, dk, dv) in fp32."""
@@ -351,13 +358,15 @@ def attn_bwd_sharded(q_shards, k_shards, v_shards, o_shards, lse, do_shards, dq_
                      dk_shards, dv_shards, rank: int, scale: float | None = None,
                      workspace=None):
     """Backward of attn_fwd_sharded: dQ, dK, dV (fp32) into the rank's head
-    slices of their shard buffers."""
+    slices of their shard buffers.  With a shared kv head (H_kv < G),
+    dk_shards / dv_shards are the G send blocks [b, S/G, 1, d] of this
+    member's partial dK, dV instead."""
     G = len(q_shards)
     b, Sg, H, d = q_shards[0].shape
     H_kv = k_shards[0].shape[2]
     S = Sg * G
     scale = d ** -0.5 if scale is None else scale
-    need = attn_bwd_workspace_bytes(b, S, H, H_kv, d, G)
+    need = attn_bwd_sharded_workspace_bytes(b, S, H, H_kv, d, G)
     if workspace is None:
         workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=lse.device)
     bf, f32 = torch.bfloat16, torch.float32

@@ -249,6 +249,12 @@ int check_shard_table(const void *const *tab, int G) {
   return BASP_OK;
 }
 
+// Bytes of one local [b, S, H/G, d] bf16 copy inside the in-place
+// backward's workspace, rounded up to 256.
+size_t local_copy_bytes(const basp::AttnShape &s) {
+  return ((size_t)s.b * s.S * s.Hl * s.d * 2 + 255) & ~(size_t)255;
+}
+
 }  // namespace
 
 namespace basp {
@@ -425,6 +431,13 @@ size_t basp_attn_bwd_workspace_bytes(int b, int S, int H, int H_kv, int d, int G
   return basp::attn_bwd_workspace_bytes(s);
 }
 
+size_t basp_attn_bwd_sharded_workspace_bytes(int b, int S, int H, int H_kv, int d, int G) {
+  if (check_share(b, S, H, H_kv, d, G) != BASP_OK) return 0;
+  basp::AttnShape s = attn_shape(b, S, H, H_kv, d, G, 1.f);
+  if ((long long)b * S == 0) return 0;
+  return 2 * local_copy_bytes(s) + basp::attn_bwd_workspace_bytes(s);
+}
+
 }  // extern "C"
 
 namespace {
@@ -503,9 +516,12 @@ int basp_attn_bwd_sharded(const void *const *q_shards, const void *const *k_shar
   if (rc) return rc;
   rc = check_sharded(S, H, H_kv, d, G, rank);
   if (rc) return rc;
-  // A kv head shared by several members gets a partial gradient from each;
-  // written in place, the members would overwrite one another.
-  if (H_kv < G) return BASP_ERR_UNSUPPORTED;
+  // A kv head shared by several members gets a partial gradient from each:
+  // dK and dV then go to G send blocks [b, S/G, 1, d], one per destination
+  // member, whose receiver sums them (basp_a2a_unpack), instead of the head
+  // slices of the shard buffers, where the members would overwrite one
+  // another.
+  const bool shared_kv = H_kv < G;
   if ((long long)b * S == 0) return BASP_OK;  // empty: no pointer is inspected
   using Tab = const void *const *;
   for (Tab t : {q_shards, k_shards, v_shards, o_shards, do_shards, (Tab)dq_shards,
@@ -514,22 +530,42 @@ int basp_attn_bwd_sharded(const void *const *q_shards, const void *const *k_shar
   if (!lse) return BASP_ERR_NULL;
   if (!aligned(lse, 4)) return BASP_ERR_ALIGN;
   basp::AttnShape s = attn_shape(b, S, H, H_kv, d, G, scale);
-  const size_t need = basp::attn_bwd_workspace_bytes(s);
+  const size_t copy = local_copy_bytes(s);
+  const size_t need = 2 * copy + basp::attn_bwd_workspace_bytes(s);
   if (workspace_bytes < need) return BASP_ERR_WORKSPACE;
   if (!workspace) return BASP_ERR_NULL;
   if (!aligned(workspace, 16)) return BASP_ERR_ALIGN;
+  // Q and dO rows are streamed once per key tile by the key-stationary pass;
+  // read from the shards, rows sit the whole shard row (all H heads) apart
+  // and stream measurably slower than from a local copy.  So the rank's
+  // heads of Q and dO are first packed into the workspace (one launch), and
+  // the kernels read those copies; everything else is read and written in
+  // place.
+  char *ws = static_cast<char *>(workspace);
+  void *q_loc = ws, *do_loc = ws + copy;
+  basp::PermCall pc[2];
+  bool empty = false;
+  rc = prep_pack(true, false, q_shards, q_loc, b, S, H, d, G, rank, BASP_BF16, &pc[0], &empty);
+  if (!rc) rc = prep_pack(true, false, do_shards, do_loc, b, S, H, d, G, rank, BASP_BF16, &pc[1],
+                          &empty);
+  if (rc) return rc;
+  (void)hipGetLastError();
+  rc = hip_status(basp::launch_permute_batch(pc, 2, (hipStream_t)stream));
+  if (rc) return rc;
   using basp::shard_view;
-  const basp::RowView qv = shard_view(q_shards, G, S, H, d, rank),
+  const basp::RowView qv = basp::local_view(q_loc, S, s.Hl, d),
                       kv = shard_view(k_shards, G, S, H_kv, d, rank),
                       vv = shard_view(v_shards, G, S, H_kv, d, rank),
                       ov = shard_view(o_shards, G, S, H, d, rank),
-                      dov = shard_view(do_shards, G, S, H, d, rank),
+                      dov = basp::local_view(do_loc, S, s.Hl, d),
                       dqv = shard_view((Tab)dq_shards, G, S, H, d, rank),
-                      dkv = shard_view((Tab)dk_shards, G, S, H_kv, d, rank),
-                      dvv = shard_view((Tab)dv_shards, G, S, H_kv, d, rank);
+                      dkv = shared_kv ? shard_view((Tab)dk_shards, G, S, 1, d, 0)
+                                      : shard_view((Tab)dk_shards, G, S, H_kv, d, rank),
+                      dvv = shared_kv ? shard_view((Tab)dv_shards, G, S, 1, d, 0)
+                                      : shard_view((Tab)dv_shards, G, S, H_kv, d, rank);
   (void)hipGetLastError();
-  return hip_status(basp::launch_attn_bwd(qv, kv, vv, ov, lse, dov, dqv, dkv, dvv, workspace, s,
-                                          true, (hipStream_t)stream));
+  return hip_status(basp::launch_attn_bwd(qv, kv, vv, ov, lse, dov, dqv, dkv, dvv,
+                                          ws + 2 * copy, s, true, (hipStream_t)stream));
 }
 
 }  // extern "C"

@@ -36,7 +36,9 @@
 //   * Q, K, V, O, dO and the gradients are addressed through row views:
 //     the local head-sharded tensors, or (SH) the G sequence shards of the
 //     exchange in place (row counts multiples of 256: a workgroup's rows or
-//     keys, and every streamed tile, lie in one shard).
+//     keys, and every streamed tile, lie in one shard).  Q and dO, which the
+//     key-stationary pass streams once per key tile, are always local
+//     one-buffer views (the in-place entry point packs them first).
 #include <math.h>
 
 #include <type_traits>
@@ -86,7 +88,7 @@ __global__ __launch_bounds__(kPreThreads) void bwd_pre_kernel(
       const int beta = (int)(bi / S), i = (int)(bi - (long long)beta * S);
       uint32_t left;
       orow = view_row<true, const uint16_t>(ov, beta, i, h, D, left);
-      drow = view_row<true, const uint16_t>(dov, beta, i, h, D, left);
+      drow = view_row<false, const uint16_t>(dov, beta, i, h, D, left);
     } else {  // local [b][S][Hl][D]: row r is r*D elements in
       orow = static_cast<const uint16_t *>(ov.p[0]) + r * D;
       drow = static_cast<const uint16_t *>(dov.p[0]) + r * D;
@@ -251,9 +253,9 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
     int h, i0;
     step_coords(st, h, i0);
     uint32_t left;  // the step's rows; rows past the buffer's end read as zeros
-    const u32x4 rq = make_rsrc_words(view_row<SH, const uint16_t>(qv, beta, i0, h, D, left),
+    const u32x4 rq = make_rsrc_words(view_row<false, const uint16_t>(qv, beta, i0, h, D, left),
                                      left * q_row_bytes);
-    const u32x4 rd = make_rsrc_words(view_row<SH, const uint16_t>(dov, beta, i0, h, D, left),
+    const u32x4 rd = make_rsrc_words(view_row<false, const uint16_t>(dov, beta, i0, h, D, left),
                                      left * q_row_bytes);
     const uint32_t stage = smem_lds + (st % kStages) * C::STAGE_BYTES;
 #pragma unroll
@@ -556,9 +558,9 @@ __global__ __launch_bounds__(kDqThreads, 1) void bwd_dq_kernel(
   const uint32_t q_row_bytes = qv.row_elems * 2, kv_row_bytes = kv.row_elems * 2;
   uint32_t left;
   const rsrc_t rq =
-      make_rsrc(view_row<SH, const uint16_t>(qv, beta, q0, h, D, left), left * q_row_bytes);
+      make_rsrc(view_row<false, const uint16_t>(qv, beta, q0, h, D, left), left * q_row_bytes);
   const rsrc_t rd =
-      make_rsrc(view_row<SH, const uint16_t>(dov, beta, q0, h, D, left), left * q_row_bytes);
+      make_rsrc(view_row<false, const uint16_t>(dov, beta, q0, h, D, left), left * q_row_bytes);
   u32x4 rk = {}, rv = {};  // local K/V: one resource per head; sharded: one per shard
   if constexpr (!SH) {
     rk = make_rsrc_words(view_row<false, const uint16_t>(kv, beta, 0, kvh, D, left),

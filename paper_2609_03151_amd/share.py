@@ -23,13 +23,16 @@ buffers stand for the receive and send buffers of that exchange.
 
 `forward_sharded` / `backward_sharded` run the same step with no pack or
 unpack pass: attention reads the shard buffers in place and writes O, dQ,
-dK, dV straight into the send buffers (bit for bit the same results).
+dK, dV straight into the send buffers (bit for bit the same results); with a
+shared kv head, dK and dV go to one send block per member (`dk_send`,
+`dv_send`), each the member's partial gradient for that member's tokens.
 """
 from __future__ import annotations
 
 import torch
 
-from . import (attn_bwd, attn_bwd_sharded, attn_bwd_workspace_bytes, attn_fwd,
+from . import (attn_bwd, attn_bwd_sharded, attn_bwd_sharded_workspace_bytes,
+               attn_bwd_workspace_bytes, attn_fwd,
                attn_fwd_sharded, heads_per_member, pack, pack_qkv, unpack, unpack_add,
                unpack_grads)
 
@@ -64,7 +67,13 @@ class RankShare:
         self.dq_shards = [torch.zeros((b, Sg, H, d), dtype=f32, device=dev) for _ in range(G)]
         self.dk_shards = [torch.zeros((b, Sg, H_kv, d), dtype=f32, device=dev) for _ in range(G)]
         self.dv_shards = [torch.zeros((b, Sg, H_kv, d), dtype=f32, device=dev) for _ in range(G)]
-        ws = attn_bwd_workspace_bytes(b, S, H, H_kv, d, G)
+        # in-place backward with a shared kv head: the partial dK, dV go to
+        # one send block per member (the reverse exchange sums them)
+        if self.shared_kv:
+            self.dk_send = [torch.zeros((b, Sg, 1, d), dtype=f32, device=dev) for _ in range(G)]
+            self.dv_send = [torch.zeros((b, Sg, 1, d), dtype=f32, device=dev) for _ in range(G)]
+        ws = max(attn_bwd_workspace_bytes(b, S, H, H_kv, d, G),
+                 attn_bwd_sharded_workspace_bytes(b, S, H, H_kv, d, G))
         self.workspace = torch.empty(max(ws, 16), dtype=torch.uint8, device=dev)
 
     # individual steps, so that callers can time them
@@ -113,9 +122,11 @@ class RankShare:
                          scale=self.scale, lse=self.lse)
 
     def backward_sharded(self):
+        dk, dv = ((self.dk_send, self.dv_send) if self.shared_kv
+                  else (self.dk_shards, self.dv_shards))
         attn_bwd_sharded(self.q_shards, self.k_shards, self.v_shards, self.o_shards, self.lse,
-                         self.do_shards, self.dq_shards, self.dk_shards, self.dv_shards,
-                         self.rank, scale=self.scale, workspace=self.workspace)
+                         self.do_shards, self.dq_shards, dk, dv, self.rank, scale=self.scale,
+                         workspace=self.workspace)
 
     def step_sharded(self):
         self.forward_sharded()

@@ -250,7 +250,9 @@ int main() {
   EXPECT(basp_attn_fwd_sharded(tq, tk, tv, to, lse, 1, 4096, 8, 4, 128, 4, 3, 0.1f, nullptr),
          BASP_OK);
   CHECK(basp::g_sharded && basp::g_attn.Hl == 2 && basp::g_attn.Hkl == 1);
-  const size_t need_s = basp_attn_bwd_workspace_bytes(1, 4096, 8, 4, 128, 4);
+  const size_t need_s = basp_attn_bwd_sharded_workspace_bytes(1, 4096, 8, 4, 128, 4);
+  CHECK(need_s == basp_attn_bwd_workspace_bytes(1, 4096, 8, 4, 128, 4) + 2ull * 4096 * 2 * 128 * 2);
+  CHECK(basp_attn_bwd_sharded_workspace_bytes(0, 4096, 8, 4, 128, 4) == 0);
   EXPECT(basp_attn_bwd_sharded(tq, tk, tv, to, lse, td, (float *const *)tdq, (float *const *)tdk,
                                (float *const *)tdv, p[9], need_s - 16, 1, 4096, 8, 4, 128, 4, 1,
                                0.1f, nullptr),
@@ -259,6 +261,12 @@ int main() {
                                (float *const *)tdv, p[9], need_s, 1, 4096, 8, 4, 128, 4, 1, 0.1f,
                                nullptr),
          BASP_OK);
+  // a kv head shared by two members: partial dK, dV into send blocks, accepted
+  EXPECT(basp_attn_bwd_sharded(tq, tk, tv, to, lse, td, (float *const *)tdq, (float *const *)tdk,
+                               (float *const *)tdv, p[9], need_s, 1, 4096, 8, 2, 128, 4, 3, 0.1f,
+                               nullptr),
+         BASP_OK);
+  CHECK(basp::g_sharded && basp::g_attn.Hkl == 1 && basp::g_attn.Hl == 2);
   printf("abi ok %d\n", g_cases);
   return 0;
 }

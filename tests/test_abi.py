@@ -184,7 +184,8 @@ def test_sharded_attn_rejects_before_any_hip_call():
     assert fwd(0, 1024, 8, 2, 128, 4, 0) == OK                     # empty
     bwd = lambda *a, G=4, ws=_fake(0x80), n=1 << 30: L.basp_attn_bwd_sharded(
         *([tab(G)] * 4), _fake(0x40), *([tab(G)] * 4), ws, n, *a, f(0.1), None)
-    assert bwd(1, 1024, 8, 2, 128, 4, 1) == UNSUP                  # shared kv head (2 < 4)
+    assert bwd(1, 1024, 8, 2, 128, 4, 1, n=16) == WS               # shared kv head (2 < 4)
+    assert bwd(1, 1024, 8, 2, 128, 4, 1, ws=None) == NULL
     assert bwd(1, 1024, 8, 4, 128, 4, 1, n=16) == WS
     assert bwd(1, 1024, 8, 4, 128, 4, 1, ws=None) == NULL
     assert bwd(1, 1024, 8, 4, 128, 4, 9) == RANK

@@ -6,11 +6,13 @@ rank's head slices of the send buffers.
 * bit for bit the same as the composed path (pack -> attention -> unpack) at
   shapes covering one and several row chunks of the backward, b > 1, group
   sizes 2 to 16 (shard row counts that are not powers of two included), head
-  dims 64/80/96/128, and a kv head shared by several members (forward);
+  dims 64/80/96/128, and a kv head shared by several members (the partial
+  dK, dV then go to one send block per member);
 * other heads of the shard buffers untouched (sentinels);
 * one shape against the oracle's composition directly;
-* full size (the Llama-3-8B share, and the batch-agnostic share with b = 2,
-  G = 8): every output bit for bit against the composed path."""
+* full size (the Llama-3-8B share, the batch-agnostic share with b = 2,
+  G = 8, and the G = 16 share whose kv head two members share): every
+  output bit for bit against the composed path."""
 import math
 
 import numpy as np
@@ -74,18 +76,32 @@ def test_sharded_step_equals_composed_bitwise(b, S, H, H_kv, d, G, rank):
     _compare_shares(ref, got)
 
 
-def test_shared_kv_head_forward_and_refused_backward():
-    b, S, H, H_kv, d, G, rank = 1, 2048, 16, 4, 128, 8, 3
-    _, _, _, _, qs, ks, vs, ds = _inputs(b, S, H, H_kv, d, G, seed=5)
+SHARED = [  # b, S, H, H_kv, d, G, rank: a kv head shared by G / H_kv members
+    (1, 2048, 16, 4, 128, 8, 3),    # one row chunk
+    (2, 4096, 8, 2, 64, 4, 1),      # two row chunks, b = 2
+    (1, 4096, 16, 8, 96, 16, 9),    # G = 16, 2 members per kv head
+]
+
+
+@pytest.mark.parametrize("b,S,H,H_kv,d,G,rank", SHARED)
+def test_shared_kv_head_in_place(b, S, H, H_kv, d, G, rank):
+    """Forward in place as composed; the in-place backward writes the member's
+    partial dK, dV into G send blocks, bit for bit the rows of the composed
+    path's local dK, dV, and dQ into the shards as composed."""
+    log(f"[sharded shared kv] b={b} S={S} H={H} H_kv={H_kv} d={d} G={G} rank={rank}")
+    _, _, _, _, qs, ks, vs, ds = _inputs(b, S, H, H_kv, d, G, seed=5 + S + G)
     ref = RankShare(qs, ks, vs, ds, G=G, rank=rank)
-    ref.forward()
+    ref.step()
     got = RankShare(qs, ks, vs, ds, G=G, rank=rank)
-    got.forward_sharded()
+    got.step_sharded()
     torch.cuda.synchronize()
     _compare_shares(ref, got, grads=False)
-    with pytest.raises(basp.BaspError) as e:
-        got.backward_sharded()
-    assert e.value.status == 4
+    for j, (x, y) in enumerate(zip(ref.dq_shards, got.dq_shards)):
+        assert _same(x, y), f"dQ shard {j}"
+    Sg = S // G
+    for name, local, blocks in (("dK", ref.dk, got.dk_send), ("dV", ref.dv, got.dv_send)):
+        for j in range(G):
+            assert _same(blocks[j], local[:, j * Sg:(j + 1) * Sg].contiguous()), f"{name} block {j}"
 
 
 def test_other_heads_untouched():
@@ -130,7 +146,7 @@ def test_sharded_against_oracle():
             check_close(f"{name} shard {j}", got, ref_sh[j][:, :, rank * nl:(rank + 1) * nl])
 
 
-@pytest.mark.parametrize("name", ["llama3_8b_s32k", "ulysses_g8_b2_s64k"])
+@pytest.mark.parametrize("name", ["llama3_8b_s32k", "ulysses_g8_b2_s64k", "llama3_8b_g16_s64k"])
 def test_sharded_full_size_equals_composed(name):
     w = WORKLOADS[name]
     log(f"[sharded full] {name}")
@@ -141,6 +157,16 @@ def test_sharded_full_size_equals_composed(name):
     got = RankShare(*shards, G=w.G, rank=w.rank, scale=w.scale)
     got.step_sharded()
     torch.cuda.synchronize()
-    _compare_shares(ref, got)
+    if w.H_kv >= w.G:
+        _compare_shares(ref, got)
+    else:
+        _compare_shares(ref, got, grads=False)
+        for j, (x, y) in enumerate(zip(ref.dq_shards, got.dq_shards)):
+            assert _same(x, y), f"dQ shard {j}"
+        Sg = w.S // w.G
+        for name_, local, blocks in (("dK", ref.dk, got.dk_send), ("dV", ref.dv, got.dv_send)):
+            for j in range(w.G):
+                assert _same(blocks[j], local[:, j * Sg:(j + 1) * Sg].contiguous()), \
+                    f"{name_} block {j}"
     del ref, got, shards
     torch.cuda.empty_cache()

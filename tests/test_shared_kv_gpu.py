@@ -177,3 +177,49 @@ def test_whole_group_matches_global_oracle(b, S, H, H_kv, d, G):
             got = basp.a2a_unpack(recv, n_heads=H_kv)
             torch.cuda.synchronize()
             assert torch.equal(got, ref_sh[r]), r
+
+
+IN_PLACE_GROUP = [  # b, S, H, H_kv, d, G  (S/G a multiple of 256)
+    (1, 2048, 8, 2, 128, 4),
+    (2, 2048, 16, 4, 64, 8),
+]
+
+
+@pytest.mark.parametrize("b,S,H,H_kv,d,G", IN_PLACE_GROUP)
+def test_whole_group_in_place_matches_global_oracle(b, S, H, H_kv, d, G):
+    """Every member runs attention in place on the shard buffers; the members
+    sharing a kv head write their partial dK, dV into send blocks, and each
+    owner sums the blocks it receives (a2a_unpack, member order).  The
+    assembled O, dQ, dK, dV equal the oracle's attention of the global
+    tensors."""
+    log(f"[shared kv group in place] b={b} S={S} H={H} H_kv={H_kv} d={d} G={G}")
+    g = torch.Generator().manual_seed(3 * S + H + G)
+    mk = lambda n: torch.randn(b, S, n, d, generator=g).to(torch.bfloat16)
+    q, k, v, do = mk(H), mk(H_kv), mk(H_kv), mk(H)
+    c = 1.0 / math.sqrt(d)
+    Sg = S // G
+    sh = lambda x: [x[:, j * Sg:(j + 1) * Sg].contiguous().cuda() for j in range(G)]
+    qs, ks, vs, ds = sh(q), sh(k), sh(v), sh(do)
+    o_sh = [torch.zeros(b, Sg, H, d, dtype=torch.bfloat16, device="cuda") for _ in range(G)]
+    dq_sh = [torch.zeros(b, Sg, H, d, device="cuda") for _ in range(G)]
+    sends_k, sends_v = [], []
+    for l in range(G):
+        lse = basp.attn_fwd_sharded(qs, ks, vs, o_sh, l, scale=c)
+        dk_send = [torch.empty(b, Sg, 1, d, device="cuda") for _ in range(G)]
+        dv_send = [torch.empty(b, Sg, 1, d, device="cuda") for _ in range(G)]
+        basp.attn_bwd_sharded(qs, ks, vs, o_sh, lse, ds, dq_sh, dk_send, dv_send, l, scale=c)
+        sends_k.append(dk_send)
+        sends_v.append(dv_send)
+    dk_own, dv_own = [], []
+    for r in range(G):   # the exchange: owner r receives block r of every member
+        for sends, out in ((sends_k, dk_own), (sends_v, dv_own)):
+            recv = torch.stack([sends[l][r] for l in range(G)]).contiguous()
+            out.append(basp.a2a_unpack(recv, n_heads=H_kv))
+    torch.cuda.synchronize()
+    ro, rl = oracle.attn_fwd(q, k, v, c)
+    rdq, rdk, rdv = oracle.attn_bwd(q, k, v, do, ro, rl, c)
+    cat = lambda xs: torch.cat(xs, dim=1).double().cpu().numpy()
+    check_close("O", cat(o_sh), ro)
+    check_close("dQ", cat(dq_sh), rdq)
+    check_close("dK", cat(dk_own), rdk)
+    check_close("dV", cat(dv_own), rdv)
