@@ -251,16 +251,21 @@ def cold_permutation_rates(sh, reps: int = 5):
     send_k = basp.a2a_pack(own_k, G)
     own_dq = torch.empty(sh.dq_shards[r].shape, dtype=torch.float32, device="cuda")
     recv_dq = basp.a2a_pack(own_dq.zero_(), G)
+    # an fp32 dO shard sent as bf16 (the cast fused into the send-side split)
+    own_do32 = sh.do_shards[r].float()
+    send_do16 = basp.a2a_pack_bf16(own_do32, G)
     two = lambda t: 2 * t.numel() * t.element_size()
     a2a = {
         "a2a_pack_q": (cold(lambda: basp.a2a_pack(own_q, G, out=send_q)), two(own_q)),
         "a2a_pack_k": (cold(lambda: basp.a2a_pack(own_k, G, out=send_k)), two(own_k)),
         "a2a_unpack_o": (cold(lambda: basp.a2a_unpack(send_q, out=sh.o_shards[r])), two(own_q)),
         "a2a_unpack_dq": (cold(lambda: basp.a2a_unpack(recv_dq, out=own_dq)), two(own_dq)),
+        "a2a_pack_bf16_do": (cold(lambda: basp.a2a_pack_bf16(own_do32, G, out=send_do16)),
+                             6 * own_do32.numel()),
     }
     total_ms = sum(t for t, _ in per.values())
     total_bytes = sum(b for _, b in per.values())
-    del scratch, send_q, send_k, own_dq, recv_dq
+    del scratch, send_q, send_k, own_dq, recv_dq, own_do32, send_do16
     return {
         "pack_unpack_cold_gbps": round(total_bytes / (total_ms * 1e-3) / 1e9, 1),
         "pack_unpack_cold_gbps_by_call": {n: round(b / (t * 1e-3) / 1e9, 1) for n, (t, b) in per.items()},

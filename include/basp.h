@@ -21,6 +21,8 @@
  *                  the shard buffers of the exchange (no pack/unpack pass)
  *   basp_a2a_pack / basp_a2a_unpack   the owner's side of the same exchanges:
  *                  own shard <-> one contiguous block per member
+ *   basp_a2a_pack_bf16  the send side for an fp32 tensor, cast to bf16
+ *   basp_attn_bwd_noalloc  the backward with a static device workspace
  *
  * The exchange itself (RCCL) is not part of this library.
  *
@@ -201,6 +203,20 @@ int basp_a2a_pack(const void *own, void *send, int b, int S, int n_heads, int d,
  * with n < G. */
 int basp_a2a_unpack(const void *recv, void *own, int b, int S, int n_heads, int d,
                     int G, basp_dtype dtype, void *stream);
+
+/* basp_a2a_pack of an fp32 tensor with the conversion to bf16 fused, so that
+ * a gradient kept in fp32 crosses the exchange at half the bytes (Sec. II-C:
+ * in the backward the sequence owner sends its dO shard through the same
+ * all-to-all as Q in the forward; mixed-precision training, Sec. V):
+ *   send[j][beta][t][h][e] = bf16(own[beta][t][j*n/G + h][e])
+ * bf16() rounds to nearest even (infinities stay infinite; NaN stays NaN).
+ * own: device [b, S/G, n, d] fp32, 4-byte aligned; send: device
+ * [G, b, S/G, n/G, d] bf16 (with n < G: [G, b, S/G, 1, d], block j holding
+ * head j*n/G), 2-byte aligned.  16/8-byte aligned pointers and row lengths
+ * that are multiples of 4 elements move 4 elements at a time.
+ * Errors: NULL, SHAPE and UNSUPPORTED as basp_a2a_pack, ALIGN, HIP. */
+int basp_a2a_pack_bf16(const float *own, void *send, int b, int S, int n_heads,
+                       int d, int G, void *stream);
 
 /* Causal GQA scaled dot-product attention (Sec. II-A) over the full sequence
  * for the rank's H/G query heads:

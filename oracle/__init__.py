@@ -56,6 +56,7 @@ def lib():
     L.oracle_unpack_add.argtypes = [vp, ctypes.POINTER(vp)] + [c_long] * 6
     L.oracle_a2a_pack.argtypes = [vp, vp] + [c_long] * 6
     L.oracle_a2a_unpack.argtypes = [vp, vp] + [c_long] * 6
+    L.oracle_a2a_pack_bf16.argtypes = [vp, vp] + [c_long] * 5
     L.oracle_attn_fwd.argtypes = [vp] * 5 + [c_long] * 5 + [c_double, c_long, c_long]
     L.oracle_attn_bwd.argtypes = [vp] * 9 + [c_long] * 5 + [c_double, c_long]
     L.oracle_attn_rows.argtypes = ([vp] * 4 + [c_long] * 5 + [c_double, c_long]
@@ -180,6 +181,19 @@ def a2a_pack(own, G: int) -> np.ndarray:
     out = np.empty((G, b, Sg, nl, d), dtype=src.dtype)
     rc = lib().oracle_a2a_pack(_ptr(src), _ptr(out), b, Sg * G, n, d, G, src.dtype.itemsize)
     _check(rc, "a2a_pack")
+    return out
+
+
+def a2a_pack_bf16(own, G: int) -> np.ndarray:
+    """fp32 own shard [b, S/G, n, d] -> bf16 bit patterns [G, b, S/G, n/G, d]
+    (uint16), each element rounded to nearest even."""
+    src = np.ascontiguousarray(own.detach().cpu().numpy() if hasattr(own, "detach") else own,
+                               dtype=np.float32)
+    b, Sg, n, d = src.shape
+    nl = n // G if n % G == 0 else (1 if (n < G and G % n == 0) else 0)
+    out = np.empty((G, b, Sg, nl, d), dtype=np.uint16)
+    rc = lib().oracle_a2a_pack_bf16(_ptr(src), _ptr(out), b, Sg * G, n, d, G)
+    _check(rc, "a2a_pack_bf16")
     return out
 
 

@@ -243,6 +243,38 @@ int oracle_a2a_unpack(const void *recv, void *own, long b, long S, long n,
   return ORC_OK;
 }
 
+/* fp32 -> bf16, round to nearest even: keep the upper 16 bits after adding
+ * half an ulp of the result, minus one when the kept part is even (so that a
+ * tie rounds to the even neighbour).  Infinities stay infinite and finite
+ * values too large for bf16 become infinite, as rounding defines; a NaN
+ * becomes the quiet NaN with the same sign. */
+static unsigned short bf16_rne(float x) {
+  unsigned int u;
+  memcpy(&u, &x, sizeof u);
+  if ((u & 0x7F800000u) == 0x7F800000u && (u & 0x007FFFFFu) != 0)
+    return (unsigned short)((u >> 16) | 0x0040u);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return (unsigned short)(u >> 16);
+}
+
+int oracle_a2a_pack_bf16(const float *own, unsigned short *send, long b, long S,
+                         long n, long d, long G) {
+  int rc = perm_args_ok(b, S, n, d, G, 0, 4);
+  if (rc) return rc;
+  if (!own || !send) return ORC_ERR_NULL;
+  long Sg = S / G, nl = heads_per_member(n, G);
+  for (long j = 0; j < G; ++j)
+    for (long beta = 0; beta < b; ++beta)
+      for (long t = 0; t < Sg; ++t)
+        for (long h = 0; h < nl; ++h)
+          for (long e = 0; e < d; ++e) {
+            long from = ((beta * Sg + t) * n + (first_head(n, G, j) + h)) * d + e;
+            long to = (((j * b + beta) * Sg + t) * nl + h) * d + e;
+            send[to] = bf16_rne(own[from]);
+          }
+  return ORC_OK;
+}
+
 /* ------------------------------------------------------------ attention */
 static double dot(const double *x, const double *y, long d) {
   double acc = 0.0;

@@ -69,6 +69,11 @@ int oracle_a2a_pack(const void *own, void *send, long b, long S, long n,
 int oracle_a2a_unpack(const void *recv, void *own, long b, long S, long n,
                       long d, long G, long elem);
 
+/* oracle_a2a_pack of an fp32 own shard with every element converted to bf16
+ * by round to nearest even (raw bf16 bit patterns out). */
+int oracle_a2a_pack_bf16(const float *own, unsigned short *send, long b, long S,
+                         long n, long d, long G);
+
 /* Causal scaled dot-product attention (Sec. II-A), local q head h reads local
  * kv head h / (Hl/Hkl).  Computes rows [r0, r1) of every (beta, h):
  *   o   [b, r1-r0, Hl, d],  lse [b, Hl, r1-r0].

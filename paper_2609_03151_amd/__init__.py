@@ -27,7 +27,8 @@ STATUS = {
 }
 # Every symbol include/basp.h declares.
 EXPORTS = ("basp_status_str", "basp_group_of", "basp_validate", "basp_pack",
-           "basp_unpack", "basp_unpack_add", "basp_pack_qkv", "basp_unpack_grads", "basp_a2a_pack", "basp_a2a_unpack", "basp_attn_fwd",
+           "basp_unpack", "basp_unpack_add", "basp_pack_qkv", "basp_unpack_grads", "basp_a2a_pack", "basp_a2a_unpack",
+           "basp_a2a_pack_bf16", "basp_attn_fwd",
            "basp_attn_fwd_sharded", "basp_attn_bwd_workspace_bytes", "basp_attn_bwd",
            "basp_attn_bwd_noalloc", "basp_attn_bwd_sharded_workspace_bytes",
            "basp_attn_bwd_sharded")
@@ -67,6 +68,7 @@ def lib() -> ctypes.CDLL:
     L.basp_unpack_grads.argtypes = [vp] * 3 + [ctypes.POINTER(vp)] * 3 + [i] * 7 + [vp]
     L.basp_a2a_pack.argtypes = [vp, vp] + [i] * 6 + [vp]
     L.basp_a2a_unpack.argtypes = [vp, vp] + [i] * 6 + [vp]
+    L.basp_a2a_pack_bf16.argtypes = [vp, vp] + [i] * 5 + [vp]
     L.basp_attn_fwd.argtypes = [vp] * 5 + [i] * 6 + [f, vp]
     L.basp_attn_bwd_workspace_bytes.argtypes = [i] * 6
     L.basp_attn_bwd_workspace_bytes.restype = sz
@@ -79,7 +81,8 @@ def lib() -> ctypes.CDLL:
     L.basp_attn_bwd_sharded.argtypes = ([tab] * 4 + [vp] + [tab] * 4 + [vp, sz] + [i] * 7
                                         + [f, vp])
     for name in ("basp_group_of", "basp_validate", "basp_pack", "basp_unpack",
-                 "basp_a2a_pack", "basp_a2a_unpack", "basp_attn_fwd", "basp_attn_bwd",
+                 "basp_a2a_pack", "basp_a2a_unpack", "basp_a2a_pack_bf16", "basp_attn_fwd",
+                 "basp_attn_bwd",
                  "basp_attn_bwd_noalloc"):
         getattr(L, name).restype = i
     _lib = L
@@ -225,6 +228,19 @@ def a2a_pack(own: torch.Tensor, G: int, out: torch.Tensor | None = None) -> torc
                           device=own.device)
     _check(lib().basp_a2a_pack(_dev(own, "own"), _dev(out, "out", own.dtype), b, Sg * G, n, d,
                                G, _dtype_code(own), _stream(own)), "basp_a2a_pack")
+    return out
+
+
+def a2a_pack_bf16(own: torch.Tensor, G: int, out: torch.Tensor | None = None) -> torch.Tensor:
+    """fp32 own shard [b, S/G, n, d] -> bf16 send buffer [G, b, S/G, nl, d]
+    (a2a_pack with the conversion to bf16, round to nearest even, fused)."""
+    b, Sg, n, d = own.shape
+    if out is None:
+        out = torch.empty((G, b, Sg, heads_per_member(n, G), d), dtype=torch.bfloat16,
+                          device=own.device)
+    _check(lib().basp_a2a_pack_bf16(_dev(own, "own", torch.float32),
+                                    _dev(out, "out", torch.bfloat16), b, Sg * G, n, d, G,
+                                    _stream(own)), "basp_a2a_pack_bf16")
     return out
 
 

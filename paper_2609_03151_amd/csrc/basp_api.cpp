@@ -387,6 +387,35 @@ int basp_a2a_unpack(const void *recv, void *own, int b, int S, int n_heads, int 
   return run_a2a(false, recv, own, b, S, n_heads, d, G, dtype, stream);
 }
 
+int basp_a2a_pack_bf16(const float *own, void *send, int b, int S, int n_heads, int d, int G,
+                       void *stream) {
+  int rc = check_perm_shape(b, S, n_heads, d, G, BASP_F32);
+  if (rc) return rc;
+  if ((long long)b * S == 0) return BASP_OK;  // empty: no pointer is inspected
+  if (!own || !send) return BASP_ERR_NULL;
+  if (!aligned(own, 4) || !aligned(send, 2)) return BASP_ERR_ALIGN;
+  const int n = n_heads;
+  const uint64_t nl = (uint64_t)heads_per_member(n, G), Sg = (uint64_t)(S / G);
+  basp::CastShape c{};
+  c.b = b, c.G = G, c.Sg = (int)Sg;
+  c.row_elems = nl * d;
+  // own [b, S/G, n, d] -> send [G, b, S/G, nl, d]; block j from head j*n/G on
+  c.src_beta = Sg * n * d, c.src_j = 0, c.src_row = (uint64_t)n * d, c.src_off = 0;
+  c.dst_beta = Sg * nl * d, c.dst_j = b * Sg * nl * d, c.dst_row = nl * d, c.dst_off = 0;
+  const float *st[BASP_MAX_GROUP];
+  uint16_t *dt[BASP_MAX_GROUP];
+  bool vec4 = aligned(own, 16) && aligned(send, 8) && c.row_elems % 4 == 0 && c.src_row % 4 == 0;
+  for (int j = 0; j < G; ++j) {
+    const uint64_t h0 = (uint64_t)j * n / G * d;  // first element of member j's heads
+    st[j] = own + h0;
+    dt[j] = static_cast<uint16_t *>(send);
+    vec4 = vec4 && h0 % 4 == 0;
+  }
+  c.vec_elems = vec4 ? 4 : 1;
+  (void)hipGetLastError();
+  return hip_status(basp::launch_cast_bf16(st, dt, c, (hipStream_t)stream));
+}
+
 int basp_attn_fwd(const void *q, const void *k, const void *v, void *o, float *lse, int b,
                   int S, int H, int H_kv, int d, int G, float scale, void *stream) {
   int rc = check_attn(b, S, H, H_kv, d, G, scale);

@@ -156,6 +156,21 @@ struct PermCall {
 // bytes); otherwise one launch each.  Results are those of launch_permute.
 hipError_t launch_permute_batch(const PermCall *calls, int n, hipStream_t stream);
 
+// The owner's send-side split of an fp32 tensor with the conversion to bf16
+// fused (round to nearest even): like a kCopy PermShape, but every offset and
+// the row length count elements (4 bytes read, 2 written), and vec_elems (4
+// or 1) elements move together.
+struct CastShape {
+  int b, G, Sg;
+  uint64_t row_elems;
+  uint64_t src_beta, src_j, src_row, src_off;
+  uint64_t dst_beta, dst_j, dst_row, dst_off;
+  int vec_elems;
+};
+
+hipError_t launch_cast_bf16(const float *const *src_tab, uint16_t *const *dst_tab,
+                            const CastShape &s, hipStream_t stream);
+
 struct AttnShape {
   int b, S, Hl, Hkl, d;  // local heads
   float scale;

@@ -7,6 +7,8 @@
 // send side, a2a_pack:      own shard [b, S/G, n, d] -> [G, b, S/G, n/G, d]
 //         send[j][beta][t][h][e] = own[beta][t][j*n/G + h][e]
 // receive side, a2a_unpack: the inverse, every member's block into the own shard
+// send side, a2a_pack_bf16: a2a_pack of an fp32 tensor, each element converted
+//                           to bf16 on the way (round to nearest even)
 //
 // With fewer heads than members (n < G, G divisible by n) member r handles the
 // single head r*n/G, shared by G/n members; gradients of such a head are
@@ -166,6 +168,44 @@ __global__ __launch_bounds__(256) void permute_batch_kernel(const BatchArgs a) {
   copy_block<V, U, PermMode::kCopy>(s, d, g, bx);
 }
 
+// fp32 -> bf16 (round to nearest even, the hardware's packed conversion) of
+// one vector: 4 floats -> 4 bf16, or 1 -> 1.
+__device__ __forceinline__ u32x2 to_bf16(u32x4 v) {
+  return u32x2{pack_bf16x2(__uint_as_float(v.x), __uint_as_float(v.y)),
+               pack_bf16x2(__uint_as_float(v.z), __uint_as_float(v.w))};
+}
+__device__ __forceinline__ uint16_t to_bf16(uint32_t v) {
+  return (uint16_t)(pack_bf16x2(__uint_as_float(v), 0.f) & 0xFFFFu);
+}
+
+// The cast variant of permute_kernel: geometry in vectors of VS (fp32 side)
+// and VD (bf16 side), one to one.
+template <typename VS, typename VD, int U>
+__global__ __launch_bounds__(256) void cast_kernel(ShardTable src, ShardTable dst, CopyGeom g) {
+  const uint32_t jb = blockIdx.x % g.jb_count, bx = blockIdx.x / g.jb_count;
+  const uint32_t j = jb % g.G, beta = jb / g.G;
+  const VS *s = static_cast<const VS *>(src.p[j]) + beta * g.src_beta + j * g.src_j + g.src_off;
+  VD *d = static_cast<VD *>(const_cast<void *>(dst.p[j])) + beta * g.dst_beta + j * g.dst_j +
+          g.dst_off;
+  const uint32_t step = g.bx_count * 256u * U;
+  for (uint32_t b0 = bx * 256u * U; b0 < g.block_vecs; b0 += step) {  // workgroup-uniform
+    VS v[U];
+    uint32_t rt[U], c[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const uint32_t i = b0 + threadIdx.x + u * 256u;
+      rt[u] = g.by_row.div(i);
+      c[u] = i - rt[u] * g.row_vecs;
+      if (i < g.block_vecs) v[u] = nt_load(s + (uint64_t)rt[u] * g.src_row + c[u]);
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const uint32_t i = b0 + threadIdx.x + u * 256u;
+      if (i < g.block_vecs) nt_store(to_bf16(v[u]), d + (uint64_t)rt[u] * g.dst_row + c[u]);
+    }
+  }
+}
+
 namespace {
 
 constexpr int kU = 8;  // vectors in flight per thread
@@ -249,7 +289,45 @@ hipError_t launch_reduce(const void *const *src_tab, void *const *dst_tab, const
   }
 }
 
+template <typename VS, typename VD>
+hipError_t launch_cast_typed(const float *const *src_tab, uint16_t *const *dst_tab,
+                             const CastShape &s, hipStream_t stream) {
+  constexpr int U = kU;
+  const uint64_t ve = (uint64_t)s.vec_elems;
+  CopyGeom g{};
+  g.row_vecs = (uint32_t)(s.row_elems / ve);
+  g.by_row = FastDiv::make(g.row_vecs);
+  g.block_vecs = (uint32_t)((uint64_t)s.Sg * g.row_vecs);
+  g.G = (uint32_t)s.G;
+  g.reps = 1;
+  g.src_beta = s.src_beta / ve, g.src_j = s.src_j / ve, g.src_row = s.src_row / ve;
+  g.src_off = s.src_off / ve;
+  g.dst_beta = s.dst_beta / ve, g.dst_j = s.dst_j / ve, g.dst_row = s.dst_row / ve;
+  g.dst_off = s.dst_off / ve;
+  const uint64_t blocks = (uint64_t)s.b * s.G;
+  g.jb_count = (uint32_t)blocks;
+  if (blocks == 0 || g.block_vecs == 0) return hipSuccess;
+  uint64_t bx = ((uint64_t)g.block_vecs + 256 * U - 1) / (256 * U);
+  const uint64_t want = (8192 + blocks - 1) / blocks;
+  if (bx > want) bx = want;
+  g.bx_count = (uint32_t)bx;
+  ShardTable ts, td;
+  for (int j = 0; j < s.G; ++j) {
+    ts.p[j] = src_tab[j];
+    td.p[j] = dst_tab[j];
+  }
+  hipLaunchKernelGGL((cast_kernel<VS, VD, U>), dim3((unsigned)(g.bx_count * blocks)), dim3(256), 0,
+                     stream, ts, td, g);
+  return hipGetLastError();
+}
+
 }  // namespace
+
+hipError_t launch_cast_bf16(const float *const *src_tab, uint16_t *const *dst_tab,
+                            const CastShape &s, hipStream_t stream) {
+  if (s.vec_elems == 4) return launch_cast_typed<u32x4, u32x2>(src_tab, dst_tab, s, stream);
+  return launch_cast_typed<uint32_t, uint16_t>(src_tab, dst_tab, s, stream);
+}
 
 hipError_t launch_permute_batch(const PermCall *calls, int n, hipStream_t stream) {
   bool one_launch = n >= 1 && n <= kMaxBatch;

@@ -26,6 +26,12 @@ hipError_t launch_permute_batch(const PermCall *calls, int n, hipStream_t) {
   if (n > 0) g_perm = calls[0].s;
   return hipSuccess;
 }
+hipError_t launch_cast_bf16(const float *const *, uint16_t *const *, const CastShape &s,
+                            hipStream_t) {
+  ++g_launches;
+  if (s.vec_elems != 4 || s.row_elems != 4 * 64) return hipErrorInvalidValue;
+  return hipSuccess;
+}
 hipError_t launch_attn_fwd(const RowView &, const RowView &, const RowView &, const RowView &,
                            float *, const AttnShape &s, bool sharded, hipStream_t) {
   ++g_launches;
@@ -267,6 +273,13 @@ int main() {
                                nullptr),
          BASP_OK);
   CHECK(basp::g_sharded && basp::g_attn.Hkl == 1 && basp::g_attn.Hl == 2);
+  // the send-side split with the fp32 -> bf16 cast: checks, then the launch
+  EXPECT(basp_a2a_pack_bf16((const float *)dst, fake(0x50001), 1, 64, 8, 64, 2, nullptr),
+         BASP_ERR_ALIGN);
+  EXPECT(basp_a2a_pack_bf16((const float *)dst, fake(0x50000), 1, 64, 6, 64, 4, nullptr),
+         BASP_ERR_SHAPE);
+  EXPECT(basp_a2a_pack_bf16((const float *)dst, fake(0x50000), 1, 64, 8, 64, 2, nullptr),
+         BASP_OK);
   printf("abi ok %d\n", g_cases);
   return 0;
 }

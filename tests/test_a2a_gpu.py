@@ -142,3 +142,62 @@ def test_a2a_full_size(name):
             del own32
         del own, send, back
     torch.cuda.empty_cache()
+
+
+CAST_CASES = CASES + [(1, 64, 2, 64, 8), (2, 48, 4, 3, 8)]   # + shared heads (n < G)
+
+
+def _cast_inputs(b, S, n, d, G, seed):
+    """fp32 own shard: normals over many magnitudes, plus exact ties, values
+    that round to infinity, infinities and signed zeros (no NaN, no
+    subnormal: their handling is not part of the contract checked here)."""
+    g = torch.Generator().manual_seed(seed)
+    own = torch.randn(b, S // G, n, d, generator=g) * torch.exp2(
+        torch.randint(-30, 30, (b, S // G, n, d), generator=g).float())
+    flat = own.view(-1)
+    special = torch.tensor([1.00390625, 1.01171875, -1.00390625, 3.3961e38, -3.4e38,
+                            float("inf"), float("-inf"), 0.0, -0.0, 2.0 ** -126, 65504.0])
+    k = min(special.numel(), flat.numel())
+    flat[:k] = special[:k]
+    return own
+
+
+@pytest.mark.parametrize("b,S,n,d,G", CAST_CASES)
+def test_a2a_pack_bf16_bitexact(b, S, n, d, G):
+    own_h = _cast_inputs(b, S, n, d, G, seed=S + n + d + G)
+    nl = basp.heads_per_member(n, G)
+    send, sbuf, sent = _guarded((G, b, S // G, nl, d), torch.bfloat16)
+    basp.a2a_pack_bf16(own_h.cuda(), G, out=send)
+    torch.cuda.synchronize()
+    ref = oracle.a2a_pack_bf16(own_h.numpy(), G)
+    assert np.array_equal(_bits(send).view(np.uint16), ref)
+    assert _guards_intact(sbuf, sent)
+
+
+def test_a2a_pack_bf16_misaligned_takes_narrow_path():
+    b, S, n, d, G = 1, 64, 8, 64, 4
+    own_h = _cast_inputs(b, S, n, d, G, seed=77)
+    flat = torch.zeros(own_h.numel() + 1, device="cuda")
+    own = flat[1:].view(own_h.shape)            # 4-byte but not 16-byte aligned
+    own.copy_(own_h.cuda())
+    out_flat = torch.zeros(own_h.numel() + 1, dtype=torch.bfloat16, device="cuda")
+    out = out_flat[1:].view(G, b, S // G, n // G, d)   # 2-byte aligned only
+    lib = basp.lib()
+    import ctypes
+    rc = lib.basp_a2a_pack_bf16(ctypes.c_void_p(own.data_ptr()), ctypes.c_void_p(out.data_ptr()),
+                                b, S, n, d, G, ctypes.c_void_p(torch.cuda.current_stream().cuda_stream))
+    assert rc == 0
+    torch.cuda.synchronize()
+    assert np.array_equal(_bits(out).view(np.uint16), oracle.a2a_pack_bf16(own_h.numpy(), G))
+
+
+def test_a2a_pack_bf16_full_size_dout_shard():
+    """The Llama-3-70B share's own dO shard [1, 16384, 64, 128] as fp32, sent as bf16."""
+    w = WORKLOADS["llama3_70b_s128k"]
+    g = torch.Generator().manual_seed(5)
+    own_h = torch.randn(1, w.S // w.G, w.H, w.d, generator=g)
+    send = basp.a2a_pack_bf16(own_h.cuda(), w.G)
+    torch.cuda.synchronize()
+    got = _bits(send).view(np.uint16)
+    ref = oracle.a2a_pack_bf16(own_h.numpy(), w.G)
+    assert np.array_equal(got, ref)

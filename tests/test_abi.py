@@ -260,3 +260,19 @@ def test_noalloc_backward_rejects_before_any_hip_call():
     assert L.basp_attn_bwd_noalloc(*p, 1, 4096, 8, 2, 72, 2, f, None) == UNSUP
     assert L.basp_attn_bwd_noalloc(*p, 1, 4095, 8, 2, 128, 2, f, None) == SHAPE
     assert L.basp_attn_bwd_noalloc(*([None] * 9), 0, 4096, 8, 2, 128, 2, f, None) == OK
+
+
+def test_a2a_pack_bf16_rejects_before_any_hip_call():
+    """Only invalid (or empty) calls: the pointers are fake host values."""
+    L = basp.lib()
+    a, c = _fake(0x1000), _fake(0x2000)
+    f = L.basp_a2a_pack_bf16
+    assert f(a, c, 1, 63, 8, 64, 2, None) == SHAPE       # S % G
+    assert f(a, c, 1, 64, 6, 64, 4, None) == SHAPE       # n neither multiple nor divisor of G
+    assert f(a, c, 1, 64, 8, 64, 256, None) == SHAPE
+    assert f(None, c, 1, 64, 8, 64, 2, None) == NULL
+    assert f(a, None, 1, 64, 8, 64, 2, None) == NULL
+    assert f(_fake(0x1002), c, 1, 64, 8, 64, 2, None) == ALIGN
+    assert f(a, _fake(0x2001), 1, 64, 8, 64, 2, None) == ALIGN
+    assert f(a, c, 1, 1 << 22, 32, 64, 2, None) == UNSUP
+    assert f(None, None, 0, 64, 8, 64, 2, None) == OK    # empty

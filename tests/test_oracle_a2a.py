@@ -72,3 +72,31 @@ def test_rejects_bad_shapes():
         oracle.a2a_pack(own, 4)        # n % G
     with pytest.raises(oracle.OracleError):
         oracle.a2a_pack(np.zeros((1, 4, 6, 2), dtype=np.uint8), 2)   # element size
+
+
+def test_a2a_pack_bf16_rounds_like_torch_and_indexes_like_a2a_pack():
+    """The cast variant: its bits equal torch's fp32 -> bfloat16 conversion
+    (round to nearest even, a library routine) of a2a_pack's fp32 blocks, on
+    normals of many magnitudes, exact ties, values that round to infinity,
+    infinities, signed zeros and subnormals; shared heads (n < G) too."""
+    import torch
+    g = torch.Generator().manual_seed(3)
+    for b, S, n, d, G in ((2, 16, 8, 8, 4), (1, 24, 2, 5, 4), (1, 8, 3, 4, 1)):
+        own = torch.randn(b, S // G, n, d, generator=g) * torch.exp2(
+            torch.randint(-20, 20, (b, S // G, n, d), generator=g).float())
+        flat = own.view(-1)
+        special = torch.tensor([1.00390625, 1.01171875, -1.00390625, 3.3961e38, -3.4e38,
+                                float("inf"), float("-inf"), 0.0, -0.0, 1e-40, -3e-39,
+                                65504.0, 2.0 ** -126], dtype=torch.float32)
+        flat[:special.numel()] = special
+        got = oracle.a2a_pack_bf16(own.numpy(), G)
+        blocks = torch.from_numpy(oracle.a2a_pack(own.numpy(), G))
+        ref = blocks.to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+        assert np.array_equal(got, ref)
+
+
+def test_a2a_pack_bf16_nan_stays_nan():
+    own = np.full((1, 2, 2, 2), np.nan, dtype=np.float32)
+    own[0, 0, 0, 0] = -np.nan
+    got = oracle.a2a_pack_bf16(own, 2)
+    assert np.all((got & 0x7F80) == 0x7F80) and np.all((got & 0x007F) != 0)
