@@ -249,7 +249,7 @@ int basp_attn_fwd(const void *q, const void *k, const void *v, void *o,
  * heads [rank*H_kv/G, ..), or the one shared head when H_kv < G); lse
  * [b, H/G, S] fp32 as basp_attn_fwd.  Heads of o_shards outside the rank's
  * slice are untouched.  Alignment: every shard pointer 16 bytes, lse 4.
- * Errors: as basp_attn_fwd, plus RANK, and UNSUPPORTED when G > 16, S/G is
+ * Errors: as basp_attn_fwd, plus RANK, and UNSUPPORTED when G > 64, S/G is
  * not a multiple of 256, or (S/G)*max(H, H_kv)*d*4 >= 2^31 bytes. */
 int basp_attn_fwd_sharded(const void *const *q_shards,
                           const void *const *k_shards,

@@ -89,8 +89,10 @@ __host__ __device__ inline int kv_masked_steps(int k0, int r_lo, int steps, int 
 // A head-sharded local tensor [b, S, nl, d] is the one-buffer case
 // (rows = S, row_elems = nl*d, head0 = 0).  The G sequence shards
 // [b, S/G, n, d] of the exchange are G buffers (rows = S/G, row_elems = n*d,
-// head0 = rank*n/G), so the kernels read and write them in place.
-constexpr int kMaxViewBuffers = 16;
+// head0 = rank*n/G), so the kernels read and write them in place.  The
+// view travels as a kernel argument: 64 buffers keep the largest argument
+// list (the key-stationary pass, six views) near 3.3 KB.
+constexpr int kMaxViewBuffers = 64;
 
 struct RowView {
   const void *p[kMaxViewBuffers];
@@ -152,8 +154,9 @@ struct PermCall {
 };
 
 // Up to three permutations in one launch when each has at most
-// kMaxViewBuffers members and all take the same vector width (at least 4
+// kMaxBatchBuffers members and all take the same vector width (at least 4
 // bytes); otherwise one launch each.  Results are those of launch_permute.
+constexpr int kMaxBatchBuffers = 16;
 hipError_t launch_permute_batch(const PermCall *calls, int n, hipStream_t stream);
 
 // The owner's send-side split of an fp32 tensor with the conversion to bf16

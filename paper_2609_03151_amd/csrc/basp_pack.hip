@@ -140,7 +140,7 @@ __global__ __launch_bounds__(256) void permute_kernel(ShardTable src, ShardTable
 // not each pay a launch and a ramp.
 constexpr int kMaxBatch = 3;
 struct BatchTable {
-  const void *p[kMaxViewBuffers];
+  const void *p[kMaxBatchBuffers];
 };
 struct BatchArgs {
   BatchTable src[kMaxBatch], dst[kMaxBatch];
@@ -333,7 +333,7 @@ hipError_t launch_permute_batch(const PermCall *calls, int n, hipStream_t stream
   bool one_launch = n >= 1 && n <= kMaxBatch;
   int vec = 16;
   for (int k = 0; k < n; ++k) {
-    one_launch = one_launch && calls[k].s.G <= kMaxViewBuffers &&
+    one_launch = one_launch && calls[k].s.G <= kMaxBatchBuffers &&
                  calls[k].s.vec_bytes == calls[0].s.vec_bytes;
     vec = calls[k].s.vec_bytes < vec ? calls[k].s.vec_bytes : vec;
   }

@@ -176,7 +176,7 @@ def test_sharded_attn_rejects_before_any_hip_call():
     assert fwd(1, 1024, 8, 2, 128, 4, 4) == RANK
     assert fwd(1, 1002, 8, 2, 128, 4, 0) == SHAPE                  # S % G
     assert fwd(1, 1536, 8, 2, 128, 4, 0) == UNSUP                  # 384 rows per shard
-    assert fwd(1, 32 * 256, 32, 32, 128, 32, 0, G=32) == UNSUP     # G > 16
+    assert fwd(1, 128 * 256, 128, 128, 128, 128, 0, G=128) == UNSUP  # G > 64
     assert fwd(1, 1024, 8, 2, 72, 4, 0) == UNSUP                   # head dim
     assert fwd(1, 1024, 8, 2, 128, 4, 0, t=(vp * 4)(0x1000, 0, 0x3000, 0x4000)) == NULL
     assert fwd(1, 1024, 8, 2, 128, 4, 0, t=(vp * 4)(0x1000, 0x2008, 0x3000, 0x4000)) == ALIGN

@@ -5,9 +5,9 @@ rank's head slices of the send buffers.
 
 * bit for bit the same as the composed path (pack -> attention -> unpack) at
   shapes covering one and several row chunks of the backward, b > 1, group
-  sizes 2 to 16 (shard row counts that are not powers of two included), head
-  dims 64/80/96/128, and a kv head shared by several members (the partial
-  dK, dV then go to one send block per member);
+  sizes 2 to 64 (shard row counts that are not powers of two included), head
+  dims 64/80/96/128, and a kv head shared by several members, up to 8 (the
+  partial dK, dV then go to one send block per member);
 * other heads of the shard buffers untouched (sentinels);
 * one shape against the oracle's composition directly;
 * full size (the Llama-3-8B share, the batch-agnostic share with b = 2,
@@ -60,7 +60,9 @@ CASES = [  # b, S, H, H_kv, d, G, rank
     (1, 2048, 12, 4, 96, 4, 3),     # d = 96, one kv head per member
     (1, 3072, 8, 8, 80, 4, 2),      # d = 80, 768 rows per shard
     (2, 1536, 6, 6, 128, 6, 5),     # G = 6
-    (1, 4096, 16, 16, 64, 16, 9),   # G = 16, the most the in-place path takes
+    (1, 4096, 16, 16, 64, 16, 9),   # G = 16
+    (2, 8192, 32, 32, 128, 32, 17), # G = 32, b = 2, two row chunks
+    (1, 16384, 64, 64, 64, 64, 63), # G = 64, the most the in-place path takes
 ]
 
 
@@ -80,6 +82,7 @@ SHARED = [  # b, S, H, H_kv, d, G, rank: a kv head shared by G / H_kv members
     (1, 2048, 16, 4, 128, 8, 3),    # one row chunk
     (2, 4096, 8, 2, 64, 4, 1),      # two row chunks, b = 2
     (1, 4096, 16, 8, 96, 16, 9),    # G = 16, 2 members per kv head
+    (1, 16384, 64, 8, 128, 64, 37), # G = 64: Llama-3-70B heads, 8 members per kv head
 ]
 
 
