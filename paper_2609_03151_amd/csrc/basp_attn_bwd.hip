@@ -542,7 +542,11 @@ __global__ __launch_bounds__(kDqThreads, 1) void bwd_dq_kernel(
     int qtiles, float c, float scale) {
   using C = DqCfg<D>;
   using T = LdsTile<C::LW>;
+  // LDS: the K tiles of the kStages ring stages, then their V tiles; with
+  // the tile loop unrolled over the stages every operand address is a lane's
+  // fixed offset plus an instruction immediate.
   __shared__ __attribute__((aligned(16))) unsigned char smem[kStages * C::STAGE_BYTES];
+  constexpr int kVRegion = kStages * C::TILE_BYTES;
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -597,7 +601,7 @@ __global__ __launch_bounds__(kDqThreads, 1) void bwd_dq_kernel(
   // shard only when the tiles of the current one are used up.
   uint32_t sh_tiles = 0, sh_base = 0;
   auto load_tile = [&](int t) __attribute__((always_inline)) {
-    const uint32_t ks = smem_lds + (t % kStages) * C::STAGE_BYTES;
+    const uint32_t ks = smem_lds + (t % kStages) * C::TILE_BYTES;
     uint32_t base = (uint32_t)(t * kDQN) * kv_row_bytes;
     if constexpr (SH) {
       if (sh_tiles == 0) {  // wave-uniform; tile t is the first of its shard
@@ -617,7 +621,7 @@ __global__ __launch_bounds__(kDqThreads, 1) void bwd_dq_kernel(
     for (int i = 0; i < C::DMA_PER_WAVE; ++i) {
       const uint32_t lds = ks + (w * C::DMA_PER_WAVE + i) * 1024;
       buf_load16_lds_async(rk, base + g_off[i], lds);
-      buf_load16_lds_async(rv, base + g_off[i], lds + C::TILE_BYTES);
+      buf_load16_lds_async(rv, base + g_off[i], lds + kVRegion);
     }
   };
   auto wait_tile = [&](int ahead) __attribute__((always_inline)) {
@@ -626,12 +630,24 @@ __global__ __launch_bounds__(kDqThreads, 1) void bwd_dq_kernel(
     else wait_vmcnt<0>();
   };
 
-  int a_off[C::NS];  // row l32 (+32 for m = 1), chunk 2s + hh
+  // Row l32 (+32 for m = 1), chunk 2s + hh, of the K tile (a_off) and the V
+  // tile (v_off).  With 64-wide rows the V region starts within reach of the
+  // instruction immediate, so V takes the K offsets.
+  constexpr bool kVImm = kVRegion + kStages * C::TILE_BYTES <= 65536;
+  int a_off[C::NS], v_off[C::NS];
 #pragma unroll
   for (int s = 0; s < C::NS; ++s) {
     a_off[s] = T::off(l32, 2 * s + hh);
     asm volatile("" : "+v"(a_off[s]));
+    if constexpr (!kVImm) {
+      v_off[s] = a_off[s] + kVRegion;
+      asm volatile("" : "+v"(v_off[s]));
+    }
   }
+  auto v_at = [&](int s) __attribute__((always_inline)) {
+    if constexpr (kVImm) return a_off[s] + kVRegion;
+    else return v_off[s];
+  };
   // Transposed A operand: rows 16*s2 + 4hh (+8), columns 32n + 16*((lane/16)&1).
   int t_off[C::NE][2];
 #pragma unroll
@@ -651,25 +667,26 @@ __global__ __launch_bounds__(kDqThreads, 1) void bwd_dq_kernel(
   // One 64-key tile in two 32-key halves (keeps the score state at 2 x 16
   // registers).  S^T = K Q^T and dP^T = V dO^T: M = 32 keys, N = this wave's
   // rows; sacc[r] holds key j0 + 32m + 8(r/4) + 4hh + r%4, query row `row`.
-  auto tile = [&](int t, auto mask_tag) __attribute__((always_inline)) {
+  // `st` = t % kStages (a constant in the unrolled loop).
+  auto tile = [&](int t, int st, auto mask_tag) __attribute__((always_inline)) {
     constexpr bool MASK = decltype(mask_tag)::value;
     const int j0 = t * kDQN;
-    const unsigned char *Ks = smem + (t % kStages) * C::STAGE_BYTES;
-    const unsigned char *Vs = Ks + C::TILE_BYTES;
+    const unsigned char *Ks = smem + st * C::TILE_BYTES;
+    const unsigned char *Vs = Ks;  // v_at adds the V region's base
 #pragma unroll
     for (int m = 0; m < 2; ++m) {
       if (MASK && j0 + 32 * m > wrow0 + 31) continue;  // wave-uniform: half entirely masked
       f32x16 sacc, pacc;
       {
         const bf16x8 ak = *reinterpret_cast<const bf16x8 *>(Ks + a_off[0] + m * 32 * T::ROW_BYTES);
-        const bf16x8 av = *reinterpret_cast<const bf16x8 *>(Vs + a_off[0] + m * 32 * T::ROW_BYTES);
+        const bf16x8 av = *reinterpret_cast<const bf16x8 *>(Vs + v_at(0) + m * 32 * T::ROW_BYTES);
         sacc = mfma32x32x16(ak, qf[0], f32x16{});
         pacc = mfma32x32x16(av, df[0], f32x16{});
       }
 #pragma unroll
       for (int s = 1; s < C::NS; ++s) {
         const bf16x8 ak = *reinterpret_cast<const bf16x8 *>(Ks + a_off[s] + m * 32 * T::ROW_BYTES);
-        const bf16x8 av = *reinterpret_cast<const bf16x8 *>(Vs + a_off[s] + m * 32 * T::ROW_BYTES);
+        const bf16x8 av = *reinterpret_cast<const bf16x8 *>(Vs + v_at(s) + m * 32 * T::ROW_BYTES);
         sacc = mfma32x32x16(ak, qf[s], sacc);
         pacc = mfma32x32x16(av, df[s], pacc);
       }
@@ -716,13 +733,22 @@ __global__ __launch_bounds__(kDqThreads, 1) void bwd_dq_kernel(
   };
   for (int t = 0; t < 2 && t < nt; ++t) load_tile(t);
   const int t_mask = min(nt, q0 / kDQN);  // tiles before t_mask need no mask
-  for (int t = 0; t < t_mask; ++t) {
-    step(t);
-    tile(t, std::false_type{});
+  static_assert(kStages == 4, "the unrolled loop assumes four ring stages");
+  int t = 0;
+  for (; t + 4 <= t_mask; t += 4) {  // t % 4 == 0
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      step(t + u);
+      tile(t + u, u, std::false_type{});
+    }
   }
-  for (int t = t_mask; t < nt; ++t) {
+  for (; t < t_mask; ++t) {
     step(t);
-    if (t * kDQN <= wrow0 + 31) tile(t, std::true_type{});  // wave-uniform
+    tile(t, t % kStages, std::false_type{});
+  }
+  for (; t < nt; ++t) {
+    step(t);
+    if (t * kDQN <= wrow0 + 31) tile(t, t % kStages, std::true_type{});  // wave-uniform
   }
 
   if (row < S) {

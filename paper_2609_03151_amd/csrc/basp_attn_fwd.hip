@@ -35,6 +35,10 @@
 //     read two slots ahead.  Every stretch of a wave's instruction stream
 //     thus mixes matrix and vector work; the arithmetic and its order per
 //     tile are unchanged (bit-identical results).
+//   * LDS holds the K tiles of the four ring stages, then their V tiles, and
+//     the pipelined loop is unrolled over the four stages: every operand
+//     address is a lane's fixed offset plus an instruction immediate, with
+//     no per-tile address arithmetic.
 //   * the running maximum used as the exponent reference only moves when a
 //     row's maximum grows by more than 8 (in log2 units): P <= 2^8 stays exact
 //     in bf16's relative precision and O is rescaled only on those tiles.
@@ -91,7 +95,10 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
     float c /* scale * log2(e) */) {
   using C = FwdCfg<D>;
   using T = LdsTile<C::LW>;
+  // LDS: the K tiles of the kStages ring stages, then their V tiles, so that
+  // a stage's K and V tiles sit at the same offset from two fixed bases.
   __shared__ __attribute__((aligned(16))) unsigned char smem[kStages * C::STAGE_BYTES];
+  constexpr int kVRegion = kStages * C::TILE_BYTES;
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave index, held in an SGPR
@@ -143,7 +150,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
   // shard only when the tiles of the current one are used up.
   uint32_t sh_tiles = 0, sh_base = 0;
   auto load_tile = [&](int t) {  // issue; lands asynchronously in stage t % kStages
-    const uint32_t ks = smem_lds + (t % kStages) * C::STAGE_BYTES;
+    const uint32_t ks = smem_lds + (t % kStages) * C::TILE_BYTES;
     uint32_t base = (uint32_t)(t * kBN) * kv_row_bytes;
     if constexpr (SH) {
       if (sh_tiles == 0) {  // wave-uniform; tile t is the first of its shard
@@ -163,7 +170,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
     for (int i = 0; i < C::DMA_PER_WAVE; ++i) {
       const uint32_t lds_off = ks + (w * C::DMA_PER_WAVE + i) * 1024;
       buf_load16_lds_async(rk, base + g_off[i], lds_off);
-      buf_load16_lds_async(rv, base + g_off[i], lds_off + C::TILE_BYTES);
+      buf_load16_lds_async(rv, base + g_off[i], lds_off + kVRegion);
     }
   };
   // Wait until this wave's loads of tile t landed, with `ahead` later tiles
@@ -191,7 +198,8 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
   for (int n = 0; n < C::NE; ++n)
 #pragma unroll
     for (int x = 0; x < 2; ++x) {
-      v_off[n][x] = tr_piece_off<C::LW>(4 * hh + 8 * x, 32 * n + 16 * ((lane >> 4) & 1), lane);
+      v_off[n][x] =
+          kVRegion + tr_piece_off<C::LW>(4 * hh + 8 * x, 32 * n + 16 * ((lane >> 4) & 1), lane);
       asm volatile("" : "+v"(v_off[n][x]));
     }
 
@@ -209,8 +217,8 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
   auto tile = [&](int t, auto mask_tag) {
     constexpr bool MASK = decltype(mask_tag)::value;
     const int j0 = t * kBN;
-    const unsigned char *Ks = smem + (t % kStages) * C::STAGE_BYTES;
-    const unsigned char *Vs = Ks + C::TILE_BYTES;
+    const unsigned char *Ks = smem + (t % kStages) * C::TILE_BYTES;
+    const unsigned char *Vs = Ks;  // v_off holds the V region's base
 
     wave_priority<1>();  // the score products run ahead of the partner wave's softmax
     f32x16 sacc[2];
@@ -323,7 +331,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
   // and its order per tile are those of `tile`: bit-identical results.
   const int t_mask = min(nt, q0 / kBN);
   auto scores = [&](int t, f32x16 (&sc)[2]) __attribute__((always_inline)) {
-    const unsigned char *Ks = smem + (t % kStages) * C::STAGE_BYTES;
+    const unsigned char *Ks = smem + (t % kStages) * C::TILE_BYTES;
 #pragma unroll
     for (int m = 0; m < 2; ++m) {
       const bf16x8 a = *reinterpret_cast<const bf16x8 *>(Ks + k_off[0] + m * 32 * T::ROW_BYTES);
@@ -382,7 +390,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
     l_run += psum;
   };
   auto pv = [&](int t, const bf16x8 (&pf)[kBN / 16]) __attribute__((always_inline)) {
-    const unsigned char *Vs = smem + (t % kStages) * C::STAGE_BYTES + C::TILE_BYTES;
+    const unsigned char *Vs = smem + (t % kStages) * C::TILE_BYTES;
 #pragma unroll
     for (int n = 0; n < C::NE; ++n)
 #pragma unroll
@@ -398,14 +406,16 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
   // fenced by scheduling barriers: the slot's share of the vector work, and
   // the operand read for the product kPf slots later.
   constexpr int kPf = 2;
-  auto pipelined = [&](int t, f32x16 (&cur)[2], f32x16 (&nxt)[2]) __attribute__((always_inline)) {
+  auto pipelined = [&](int t, auto stage_tag, f32x16 (&cur)[2], f32x16 (&nxt)[2])
+                       __attribute__((always_inline)) {
+    constexpr int ST = decltype(stage_tag)::value;  // t % kStages
     make_visible(min(1, nt - 2 - t), t + kPD + 1);  // tile t+1 readable, t+2 in flight
     asm volatile("" : "+v"(m_ref));  // keep the exponent arguments here
     bf16x8 pf[kBN / 16];
     // Block X: scores of tile t+1 (16 products), exponentials of tile t.
     {
       constexpr int NG = 2 * C::NS;
-      const unsigned char *Ks = smem + ((t + 1) % kStages) * C::STAGE_BYTES;
+      const unsigned char *Ks = smem + ((ST + 1) % kStages) * C::TILE_BYTES;
       bf16x8 op[NG];
       auto read = [&](int g) __attribute__((always_inline)) {
         op[g] = *reinterpret_cast<const bf16x8 *>(Ks + k_off[g / 2] + (g % 2) * 32 * T::ROW_BYTES);
@@ -438,7 +448,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
     float psum = 0.f, mx = -INFINITY;
     {
       constexpr int NG = C::NE * (kBN / 16);
-      const unsigned char *Vs = smem + (t % kStages) * C::STAGE_BYTES + C::TILE_BYTES;
+      const unsigned char *Vs = smem + ST * C::TILE_BYTES;
       bf16x8 op[NG];
       auto read = [&](int g) __attribute__((always_inline)) {
         const int n = g / (kBN / 16), s2 = g % (kBN / 16);
@@ -487,14 +497,32 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
     make_visible(min(kPD, nt - 1), nt);  // tile 0; tile kPD + 1 is issued by iteration 0
     scores(0, sa);
     move_reference(row_max(sa));
+    using I0 = std::integral_constant<int, 0>;
+    using I1 = std::integral_constant<int, 1>;
+    using I2 = std::integral_constant<int, 2>;
+    using I3 = std::integral_constant<int, 3>;
+    static_assert(kStages == 4, "the unrolled loop assumes four ring stages");
     int t = 0;
-    for (; t + 2 < t_mask; t += 2) {
-      pipelined(t, sa, sb);
-      pipelined(t + 1, sb, sa);
+    for (; t + 4 < t_mask; t += 4) {  // t % 4 == 0: every stage offset a constant
+      pipelined(t, I0{}, sa, sb);
+      pipelined(t + 1, I1{}, sb, sa);
+      pipelined(t + 2, I2{}, sa, sb);
+      pipelined(t + 3, I3{}, sb, sa);
     }
+    // 1 to 4 unmasked tiles left, the last of them without scores to start
     if (t + 1 < t_mask) {
-      pipelined(t, sa, sb);
-      pipelined_last(t + 1, sb);
+      pipelined(t, I0{}, sa, sb);
+      if (t + 2 < t_mask) {
+        pipelined(t + 1, I1{}, sb, sa);
+        if (t + 3 < t_mask) {
+          pipelined(t + 2, I2{}, sa, sb);
+          pipelined_last(t + 3, sb);
+        } else {
+          pipelined_last(t + 2, sa);
+        }
+      } else {
+        pipelined_last(t + 1, sb);
+      }
     } else {
       pipelined_last(t, sa);
     }
