@@ -588,6 +588,10 @@ __global__ __launch_bounds__(kDqThreads, 1) void bwd_dq_kernel(
   f32x2 ldr = {INFINITY, 0.f};  // rows past S: P = 0
   if (row < S) ldr = ld[((size_t)beta * Hl + h) * S + row];
   const float lse2 = ldr[0], Drow = ldr[1];
+  // dP^T starts from -D (the accumulator's initial value), so dS = P dP'.
+  f32x16 negd;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) negd[r] = -Drow;
   wait_vmcnt<0>();  // retire the tracked loads before untracked copies start
 
   const int kv_end = min(S, q0 + kDQM);
@@ -681,7 +685,7 @@ __global__ __launch_bounds__(kDqThreads, 1) void bwd_dq_kernel(
         const bf16x8 ak = *reinterpret_cast<const bf16x8 *>(Ks + a_off[0] + m * 32 * T::ROW_BYTES);
         const bf16x8 av = *reinterpret_cast<const bf16x8 *>(Vs + v_at(0) + m * 32 * T::ROW_BYTES);
         sacc = mfma32x32x16(ak, qf[0], f32x16{});
-        pacc = mfma32x32x16(av, df[0], f32x16{});
+        pacc = mfma32x32x16(av, df[0], negd);
       }
 #pragma unroll
       for (int s = 1; s < C::NS; ++s) {
@@ -698,7 +702,7 @@ __global__ __launch_bounds__(kDqThreads, 1) void bwd_dq_kernel(
           const int j = j0 + 32 * m + 8 * (r >> 2) + 4 * hh + (r & 3);
           if (j > row) p = 0.f;
         }
-        pacc[r] = p * (pacc[r] - Drow);
+        pacc[r] = p * pacc[r];
       }
       bf16x8 sb[2];
 #pragma unroll
