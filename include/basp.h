@@ -319,8 +319,8 @@ int basp_attn_bwd_noalloc(const void *q, const void *k, const void *v,
  * other heads are untouched.  The result is bit for bit that of basp_pack
  * (of dO), basp_attn_bwd and basp_unpack of each gradient.  lse as there;
  * workspace of basp_attn_bwd_sharded_workspace_bytes(), 16-byte aligned
- * (the rank's heads of Q and dO are first packed into it: the key pass
- * streams those rows many times, and local rows stream faster than rows a
+ * (the rank's heads of Q, dO, K and V are first packed into it: the passes
+ * stream those rows many times, and local rows stream faster than rows a
  * whole shard row apart).
  * With a kv head shared by G/H_kv members (H_kv < G, Sec. II-A GQA under the
  * head split of Sec. II-C) each member holds only a partial dK, dV of that
@@ -331,8 +331,9 @@ int basp_attn_bwd_noalloc(const void *q, const void *k, const void *v,
  * (basp_a2a_unpack does this).
  * Errors: as basp_attn_fwd_sharded, plus WORKSPACE. */
 /* Bytes of device workspace basp_attn_bwd_sharded needs: local copies of
- * the rank's heads of Q and dO (each [b, S, H/G, d] bf16, rounded up to 256
- * bytes), then basp_attn_bwd_workspace_bytes().  0 for an invalid or empty
+ * the rank's heads of Q and dO (each [b, S, H/G, d] bf16) and of K and V
+ * (each [b, S, Hkl, d] bf16, Hkl as basp_attn_fwd), each rounded up to 256
+ * bytes, then basp_attn_bwd_workspace_bytes().  0 for an invalid or empty
  * shape. */
 size_t basp_attn_bwd_sharded_workspace_bytes(int b, int S, int H, int H_kv,
                                              int d, int G);

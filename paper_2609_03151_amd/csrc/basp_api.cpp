@@ -249,10 +249,16 @@ int check_shard_table(const void *const *tab, int G) {
   return BASP_OK;
 }
 
-// Bytes of one local [b, S, H/G, d] bf16 copy inside the in-place
-// backward's workspace, rounded up to 256.
-size_t local_copy_bytes(const basp::AttnShape &s) {
-  return ((size_t)s.b * s.S * s.Hl * s.d * 2 + 255) & ~(size_t)255;
+// Bytes of one local [b, S, nl, d] bf16 copy inside the in-place
+// backward's workspace, rounded up to 256: nl = H/G (Q, dO) or the rank's kv
+// heads (K, V).
+size_t local_copy_bytes(const basp::AttnShape &s, int nl) {
+  return ((size_t)s.b * s.S * nl * s.d * 2 + 255) & ~(size_t)255;
+}
+// The in-place backward's copies of Q, dO, K, V, then the backward's own
+// workspace.
+size_t sharded_bwd_copies_bytes(const basp::AttnShape &s) {
+  return 2 * local_copy_bytes(s, s.Hl) + 2 * local_copy_bytes(s, s.Hkl);
 }
 
 }  // namespace
@@ -464,7 +470,7 @@ size_t basp_attn_bwd_sharded_workspace_bytes(int b, int S, int H, int H_kv, int 
   if (check_share(b, S, H, H_kv, d, G) != BASP_OK) return 0;
   basp::AttnShape s = attn_shape(b, S, H, H_kv, d, G, 1.f);
   if ((long long)b * S == 0) return 0;
-  return 2 * local_copy_bytes(s) + basp::attn_bwd_workspace_bytes(s);
+  return sharded_bwd_copies_bytes(s) + basp::attn_bwd_workspace_bytes(s);
 }
 
 }  // extern "C"
@@ -559,32 +565,38 @@ int basp_attn_bwd_sharded(const void *const *q_shards, const void *const *k_shar
   if (!lse) return BASP_ERR_NULL;
   if (!aligned(lse, 4)) return BASP_ERR_ALIGN;
   basp::AttnShape s = attn_shape(b, S, H, H_kv, d, G, scale);
-  const size_t copy = local_copy_bytes(s);
-  const size_t need = 2 * copy + basp::attn_bwd_workspace_bytes(s);
+  const size_t copies = sharded_bwd_copies_bytes(s);
+  const size_t need = copies + basp::attn_bwd_workspace_bytes(s);
   if (workspace_bytes < need) return BASP_ERR_WORKSPACE;
   if (!workspace) return BASP_ERR_NULL;
   if (!aligned(workspace, 16)) return BASP_ERR_ALIGN;
-  // Q and dO rows are streamed once per key tile by the key-stationary pass;
-  // read from the shards, rows sit the whole shard row (all H heads) apart
-  // and stream measurably slower than from a local copy.  So the rank's
-  // heads of Q and dO are first packed into the workspace (one launch), and
-  // the kernels read those copies; everything else is read and written in
-  // place.
+  // Q and dO rows are streamed once per key tile by the key-stationary pass,
+  // K and V rows once per row tile by the dQ pass; read from the shards,
+  // rows sit a whole shard row (all heads) apart and stream measurably
+  // slower than from a local copy.  So the rank's heads of Q, dO, K and V
+  // are first packed into the workspace (two launches), and the kernels read
+  // those copies; O is read and the gradients written in place.
   char *ws = static_cast<char *>(workspace);
-  void *q_loc = ws, *do_loc = ws + copy;
-  basp::PermCall pc[2];
+  const size_t cq = local_copy_bytes(s, s.Hl), ck = local_copy_bytes(s, s.Hkl);
+  void *q_loc = ws, *do_loc = ws + cq, *k_loc = ws + 2 * cq, *v_loc = ws + 2 * cq + ck;
+  basp::PermCall pc[4];
   bool empty = false;
   rc = prep_pack(true, false, q_shards, q_loc, b, S, H, d, G, rank, BASP_BF16, &pc[0], &empty);
   if (!rc) rc = prep_pack(true, false, do_shards, do_loc, b, S, H, d, G, rank, BASP_BF16, &pc[1],
                           &empty);
+  if (!rc) rc = prep_pack(true, false, k_shards, k_loc, b, S, H_kv, d, G, rank, BASP_BF16, &pc[2],
+                          &empty);
+  if (!rc) rc = prep_pack(true, false, v_shards, v_loc, b, S, H_kv, d, G, rank, BASP_BF16, &pc[3],
+                          &empty);
   if (rc) return rc;
   (void)hipGetLastError();
   rc = hip_status(basp::launch_permute_batch(pc, 2, (hipStream_t)stream));
+  if (!rc) rc = hip_status(basp::launch_permute_batch(pc + 2, 2, (hipStream_t)stream));
   if (rc) return rc;
   using basp::shard_view;
   const basp::RowView qv = basp::local_view(q_loc, S, s.Hl, d),
-                      kv = shard_view(k_shards, G, S, H_kv, d, rank),
-                      vv = shard_view(v_shards, G, S, H_kv, d, rank),
+                      kv = basp::local_view(k_loc, S, s.Hkl, d),
+                      vv = basp::local_view(v_loc, S, s.Hkl, d),
                       ov = shard_view(o_shards, G, S, H, d, rank),
                       dov = basp::local_view(do_loc, S, s.Hl, d),
                       dqv = shard_view((Tab)dq_shards, G, S, H, d, rank),
@@ -594,7 +606,7 @@ int basp_attn_bwd_sharded(const void *const *q_shards, const void *const *k_shar
                                       : shard_view((Tab)dv_shards, G, S, H_kv, d, rank);
   (void)hipGetLastError();
   return hip_status(basp::launch_attn_bwd(qv, kv, vv, ov, lse, dov, dqv, dkv, dvv,
-                                          ws + 2 * copy, s, true, (hipStream_t)stream));
+                                          ws + copies, s, true, (hipStream_t)stream));
 }
 
 }  // extern "C"

@@ -33,12 +33,12 @@
 //     SIMD (8 waves, 32 rows each), which raise their issue priority over
 //     the accumulating products so that one wave's elementwise work overlaps
 //     the other's MFMAs.
-//   * Q, K, V, O, dO and the gradients are addressed through row views:
-//     the local head-sharded tensors, or (SH) the G sequence shards of the
-//     exchange in place (row counts multiples of 256: a workgroup's rows or
-//     keys, and every streamed tile, lie in one shard).  Q and dO, which the
-//     key-stationary pass streams once per key tile, are always local
-//     one-buffer views (the in-place entry point packs them first).
+//   * O and the gradients are addressed through row views: the local
+//     head-sharded tensors, or (SH) the G sequence shards of the exchange in
+//     place (row counts multiples of 256: a workgroup's rows or keys lie in
+//     one shard).  Q, K, V and dO, which the passes stream once per tile of
+//     the other side, are always local one-buffer views (the in-place entry
+//     point packs them first).
 #include <math.h>
 
 #include <type_traits>
@@ -190,9 +190,9 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
   bf16x8 kf[C::NS], vf[C::NS];
   {
     uint32_t left;
-    const rsrc_t rk = make_rsrc(view_row<SH, const uint16_t>(kv, beta, k0, kvh, D, left),
+    const rsrc_t rk = make_rsrc(view_row<false, const uint16_t>(kv, beta, k0, kvh, D, left),
                                 left * kv_row_bytes);
-    const rsrc_t rv = make_rsrc(view_row<SH, const uint16_t>(vv, beta, k0, kvh, D, left),
+    const rsrc_t rv = make_rsrc(view_row<false, const uint16_t>(vv, beta, k0, kvh, D, left),
                                 left * kv_row_bytes);
 #pragma unroll
     for (int s = 0; s < C::NS; ++s) {
@@ -565,13 +565,12 @@ __global__ __launch_bounds__(kDqThreads, 1) void bwd_dq_kernel(
       make_rsrc(view_row<false, const uint16_t>(qv, beta, q0, h, D, left), left * q_row_bytes);
   const rsrc_t rd =
       make_rsrc(view_row<false, const uint16_t>(dov, beta, q0, h, D, left), left * q_row_bytes);
-  u32x4 rk = {}, rv = {};  // local K/V: one resource per head; sharded: one per shard
-  if constexpr (!SH) {
-    rk = make_rsrc_words(view_row<false, const uint16_t>(kv, beta, 0, kvh, D, left),
-                         left * kv_row_bytes);
-    rv = make_rsrc_words(view_row<false, const uint16_t>(vv, beta, 0, kvh, D, left),
-                         left * kv_row_bytes);
-  }
+  // K and V are local (the in-place entry point packs them): one resource
+  // per head for every tile.
+  const u32x4 rk = make_rsrc_words(view_row<false, const uint16_t>(kv, beta, 0, kvh, D, left),
+                                   left * kv_row_bytes);
+  const u32x4 rv = make_rsrc_words(view_row<false, const uint16_t>(vv, beta, 0, kvh, D, left),
+                                   left * kv_row_bytes);
   const uint32_t smem_lds = lds_addr_of(smem);
 
   bf16x8 qf[C::NS], df[C::NS];
@@ -601,26 +600,9 @@ __global__ __launch_bounds__(kDqThreads, 1) void bwd_dq_kernel(
 #pragma unroll
   for (int i = 0; i < C::DMA_PER_WAVE; ++i)
     g_off[i] = dma_src_off<C::LW, D>((w * C::DMA_PER_WAVE + i) * 64 + lane, kv_row_bytes);
-  // Sharded: tiles are loaded in order, so the resources move to the next
-  // shard only when the tiles of the current one are used up.
-  uint32_t sh_tiles = 0, sh_base = 0;
   auto load_tile = [&](int t) __attribute__((always_inline)) {
     const uint32_t ks = smem_lds + (t % kStages) * C::TILE_BYTES;
-    uint32_t base = (uint32_t)(t * kDQN) * kv_row_bytes;
-    if constexpr (SH) {
-      if (sh_tiles == 0) {  // wave-uniform; tile t is the first of its shard
-        uint32_t tl;
-        rk = make_rsrc_words(view_row<true, const uint16_t>(kv, beta, t * kDQN, kvh, D, tl),
-                             tl * kv_row_bytes);
-        rv = make_rsrc_words(view_row<true, const uint16_t>(vv, beta, t * kDQN, kvh, D, tl),
-                             tl * kv_row_bytes);
-        sh_tiles = tl / kDQN;
-        sh_base = 0;
-      }
-      base = sh_base;
-      sh_base += kDQN * kv_row_bytes;
-      --sh_tiles;
-    }
+    const uint32_t base = (uint32_t)(t * kDQN) * kv_row_bytes;
 #pragma unroll
     for (int i = 0; i < C::DMA_PER_WAVE; ++i) {
       const uint32_t lds = ks + (w * C::DMA_PER_WAVE + i) * 1024;

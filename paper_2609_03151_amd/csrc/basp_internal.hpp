@@ -220,7 +220,8 @@ inline size_t attn_bwd_workspace_bytes(const AttnShape &s) {
 // for the null stream), looked up once per device.  Allocates nothing.
 hipError_t noalloc_scratch(hipStream_t stream, void **ptr);
 
-// q and d_o must be one-buffer (local) views, also when `sharded`.
+// q, k, v and d_o must be one-buffer (local) views, also when `sharded`
+// (then only o and the gradients are shard views).
 hipError_t launch_attn_bwd(const RowView &q, const RowView &k, const RowView &v,
                            const RowView &o, const float *lse, const RowView &d_o,
                            const RowView &dq, const RowView &dk, const RowView &dv,

@@ -257,7 +257,9 @@ int main() {
          BASP_OK);
   CHECK(basp::g_sharded && basp::g_attn.Hl == 2 && basp::g_attn.Hkl == 1);
   const size_t need_s = basp_attn_bwd_sharded_workspace_bytes(1, 4096, 8, 4, 128, 4);
-  CHECK(need_s == basp_attn_bwd_workspace_bytes(1, 4096, 8, 4, 128, 4) + 2ull * 4096 * 2 * 128 * 2);
+  // local copies: Q and dO (2 heads each), K and V (1 head each), bf16
+  CHECK(need_s == basp_attn_bwd_workspace_bytes(1, 4096, 8, 4, 128, 4) + 2ull * 4096 * 2 * 128 * 2 +
+                      2ull * 4096 * 1 * 128 * 2);
   CHECK(basp_attn_bwd_sharded_workspace_bytes(0, 4096, 8, 4, 128, 4) == 0);
   EXPECT(basp_attn_bwd_sharded(tq, tk, tv, to, lse, td, (float *const *)tdq, (float *const *)tdk,
                                (float *const *)tdv, p[9], need_s - 16, 1, 4096, 8, 4, 128, 4, 1,
