@@ -242,31 +242,50 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
   // kinds run in separate inner loops, so that each keeps one set of
   // accumulator registers.
   const int nmask_ph = kv_masked_steps(k0, r_lo, steps_per_head, kQM);
-  auto step_coords = [&](int st, int &h, int &i0) __attribute__((always_inline)) {
-    const int hr = st / steps_per_head;
-    h = kvh * n_rep + hr;
-    i0 = r_lo + (st - hr * steps_per_head) * kQM;
+  // Copy state.  Steps are copied strictly in order (two ahead of use): the
+  // next one to copy is step ld_t of head ld_hr of the group, first row
+  // ld_i0, and rq, rd, ra are its resources (Q and dO rows from ld_i0 on,
+  // the head's (LSE2, D) pairs).  They advance by one step's rows at a time
+  // and are rebuilt per head, so a step costs a few scalar additions.
+  int ld_hr = 0, ld_t = 0, ld_i0 = r_lo;
+  u32x4 rq, rd, ra;
+  auto head_resources = [&]() __attribute__((always_inline)) {
+    const int h = kvh * n_rep + ld_hr;
+    uint32_t left;  // rows from r_lo to the sequence's end; rows past it read as zeros
+    rq = make_rsrc_words(view_row<false, const uint16_t>(qv, beta, r_lo, h, D, left),
+                         left * q_row_bytes);
+    rd = make_rsrc_words(view_row<false, const uint16_t>(dov, beta, r_lo, h, D, left),
+                         left * q_row_bytes);
+    ra = make_rsrc_words(ld + ((size_t)beta * Hl + h) * S, (uint32_t)S * 8);
   };
-  // Copies of step st into stage st % kStages: Q and dO tiles (every wave its
-  // share), the rows' (LSE2, D) pairs (wave 0, 1 KB of which 512 B are used).
+  auto advance = [&](u32x4 &r, uint32_t bytes) __attribute__((always_inline)) {
+    const uint64_t a = (((uint64_t)r[1] << 32) | r[0]) + bytes;  // 48-bit base, stride 0
+    r[0] = (uint32_t)a;
+    r[1] = (uint32_t)(a >> 32);
+    r[2] -= bytes;  // rows left from the new first row (at least one)
+  };
+  head_resources();
+  // Copies of the next step (index st, stage st % kStages): Q and dO tiles
+  // (every wave its share), the rows' (LSE2, D) pairs (wave 0, 1 KB of
+  // which 512 B are used).
   auto load_step = [&](int st) __attribute__((always_inline)) {
-    int h, i0;
-    step_coords(st, h, i0);
-    uint32_t left;  // the step's rows; rows past the buffer's end read as zeros
-    const u32x4 rq = make_rsrc_words(view_row<false, const uint16_t>(qv, beta, i0, h, D, left),
-                                     left * q_row_bytes);
-    const u32x4 rd = make_rsrc_words(view_row<false, const uint16_t>(dov, beta, i0, h, D, left),
-                                     left * q_row_bytes);
-    const uint32_t stage = smem_lds + (st % kStages) * C::STAGE_BYTES;
+    const uint32_t stage = smem_lds + ((uint32_t)st % kStages) * C::STAGE_BYTES;
 #pragma unroll
     for (int i = 0; i < C::DMA_PER_WAVE; ++i) {
       const uint32_t lds = stage + (w * C::DMA_PER_WAVE + i) * 1024;
       buf_load16_lds_async(rq, g_off[i], lds);
       buf_load16_lds_async(rd, g_off[i], lds + C::TILE_BYTES);
     }
-    if (w == 0) {
-      const u32x4 ra = make_rsrc_words(ld + ((size_t)beta * Hl + h) * S, (uint32_t)S * 8);
-      buf_load16_lds_async(ra, (uint32_t)i0 * 8 + lane * 16, stage + 2 * C::TILE_BYTES);
+    if (w == 0)
+      buf_load16_lds_async(ra, (uint32_t)ld_i0 * 8 + lane * 16, stage + 2 * C::TILE_BYTES);
+    if (++ld_t == steps_per_head) {  // wave-uniform
+      ld_t = 0;
+      ld_i0 = r_lo;
+      if (++ld_hr < n_rep) head_resources();
+    } else {
+      ld_i0 += kQM;
+      advance(rq, kQM * q_row_bytes);
+      advance(rd, kQM * q_row_bytes);
     }
   };
   // This wave's copies of step st landed, with `ahead` later steps in flight.
