@@ -32,9 +32,13 @@ FLAGS = [
 
 # Per-file flags.  The key-stationary backward keeps its accumulators in
 # AGPRs (inline asm); the compiler's own MFMAs there must stay in VGPR form,
-# or their results are copied out of AGPRs on every step.
+# or their results are copied out of AGPRs on every step.  Its woven step is
+# one long fully unrolled body: past the default size limit of `#pragma
+# unroll` the compiler keeps the inner loops, and their arrays then go to
+# scratch memory.
 FILE_FLAGS = {
-    "basp_attn_bwd.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
+    "basp_attn_bwd.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1",
+                          "-mllvm", "-pragma-unroll-threshold=1000000"],
 }
 
 

@@ -9,7 +9,8 @@
 //   dK_j  = scale sum_{h in group} sum_{i>=j} dS_ij q_i
 //   dQ_i  = scale sum_{j<=i} dS_ij k_j
 // Kernels, all deterministic (no atomics):
-//   bwd_pre    per (sequence, head, row): the pair (LSE in log2 units, D)
+//   bwd_pre    per (sequence, head, row): LSE in log2 units and -D, in two
+//              planes whose rows are padded to a multiple of 64 (zeros)
 //   bwd_kv     key-stationary, dV and dK together: a workgroup owns 128 keys
 //              of one kv head and sweeps the query rows at or after them (one
 //              row chunk of them), for every query head of the GQA group,
@@ -70,28 +71,32 @@ __device__ __forceinline__ void sched_reads_ahead() {
 }
 
 // ---------------------------------------------------------------- bwd_pre
-// One group of D/8 lanes per (beta, row, head); 16-byte loads of O and dO.
+// One group of D/8 lanes per (beta, row, head) of the padded planes, rows
+// r = (beta*Sp + i)*Hl + h; 16-byte loads of O and dO.  Writes
+//   lp[beta][h][i] = LSE * log2(e),  np[beta][h][i] = -D_i   (i < S)
+// and zeros for the padding rows S <= i < Sp.
 template <int D, bool SH>
 __global__ __launch_bounds__(kPreThreads) void bwd_pre_kernel(
-    const RowView ov, const RowView dov, const float *__restrict__ lse, f32x2 *__restrict__ ld,
-    long long rows /* b*S*Hl */, int S, int Hl) {
+    const RowView ov, const RowView dov, const float *__restrict__ lse, float *__restrict__ lp,
+    float *__restrict__ np, long long rows /* b*Sp*Hl */, int S, int Sp, int Hl) {
   constexpr int LPR = D <= 64 ? 8 : 16;  // lanes per row (a power of two >= D/8)
   const long long gid = (long long)blockIdx.x * kPreThreads + threadIdx.x;
   const long long r = gid / LPR;
   const int sub = (int)(gid % LPR);
+  const long long bi = r / Hl;
+  const int h = (int)(r - bi * Hl);
+  const int beta = (int)(bi / Sp), i = (int)(bi - (long long)beta * Sp);
   float acc = 0.f;
-  if (r < rows && sub < D / 8) {
+  if (r < rows && i < S && sub < D / 8) {
     const uint16_t *orow, *drow;
-    if constexpr (SH) {  // r = (beta*S + i)*Hl + h
-      const long long bi = r / Hl;
-      const int h = (int)(r - bi * Hl);
-      const int beta = (int)(bi / S), i = (int)(bi - (long long)beta * S);
+    if constexpr (SH) {
       uint32_t left;
       orow = view_row<true, const uint16_t>(ov, beta, i, h, D, left);
       drow = view_row<false, const uint16_t>(dov, beta, i, h, D, left);
-    } else {  // local [b][S][Hl][D]: row r is r*D elements in
-      orow = static_cast<const uint16_t *>(ov.p[0]) + r * D;
-      drow = static_cast<const uint16_t *>(dov.p[0]) + r * D;
+    } else {  // local [b][S][Hl][D]
+      const size_t e = (((size_t)beta * S + i) * Hl + h) * D;
+      orow = static_cast<const uint16_t *>(ov.p[0]) + e;
+      drow = static_cast<const uint16_t *>(dov.p[0]) + e;
     }
     const u32x4 a = reinterpret_cast<const u32x4 *>(orow)[sub];
     const u32x4 b = reinterpret_cast<const u32x4 *>(drow)[sub];
@@ -104,13 +109,9 @@ __global__ __launch_bounds__(kPreThreads) void bwd_pre_kernel(
 #pragma unroll
   for (int off = LPR / 2; off > 0; off >>= 1) acc += __shfl_xor(acc, off, 64);
   if (r < rows && sub == 0) {
-    // r = (beta*S + i)*Hl + h  ->  LD[beta][h][i]
-    const long long bi = r / Hl;
-    const int h = (int)(r - bi * Hl);
-    const long long beta = bi / S;
-    const int i = (int)(bi - beta * S);
-    const size_t idx = (size_t)(beta * Hl + h) * S + i;
-    ld[idx] = f32x2{lse[idx] * kLog2e, acc};
+    const size_t row = (size_t)beta * Hl + h;
+    lp[row * Sp + i] = i < S ? lse[row * S + i] * kLog2e : 0.f;
+    np[row * Sp + i] = i < S ? -acc : 0.f;
   }
 }
 
@@ -146,7 +147,7 @@ struct KvCfg {
   static constexpr int DC = HeadDim<D>::DC;  // computed width (columns past D are zero)
   static constexpr int LW = HeadDim<D>::LW;  // LDS row layout
   static constexpr int TILE_BYTES = kQM * LW * 2;
-  static constexpr int AUX_BYTES = 1024;  // (LSE2, D) of the step's rows (first 512 B)
+  static constexpr int AUX_BYTES = 1024;  // LSE2, then -D, of the step's 64 rows (first 512 B)
   static constexpr int STAGE_BYTES = 2 * TILE_BYTES + AUX_BYTES;  // Q, dO, aux
   static constexpr int NS = DC / 16;
   static constexpr int NE = DC / 32;
@@ -160,9 +161,10 @@ struct KvCfg {
 template <int D, bool SH>
 __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
     const RowView qv, const RowView kv, const RowView vv, const RowView dov,
-    const f32x2 *__restrict__ ld, const RowView dvv, const RowView dkv, size_t chunk_elems, int S,
-    int Hl, int Hkl, int n_rep, int kvheads_total, int ktiles, int nchunks, int chunk_tiles,
-    float c /* scale*log2e */, float dk_scale) {
+    const float *__restrict__ lp, uint32_t plane_bytes /* np - lp */, const RowView dvv,
+    const RowView dkv, size_t chunk_elems, int S, int Sp, int Hl, int Hkl, int n_rep,
+    int kvheads_total, int ktiles, int nchunks, int chunk_tiles, float c /* scale*log2e */,
+    float dk_scale) {
   using C = KvCfg<D>;
   using T = LdsTile<C::LW>;
   __shared__ __attribute__((aligned(16))) unsigned char smem[kStages * C::STAGE_BYTES];
@@ -249,6 +251,12 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
   // and are rebuilt per head, so a step costs a few scalar additions.
   int ld_hr = 0, ld_t = 0, ld_i0 = r_lo;
   u32x4 rq, rd, ra;
+  // Lanes 0-15 copy the step's 64 LSE2 values, lanes 16-31 its 64 -D
+  // values (the padded planes hold every row the steps reach); the other
+  // lanes read zeros.
+  const uint32_t aux_lane_off = lane < 16   ? 16u * lane
+                                : lane < 32 ? plane_bytes + 16u * (lane - 16)
+                                            : kZeroOffset;
   auto head_resources = [&]() __attribute__((always_inline)) {
     const int h = kvh * n_rep + ld_hr;
     uint32_t left;  // rows from r_lo to the sequence's end; rows past it read as zeros
@@ -256,7 +264,7 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
                          left * q_row_bytes);
     rd = make_rsrc_words(view_row<false, const uint16_t>(dov, beta, r_lo, h, D, left),
                          left * q_row_bytes);
-    ra = make_rsrc_words(ld + ((size_t)beta * Hl + h) * S, (uint32_t)S * 8);
+    ra = make_rsrc_words(lp + ((size_t)beta * Hl + h) * Sp, plane_bytes + (uint32_t)Sp * 4);
   };
   auto advance = [&](u32x4 &r, uint32_t bytes) __attribute__((always_inline)) {
     const uint64_t a = (((uint64_t)r[1] << 32) | r[0]) + bytes;  // 48-bit base, stride 0
@@ -277,7 +285,7 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
       buf_load16_lds_async(rd, g_off[i], lds + C::TILE_BYTES);
     }
     if (w == 0)
-      buf_load16_lds_async(ra, (uint32_t)ld_i0 * 8 + lane * 16, stage + 2 * C::TILE_BYTES);
+      buf_load16_lds_async(ra, aux_lane_off + (uint32_t)ld_i0 * 4, stage + 2 * C::TILE_BYTES);
     if (++ld_t == steps_per_head) {  // wave-uniform
       ld_t = 0;
       ld_i0 = r_lo;
@@ -304,40 +312,47 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
 
   // ---- the pieces of a step (half m of the stage at Qs)
   // S^T and dP^T of half m: 2 NS products, each with one 16-byte LDS read.
+  // The step's aux block holds LSE2 of its 64 rows, then their -D.  The 16
+  // rows of half m a lane's accumulator registers hold, 32m + 8g + 4hh +
+  // {0..3} for register 4g + {0..3}, are four 16-byte reads of either part.
+  auto aux_rows = [&](const unsigned char *Qs, int part, int m) __attribute__((always_inline)) {
+    const float *a = reinterpret_cast<const float *>(Qs + 2 * C::TILE_BYTES) + 64 * part;
+    f32x16 v;
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const f32x4 x = *reinterpret_cast<const f32x4 *>(a + 32 * m + 8 * g + 4 * hh);
+#pragma unroll
+      for (int y = 0; y < 4; ++y) v[4 * g + y] = x[y];
+    }
+    return v;
+  };
+  // S^T and dP^T of half m: 2 NS products, each with one 16-byte LDS read;
+  // dP^T starts from -D, so that it ends as dP - D.
   auto scores = [&](const unsigned char *Qs, int m, f32x16 &sacc, f32x16 &pacc)
       __attribute__((always_inline)) {
     const unsigned char *dOs = Qs + C::TILE_BYTES;
+    const f32x16 negd = aux_rows(Qs, 1, m);
 #pragma unroll
     for (int s = 0; s < C::NS; ++s) {
       const bf16x8 aq = *reinterpret_cast<const bf16x8 *>(Qs + a_off[s] + m * 32 * T::ROW_BYTES);
       const bf16x8 ad = *reinterpret_cast<const bf16x8 *>(dOs + a_off[s] + m * 32 * T::ROW_BYTES);
       sacc = mfma32x32x16(aq, kf[s], s == 0 ? f32x16{} : sacc);
-      pacc = mfma32x32x16(ad, vf[s], s == 0 ? f32x16{} : pacc);
+      pacc = mfma32x32x16(ad, vf[s], s == 0 ? negd : pacc);
     }
   };
   // P and dS of half m as bf16 B operands along the rows: block s2 covers rows
-  // 32m + 16*s2 .. +15, slot t <-> register 8*s2 + t.  Row 32m + 8g + 4hh + x
-  // of the step holds (LSE2, D) at aux[2 * row].  lim: rows of the half whose
-  // offset is below lim precede the key (masked); 0 for none.
+  // 32m + 16*s2 .. +15, slot t <-> register 8*s2 + t.  lim: rows of the half
+  // whose offset is below lim precede the key (masked); 0 for none.
   auto elementwise = [&](const unsigned char *Qs, int m, f32x16 &sacc, const f32x16 &pacc,
                          int lim, bf16x8 *bp, bf16x8 *bds) __attribute__((always_inline)) {
-    const float *aux = reinterpret_cast<const float *>(Qs + 2 * C::TILE_BYTES);
+    const f32x16 lse2 = aux_rows(Qs, 0, m);
     float ds[16];
 #pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      const int rr = 32 * m + 8 * g + 4 * hh;
-#pragma unroll
-      for (int x2 = 0; x2 < 2; ++x2) {
-        const f32x4 a = *reinterpret_cast<const f32x4 *>(aux + 2 * rr + 4 * x2);
-#pragma unroll
-        for (int y = 0; y < 2; ++y) {
-          const int r = 4 * g + 2 * x2 + y;
-          float p = fast_exp2(fmaf(sacc[r], c, -a[2 * y]));
-          if (8 * (r >> 2) + (r & 3) < lim) p = 0.f;
-          sacc[r] = p;
-          ds[r] = p * (pacc[r] - a[2 * y + 1]);
-        }
-      }
+    for (int r = 0; r < 16; ++r) {
+      float p = fast_exp2(fmaf(sacc[r], c, -lse2[r]));
+      if (8 * (r >> 2) + (r & 3) < lim) p = 0.f;
+      sacc[r] = p;
+      ds[r] = p * pacc[r];
     }
 #pragma unroll
     for (int s2 = 0; s2 < 2; ++s2) {
@@ -380,7 +395,6 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
     static_assert(2 * C::NS == NB, "score and accumulate blocks have equal length");
     constexpr int NG = 4 * NB;
     const unsigned char *dOs = Qs + C::TILE_BYTES;
-    const float *aux = reinterpret_cast<const float *>(Qs + 2 * C::TILE_BYTES);
     bf16x8 opnd[NG];
     auto load_opnd = [&](int g) __attribute__((always_inline)) {
       const int blk = g / NB, j = g % NB;
@@ -396,19 +410,11 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
     f32x16 sc[2], pc[2];      // S^T and dP^T of each half
     bf16x8 bp[2][2], bds[2][2];
     float pv[16], dv[16];
-    f32x4 ax[8];
-    auto load_aux = [&](int me) __attribute__((always_inline)) {
-#pragma unroll
-      for (int q = 0; q < 8; ++q)
-        ax[q] = *reinterpret_cast<const f32x4 *>(
-            aux + 2 * (32 * me + 8 * (q >> 1) + 4 * hh) + 4 * (q & 1));
-    };
+    f32x16 lse2, negd0, negd1;  // LSE2 of the half in elementwise work; -D of each half
     auto element = [&](int me, int r) __attribute__((always_inline)) {
-      const f32x4 a = ax[r / 2];
-      const int y = r & 1;
-      const float pr = fast_exp2(fmaf(sc[me][r], c, -a[2 * y]));
+      const float pr = fast_exp2(fmaf(sc[me][r], c, -lse2[r]));
       pv[r] = pr;
-      dv[r] = pr * (pc[me][r] - a[2 * y + 1]);
+      dv[r] = pr * pc[me][r];  // dP^T started from -D
       if (r & 1) {  // registers r-1, r -> dword (r % 8) / 2 of block r / 8
         const int b = r / 8, dw = (r % 8) / 2;
         reinterpret_cast<uint32_t *>(&bp[me][b])[dw] = pack_bf16x2(pv[r - 1], pv[r]);
@@ -417,14 +423,17 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
     };
 #pragma unroll
     for (int g = 0; g < kPf; ++g) load_opnd(g);
+    negd0 = aux_rows(Qs, 1, 0);  // for the first dP^T product, slot 1
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int g = 0; g < NG; ++g) {
       const int blk = g / NB, j = g % NB;
       if (g + kPf < NG) load_opnd(g + kPf);
+      if (blk == 0 && j == 2) negd1 = aux_rows(Qs, 1, 1);
       if (blk < 2) {
         const int s = j / 2;
-        if (j & 1) pc[blk] = mfma32x32x16(opnd[g], vf[s], s == 0 ? f32x16{} : pc[blk]);
+        if (j & 1)
+          pc[blk] = mfma32x32x16(opnd[g], vf[s], s == 0 ? (blk == 0 ? negd0 : negd1) : pc[blk]);
         else sc[blk] = mfma32x32x16(opnd[g], kf[s], s == 0 ? f32x16{} : sc[blk]);
       } else {
         const int n = j / 4, s2 = (j / 2) % 2, mh = blk - 2;
@@ -433,7 +442,7 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
       }
       if (blk == 1 || blk == 2) {  // elementwise of half blk-1
         const int me = blk - 1;
-        if (j == 0) load_aux(me);
+        if (j == 0) lse2 = aux_rows(Qs, 0, me);
         if (j >= kLag) {
 #pragma unroll
           for (int r = (j - kLag) * 16 / (NB - kLag); r < (j - kLag + 1) * 16 / (NB - kLag); ++r)
@@ -557,8 +566,8 @@ struct DqCfg {
 template <int D, bool SH>
 __global__ __launch_bounds__(kDqThreads, 1) void bwd_dq_kernel(
     const RowView qv, const RowView kv, const RowView vv, const RowView dov,
-    const f32x2 *__restrict__ ld, const RowView dqv, int S, int Hl, int n_rep, int heads_total,
-    int qtiles, float c, float scale) {
+    const float *__restrict__ lp, const float *__restrict__ np, const RowView dqv, int S, int Sp,
+    int Hl, int n_rep, int heads_total, int qtiles, float c, float scale) {
   using C = DqCfg<D>;
   using T = LdsTile<C::LW>;
   // LDS: the K tiles of the kStages ring stages, then their V tiles; with
@@ -603,13 +612,17 @@ __global__ __launch_bounds__(kDqThreads, 1) void bwd_dq_kernel(
       df[s] = bf16x8{};
     }
   }
-  f32x2 ldr = {INFINITY, 0.f};  // rows past S: P = 0
-  if (row < S) ldr = ld[((size_t)beta * Hl + h) * S + row];
-  const float lse2 = ldr[0], Drow = ldr[1];
+  float lse2 = INFINITY, nd = 0.f;  // rows past S: P = 0
+  if (row < S) {
+    lse2 = lp[((size_t)beta * Hl + h) * Sp + row];
+    nd = np[((size_t)beta * Hl + h) * Sp + row];
+  }
   // dP^T starts from -D (the accumulator's initial value), so dS = P dP'.
+  // (At d = 64 the 16 registers this takes leave room for one workgroup per
+  // CU instead of two; measured faster all the same.)
   f32x16 negd;
 #pragma unroll
-  for (int r = 0; r < 16; ++r) negd[r] = -Drow;
+  for (int r = 0; r < 16; ++r) negd[r] = nd;
   wait_vmcnt<0>();  // retire the tracked loads before untracked copies start
 
   const int kv_end = min(S, q0 + kDQM);
@@ -775,15 +788,19 @@ hipError_t launch_bwd_d(const RowView &q, const RowView &k, const RowView &v, co
                         const float *lse, const RowView &d_o, const RowView &dq,
                         const RowView &dk, const RowView &dv, float *ws, const AttnShape &s,
                         hipStream_t stream) {
-  auto *ld = reinterpret_cast<f32x2 *>(ws);
+  // LSE2 and -D planes, rows padded to a multiple of 64 (every row a
+  // key-stationary step reaches).
+  const int Sp = bwd_plane_rows(s.S);
+  float *lp = ws, *np = ws + (size_t)s.b * s.Hl * Sp;
+  const uint32_t plane_bytes = (uint32_t)((size_t)s.b * s.Hl * Sp * 4);
   const float c = s.scale * kLog2e;
   const int n_rep = s.Hl / s.Hkl;
 
-  const long long rows = (long long)s.b * s.S * s.Hl;
+  const long long rows = (long long)s.b * Sp * s.Hl;
   const long long pre_threads = rows * (D <= 64 ? 8 : 16);
   const long long pre_blocks = (pre_threads + kPreThreads - 1) / kPreThreads;
   hipLaunchKernelGGL((bwd_pre_kernel<D, SH>), dim3((unsigned)pre_blocks), dim3(kPreThreads), 0,
-                     stream, o, d_o, lse, ld, rows, s.S, s.Hl);
+                     stream, o, d_o, lse, lp, np, rows, s.S, Sp, s.Hl);
 
   const int ktiles = (s.S + kKN - 1) / kKN;
   const int kvheads_total = s.b * s.Hkl;
@@ -800,8 +817,8 @@ hipError_t launch_bwd_d(const RowView &q, const RowView &k, const RowView &v, co
     dk_out = local_view(dk_part, s.S, s.Hkl, D);
   }
   hipLaunchKernelGGL((bwd_kv_kernel<D, SH>), kv_grid, dim3(kKvThreads), 0, stream, q, k, v, d_o,
-                     ld, dv_out, dk_out, chunk_elems, s.S, s.Hl, s.Hkl, n_rep, kvheads_total,
-                     ktiles, ck.n, ck.T, c, s.scale);
+                     lp, plane_bytes, dv_out, dk_out, chunk_elems, s.S, Sp, s.Hl, s.Hkl, n_rep,
+                     kvheads_total, ktiles, ck.n, ck.T, c, s.scale);
   if (ck.n > 1) {
     const uint32_t row_quads = (uint32_t)(s.Hkl * D / 4);
     const uint32_t seq_quads = (uint32_t)s.S * row_quads;
@@ -816,8 +833,8 @@ hipError_t launch_bwd_d(const RowView &q, const RowView &k, const RowView &v, co
   const int qtiles = (s.S + kDQM - 1) / kDQM;
   const int heads_total = s.b * s.Hl;
   hipLaunchKernelGGL((bwd_dq_kernel<D, SH>), dim3((unsigned)(qtiles * heads_total)),
-                     dim3(kDqThreads), 0, stream, q, k, v, d_o, ld, dq, s.S, s.Hl, n_rep,
-                     heads_total, qtiles, c, s.scale);
+                     dim3(kDqThreads), 0, stream, q, k, v, d_o, lp, np, dq, s.S, Sp, s.Hl,
+                     n_rep, heads_total, qtiles, c, s.scale);
   return hipGetLastError();
 }
 

@@ -185,9 +185,10 @@ hipError_t launch_attn_fwd(const RowView &q, const RowView &k, const RowView &v,
                            const RowView &o, float *lse, const AttnShape &s, bool sharded,
                            hipStream_t stream);
 
-// Workspace of the backward: LD [b][Hl][S] of (LSE * log2(e), D), then, when
-// the key pass runs in more than one row chunk, the dV and dK partial sums
-// [chunk][b][S][Hkl][d] (fp32).  Host-callable.
+// Workspace of the backward: the planes LSE * log2(e) and -D, each
+// [b][Hl][Sp] fp32 with Sp = S rounded up to 64 (padding rows zero), then,
+// when the key pass runs in more than one row chunk, the dV and dK partial
+// sums [chunk][b][S][Hkl][d] (fp32).  Host-callable.
 struct BwdChunks {
   int rows;   // rows per chunk (a multiple of kKvKeys)
   int T;      // key tiles per chunk
@@ -196,6 +197,8 @@ struct BwdChunks {
   size_t part_offset_floats;
 };
 
+__host__ __device__ inline int bwd_plane_rows(int S) { return (S + 63) / 64 * 64; }
+
 inline BwdChunks bwd_chunks(const AttnShape &s) {
   BwdChunks ck;
   ck.rows = kv_chunk_rows(s.S);
@@ -203,7 +206,7 @@ inline BwdChunks bwd_chunks(const AttnShape &s) {
   ck.n = (s.S + ck.rows - 1) / ck.rows;
   if (ck.n < 1) ck.n = 1;
   ck.units = kv_units(ck.n, ck.T);
-  const size_t ld_floats = 2 * (size_t)s.b * s.Hl * s.S;
+  const size_t ld_floats = 2 * (size_t)s.b * s.Hl * bwd_plane_rows(s.S);
   ck.part_offset_floats = (ld_floats + 63) & ~(size_t)63;  // 256-byte aligned
   return ck;
 }
