@@ -296,18 +296,14 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
       advance(rd, kQM * q_row_bytes);
     }
   };
-  // This wave's copies of step st landed, with `ahead` later steps in flight.
-  auto wait_step = [&](int ahead) __attribute__((always_inline)) {
+  // This wave's copies of step st landed, with the next two steps' in flight.
+  // (Two steps ahead: wave 0 has 2(N+1) later copies in flight, the others
+  // 2N.  For the last two steps of the unit it waits for everything, which
+  // holds back at most one step's copies once per unit.)
+  auto wait_step_ahead2 = [&]() __attribute__((always_inline)) {
     constexpr int N = 2 * C::DMA_PER_WAVE;
-    if (w == 0) {
-      if (ahead >= 2) wait_vmcnt<2 * (N + 1)>();
-      else if (ahead == 1) wait_vmcnt<N + 1>();
-      else wait_vmcnt<0>();
-    } else {
-      if (ahead >= 2) wait_vmcnt<2 * N>();
-      else if (ahead == 1) wait_vmcnt<N>();
-      else wait_vmcnt<0>();
-    }
+    if (w == 0) wait_vmcnt<2 * (N + 1)>();
+    else wait_vmcnt<2 * N>();
   };
 
   // ---- the pieces of a step (half m of the stage at Qs)
@@ -457,8 +453,12 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
   // Stage (st+2) % 4 last held step st-2, finished by every wave before the
   // barrier of step st-1.
   auto begin_step = [&](int st) __attribute__((always_inline)) {
-    if (st + 2 < nsteps) load_step(st + 2);
-    wait_step(min(2, nsteps - 1 - st));
+    if (st + 2 < nsteps) {
+      load_step(st + 2);
+      wait_step_ahead2();
+    } else {
+      wait_vmcnt<0>();
+    }
     barrier_no_fence();
   };
   int st = 0;
