@@ -412,7 +412,10 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
     make_visible(min(1, nt - 2 - t), t + kPD + 1);  // tile t+1 readable, t+2 in flight
     asm volatile("" : "+v"(m_ref));  // keep the exponent arguments here
     bf16x8 pf[kBN / 16];
-    // Block X: scores of tile t+1 (16 products), exponentials of tile t.
+    // Block X: scores of tile t+1 (16 products), exponentials of tile t, at
+    // raised issue priority: of the two waves of a SIMD, the one in this
+    // block keeps the matrix unit while the other is in block Y.
+    wave_priority<1>();
     {
       constexpr int NG = 2 * C::NS;
       const unsigned char *Ks = smem + ((ST + 1) % kStages) * C::TILE_BYTES;
@@ -444,6 +447,7 @@ __global__ __launch_bounds__(kThreads, 1) void attn_fwd_kernel(
         __builtin_amdgcn_sched_barrier(0);
       }
     }
+    wave_priority<0>();
     // Block Y: P V of tile t (16 products), row sum of t, row maxima of t+1.
     float psum = 0.f, mx = -INFINITY;
     {
