@@ -642,12 +642,6 @@ __global__ __launch_bounds__(kDqThreads, 1) void bwd_dq_kernel(
       buf_load16_lds_async(rv, base + g_off[i], lds + kVRegion);
     }
   };
-  auto wait_tile = [&](int ahead) __attribute__((always_inline)) {
-    if (ahead >= 2) wait_vmcnt<4 * C::DMA_PER_WAVE>();
-    else if (ahead == 1) wait_vmcnt<2 * C::DMA_PER_WAVE>();
-    else wait_vmcnt<0>();
-  };
-
   // Row l32 (+32 for m = 1), chunk 2s + hh, of the K tile (a_off) and the V
   // tile (v_off).  With 64-wide rows the V region starts within reach of the
   // instruction immediate, so V takes the K offsets.
@@ -727,7 +721,7 @@ __global__ __launch_bounds__(kDqThreads, 1) void bwd_dq_kernel(
         sb[s2] = as_bf16x8(ts);
       }
       // dQ^T += K^T dS^T: M = head dim, N = rows, K = keys; K^T straight
-      // from the row-major K tile.  Raised priority, as in bwd_kv.
+      // from the row-major K tile, at raised issue priority (see the header).
       wave_priority<1>();
 #pragma unroll
       for (int n = 0; n < C::NE; ++n)
@@ -744,9 +738,14 @@ __global__ __launch_bounds__(kDqThreads, 1) void bwd_dq_kernel(
   };
   auto step = [&](int t) __attribute__((always_inline)) {
     // Stage (t+2) % 4 last held tile t-2, finished by every wave before the
-    // barrier of iteration t-1.
-    if (t + 2 < nt) load_tile(t + 2);
-    wait_tile(min(2, nt - 1 - t));
+    // barrier of iteration t-1.  With two tiles in flight the wait keeps
+    // them; the last two tiles wait for every copy.
+    if (t + 2 < nt) {
+      load_tile(t + 2);
+      wait_vmcnt<4 * C::DMA_PER_WAVE>();
+    } else {
+      wait_vmcnt<0>();
+    }
     barrier_no_fence();
   };
   for (int t = 0; t < 2 && t < nt; ++t) load_tile(t);
