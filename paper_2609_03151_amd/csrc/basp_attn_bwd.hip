@@ -25,9 +25,12 @@
 //     along the sequence (Q^T, dO^T, K^T) come from the same row-major LDS
 //     tiles through ds_read_b64_tr_b16, in the order the accumulator holds P
 //     and dS.
-//   * the streamed tiles (and, for bwd_kv, the rows' (LSE, D) pairs) are
+//   * the streamed tiles (and, for bwd_kv, the rows' LSE2 and -D) are
 //     copied HBM -> LDS by buffer loads that write LDS directly (rows past S
-//     arrive as zeros) into a ring of four stages, two steps ahead; each wave
+//     arrive as zeros): bwd_dq into a ring of four stages, two tiles ahead;
+//     bwd_kv into two stages, one step ahead (measured as fast, and its
+//     unmasked loop then runs two steps per iteration, one per stage, so
+//     every LDS address is a lane offset plus an immediate).  Each wave
 //     waits only for its own copies and passes a fence-free barrier.
 //   * bwd_kv runs one wave per SIMD (4 waves, 32 keys each) and weaves its
 //     elementwise work between its own products; bwd_dq runs two waves per
@@ -167,7 +170,13 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
     float dk_scale) {
   using C = KvCfg<D>;
   using T = LdsTile<C::LW>;
-  __shared__ __attribute__((aligned(16))) unsigned char smem[kStages * C::STAGE_BYTES];
+  // LDS: the Q tiles of the two ring stages, their dO tiles, their (LSE2,
+  // -D) blocks.  With one step body per stage, every operand address is a
+  // lane's fixed offset plus an instruction immediate.
+  constexpr int kKvStages = 2;
+  constexpr int kDoRegion = kKvStages * C::TILE_BYTES;
+  constexpr int kAuxRegion = 2 * kKvStages * C::TILE_BYTES;
+  __shared__ __attribute__((aligned(16))) unsigned char smem[kKvStages * C::STAGE_BYTES];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -239,6 +248,23 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
       asm volatile("" : "+v"(t_off[n][x]));
     }
 
+  // Byte offset of this lane's first (LSE2, -D) value in a stage's aux block
+  // (rows 4hh..), from the LDS base.
+  int aux_lane = kAuxRegion + 16 * hh;
+  asm volatile("" : "+v"(aux_lane));
+  // Opaque to loop-invariant code motion: offset + stage constant stays one
+  // instruction's immediate instead of a hoisted register per stage.
+  auto launder_offsets = [&]() __attribute__((always_inline)) {
+#pragma unroll
+    for (int s = 0; s < C::NS; ++s) asm volatile("" : "+v"(a_off[s]));
+#pragma unroll
+    for (int n = 0; n < C::NE; ++n) {
+      asm volatile("" : "+v"(t_off[n][0]));
+      asm volatile("" : "+v"(t_off[n][1]));
+    }
+    asm volatile("" : "+v"(aux_lane));
+  };
+
   // Within each head, the first nmask_ph row steps overlap some wave's keys
   // and take the masked path; the rest need no mask in any wave.  The two
   // kinds run in separate inner loops, so that each keeps one set of
@@ -273,19 +299,21 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
     r[2] -= bytes;  // rows left from the new first row (at least one)
   };
   head_resources();
-  // Copies of the next step (index st, stage st % kStages): Q and dO tiles
-  // (every wave its share), the rows' (LSE2, D) pairs (wave 0, 1 KB of
-  // which 512 B are used).
+  // Copies of the next step (index st, ring stage st % 2): Q and dO tiles
+  // (every wave its share), the rows' LSE2 and -D (wave 0, 1 KB of which
+  // 512 B are used).
   auto load_step = [&](int st) __attribute__((always_inline)) {
-    const uint32_t stage = smem_lds + ((uint32_t)st % kStages) * C::STAGE_BYTES;
+    const uint32_t sq = (uint32_t)st % kKvStages;
+    const uint32_t stage = smem_lds + sq * C::TILE_BYTES;
 #pragma unroll
     for (int i = 0; i < C::DMA_PER_WAVE; ++i) {
       const uint32_t lds = stage + (w * C::DMA_PER_WAVE + i) * 1024;
       buf_load16_lds_async(rq, g_off[i], lds);
-      buf_load16_lds_async(rd, g_off[i], lds + C::TILE_BYTES);
+      buf_load16_lds_async(rd, g_off[i], lds + kDoRegion);
     }
     if (w == 0)
-      buf_load16_lds_async(ra, aux_lane_off + (uint32_t)ld_i0 * 4, stage + 2 * C::TILE_BYTES);
+      buf_load16_lds_async(ra, aux_lane_off + (uint32_t)ld_i0 * 4,
+                           smem_lds + kAuxRegion + sq * C::AUX_BYTES);
     if (++ld_t == steps_per_head) {  // wave-uniform
       ld_t = 0;
       ld_i0 = r_lo;
@@ -296,27 +324,16 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
       advance(rd, kQM * q_row_bytes);
     }
   };
-  // This wave's copies of step st landed, with the next two steps' in flight.
-  // (Two steps ahead: wave 0 has 2(N+1) later copies in flight, the others
-  // 2N.  For the last two steps of the unit it waits for everything, which
-  // holds back at most one step's copies once per unit.)
-  auto wait_step_ahead2 = [&]() __attribute__((always_inline)) {
-    constexpr int N = 2 * C::DMA_PER_WAVE;
-    if (w == 0) wait_vmcnt<2 * (N + 1)>();
-    else wait_vmcnt<2 * N>();
-  };
-
-  // ---- the pieces of a step (half m of the stage at Qs)
-  // S^T and dP^T of half m: 2 NS products, each with one 16-byte LDS read.
+  // ---- the pieces of a step (half m of ring stage stg)
   // The step's aux block holds LSE2 of its 64 rows, then their -D.  The 16
   // rows of half m a lane's accumulator registers hold, 32m + 8g + 4hh +
   // {0..3} for register 4g + {0..3}, are four 16-byte reads of either part.
-  auto aux_rows = [&](const unsigned char *Qs, int part, int m) __attribute__((always_inline)) {
-    const float *a = reinterpret_cast<const float *>(Qs + 2 * C::TILE_BYTES) + 64 * part;
+  auto aux_rows = [&](int stg, int part, int m) __attribute__((always_inline)) {
+    const unsigned char *a = smem + aux_lane + stg * C::AUX_BYTES + 256 * part;
     f32x16 v;
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
-      const f32x4 x = *reinterpret_cast<const f32x4 *>(a + 32 * m + 8 * g + 4 * hh);
+      const f32x4 x = *reinterpret_cast<const f32x4 *>(a + 4 * (32 * m + 8 * g));
 #pragma unroll
       for (int y = 0; y < 4; ++y) v[4 * g + y] = x[y];
     }
@@ -324,10 +341,9 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
   };
   // S^T and dP^T of half m: 2 NS products, each with one 16-byte LDS read;
   // dP^T starts from -D, so that it ends as dP - D.
-  auto scores = [&](const unsigned char *Qs, int m, f32x16 &sacc, f32x16 &pacc)
-      __attribute__((always_inline)) {
-    const unsigned char *dOs = Qs + C::TILE_BYTES;
-    const f32x16 negd = aux_rows(Qs, 1, m);
+  auto scores = [&](int stg, int m, f32x16 &sacc, f32x16 &pacc) __attribute__((always_inline)) {
+    const unsigned char *Qs = smem + stg * C::TILE_BYTES, *dOs = Qs + kDoRegion;
+    const f32x16 negd = aux_rows(stg, 1, m);
 #pragma unroll
     for (int s = 0; s < C::NS; ++s) {
       const bf16x8 aq = *reinterpret_cast<const bf16x8 *>(Qs + a_off[s] + m * 32 * T::ROW_BYTES);
@@ -339,9 +355,9 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
   // P and dS of half m as bf16 B operands along the rows: block s2 covers rows
   // 32m + 16*s2 .. +15, slot t <-> register 8*s2 + t.  lim: rows of the half
   // whose offset is below lim precede the key (masked); 0 for none.
-  auto elementwise = [&](const unsigned char *Qs, int m, f32x16 &sacc, const f32x16 &pacc,
-                         int lim, bf16x8 *bp, bf16x8 *bds) __attribute__((always_inline)) {
-    const f32x16 lse2 = aux_rows(Qs, 0, m);
+  auto elementwise = [&](int stg, int m, f32x16 &sacc, const f32x16 &pacc, int lim, bf16x8 *bp,
+                         bf16x8 *bds) __attribute__((always_inline)) {
+    const f32x16 lse2 = aux_rows(stg, 0, m);
     float ds[16];
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
@@ -363,9 +379,9 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
   };
   // dV^T += dO^T P and dK^T += Q^T dS over half m: 4 NE products, each with
   // two transposed LDS reads.
-  auto accumulate = [&](const unsigned char *Qs, int m, const bf16x8 *bp, const bf16x8 *bds)
+  auto accumulate = [&](int stg, int m, const bf16x8 *bp, const bf16x8 *bds)
       __attribute__((always_inline)) {
-    const unsigned char *dOs = Qs + C::TILE_BYTES;
+    const unsigned char *Qs = smem + stg * C::TILE_BYTES, *dOs = Qs + kDoRegion;
 #pragma unroll
     for (int n = 0; n < C::NE; ++n)
 #pragma unroll
@@ -386,11 +402,11 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
   // elementwise work of a half starts kLag slots into its block, after the
   // products it reads have finished.
   constexpr int kPf = 3, kLag = 2;
-  auto unmasked_step = [&](const unsigned char *Qs) __attribute__((always_inline)) {
+  auto unmasked_step = [&](int stg) __attribute__((always_inline)) {
     constexpr int NB = 4 * C::NE;  // products per block
     static_assert(2 * C::NS == NB, "score and accumulate blocks have equal length");
     constexpr int NG = 4 * NB;
-    const unsigned char *dOs = Qs + C::TILE_BYTES;
+    const unsigned char *Qs = smem + stg * C::TILE_BYTES, *dOs = Qs + kDoRegion;
     bf16x8 opnd[NG];
     auto load_opnd = [&](int g) __attribute__((always_inline)) {
       const int blk = g / NB, j = g % NB;
@@ -419,13 +435,13 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
     };
 #pragma unroll
     for (int g = 0; g < kPf; ++g) load_opnd(g);
-    negd0 = aux_rows(Qs, 1, 0);  // for the first dP^T product, slot 1
+    negd0 = aux_rows(stg, 1, 0);  // for the first dP^T product, slot 1
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int g = 0; g < NG; ++g) {
       const int blk = g / NB, j = g % NB;
       if (g + kPf < NG) load_opnd(g + kPf);
-      if (blk == 0 && j == 2) negd1 = aux_rows(Qs, 1, 1);
+      if (blk == 0 && j == 2) negd1 = aux_rows(stg, 1, 1);
       if (blk < 2) {
         const int s = j / 2;
         if (j & 1)
@@ -438,7 +454,7 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
       }
       if (blk == 1 || blk == 2) {  // elementwise of half blk-1
         const int me = blk - 1;
-        if (j == 0) lse2 = aux_rows(Qs, 0, me);
+        if (j == 0) lse2 = aux_rows(stg, 0, me);
         if (j >= kLag) {
 #pragma unroll
           for (int r = (j - kLag) * 16 / (NB - kLag); r < (j - kLag + 1) * 16 / (NB - kLag); ++r)
@@ -449,24 +465,20 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
     }
   };
 
-  for (int st = 0; st < 2 && st < nsteps; ++st) load_step(st);
-  // Stage (st+2) % 4 last held step st-2, finished by every wave before the
-  // barrier of step st-1.
+  load_step(0);
+  // Two stages: step st's copies landed (the only ones in flight), then the
+  // barrier, after which stage (st+1) % 2, last read in step st-1, is free.
   auto begin_step = [&](int st) __attribute__((always_inline)) {
-    if (st + 2 < nsteps) {
-      load_step(st + 2);
-      wait_step_ahead2();
-    } else {
-      wait_vmcnt<0>();
-    }
+    wait_vmcnt<0>();
     barrier_no_fence();
+    if (st + 1 < nsteps) load_step(st + 1);
   };
   int st = 0;
   for (int hr = 0; hr < n_rep; ++hr) {
     for (int t = 0; t < nmask_ph; ++t, ++st) {
       begin_step(st);
       const int i0 = r_lo + t * kQM;
-      const unsigned char *Qs = smem + (st % kStages) * C::STAGE_BYTES;
+      const int stg = st % kKvStages;
       // Halves in turn, masked; halves entirely before the keys skipped
       // (wave-uniform).
 #pragma unroll
@@ -474,22 +486,39 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
         if (i0 + 32 * m + 31 < wk0) continue;
         f32x16 sacc, pacc;
         bf16x8 bp[2], bds[2];
-        scores(Qs, m, sacc, pacc);
+        scores(stg, m, sacc, pacc);
         sched_reads_ahead<2 * C::NS, 1, 4>();
         __builtin_amdgcn_sched_barrier(0);
-        elementwise(Qs, m, sacc, pacc, key - i0 - 32 * m - 4 * hh, bp, bds);
+        elementwise(stg, m, sacc, pacc, key - i0 - 32 * m - 4 * hh, bp, bds);
         __builtin_amdgcn_sched_barrier(0);
         asm volatile("s_nop 1");
-        accumulate(Qs, m, bp, bds);
+        accumulate(stg, m, bp, bds);
         __builtin_amdgcn_sched_barrier(0);
       }
     }
     // The accumulators may be moved between the loops: cover the latency of
     // the last products before anything reads them.
     asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
-    for (int t = nmask_ph; t < steps_per_head; ++t, ++st) {
+    // Two steps per iteration, ring stages 0 and 1 (constant in each body);
+    // a step before and one after align the loop to even steps.
+    int t = nmask_ph;
+    if ((st & 1) && t < steps_per_head) {
       begin_step(st);
-      unmasked_step(smem + (st % kStages) * C::STAGE_BYTES);
+      unmasked_step(1);
+      ++t;
+      ++st;
+    }
+    for (; t + 1 < steps_per_head; t += 2, st += 2) {
+      launder_offsets();
+      begin_step(st);
+      unmasked_step(0);
+      begin_step(st + 1);
+      unmasked_step(1);
+    }
+    if (t < steps_per_head) {
+      begin_step(st);
+      unmasked_step(0);
+      ++st;
     }
     asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
   }
