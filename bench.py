@@ -216,14 +216,13 @@ def sharded_step_rate(sh, steps: int, flops: float) -> dict:
             "sharded_tflops": round(flops / (ms * 1e-3) / 1e12, 2)}
 
 
-def cold_permutation_rates(sh, reps: int = 5):
+def cold_permutation_rates(sh, reps: int = 51):
     """Each pack/unpack call of the step (the batched Q/K/V pack and gradient
     unpack, and the O unpack and dO pack), and each single-tensor permutation,
     timed alone with cold caches: a 1 GiB scratch write (larger than L2 and
-    the 256 MB MALL) precedes every timed call; the median of `reps` runs.  Also a plain device-to-device copy of
-    the largest permutation's size under the same conditions, as the
-    achievable HBM rate, and the send/receive-side permutations of the
-    owner's shard (basp_a2a_pack / basp_a2a_unpack) at the same shapes."""
+    the 256 MB MALL) precedes every timed call; the median of `reps` runs.
+    Also the send/receive-side permutations of the owner's shard
+    (basp_a2a_pack / basp_a2a_unpack) at the same shapes."""
     import statistics
     import torch
     scratch = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
