@@ -30,12 +30,11 @@ FLAGS = [
     f"-I{os.path.join(ROOT, 'include')}",
 ]
 
-# Per-file flags.  The key-stationary backward keeps its accumulators in
-# AGPRs (inline asm); the compiler's own MFMAs there must stay in VGPR form,
-# or their results are copied out of AGPRs on every step.  Its woven step is
-# one long fully unrolled body: past the default size limit of `#pragma
-# unroll` the compiler keeps the inner loops, and their arrays then go to
-# scratch memory.
+# Per-file flags.  The backward kernels run two waves per SIMD with every
+# accumulator in VGPRs: MFMAs stay in VGPR form (no copies between AGPRs and
+# the VALU), and the step bodies are unrolled fully, past the default size
+# limit of `#pragma unroll` (beyond it the compiler keeps inner loops whose
+# arrays go to scratch memory).  The timed kernels were built this way.
 FILE_FLAGS = {
     "basp_attn_bwd.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1",
                           "-mllvm", "-pragma-unroll-threshold=1000000"],

@@ -32,11 +32,10 @@
 //     unmasked loop then runs two steps per iteration, one per stage, so
 //     every LDS address is a lane offset plus an immediate).  Each wave
 //     waits only for its own copies and passes a fence-free barrier.
-//   * bwd_kv runs one wave per SIMD (4 waves, 32 keys each) and weaves its
-//     elementwise work between its own products; bwd_dq runs two waves per
-//     SIMD (8 waves, 32 rows each), which raise their issue priority over
-//     the accumulating products so that one wave's elementwise work overlaps
-//     the other's MFMAs.
+//   * both passes run two waves per SIMD (8 waves: bwd_kv 32 keys and one
+//     32-row half of each step per wave, bwd_dq 32 rows per wave), which
+//     raise their issue priority over the accumulating products so that one
+//     wave's elementwise work overlaps the other's MFMAs.
 //   * O and the gradients are addressed through row views: the local
 //     head-sharded tensors, or (SH) the G sequence shards of the exchange in
 //     place (row counts multiples of 256: a workgroup's rows or keys lie in
@@ -119,48 +118,40 @@ __global__ __launch_bounds__(kPreThreads) void bwd_pre_kernel(
 }
 
 // ------------------------------------------------------ bwd_kv (dV and dK)
-// Key-stationary, dV and dK in one pass.  A workgroup of 4 waves (one per
-// SIMD) owns 128 keys of one kv head, 32 per wave, and sweeps 64-row query
-// steps for all query heads of the GQA group.  Per 32-row half a wave forms
-//   S^T = K Q^T and dP^T = V dO^T              (K, V of its keys in registers)
+// Key-stationary, dV and dK in one pass.  A workgroup of 8 waves, two per
+// SIMD, owns 128 keys of one kv head and sweeps 64-row query steps for all
+// query heads of the GQA group.  Wave w takes keys 32 (w % 4) .. +31 and the
+// 32-row half w / 4 of every step, and forms
+//   S^T = K Q^T and dP^T = V dO^T       (K of its keys in registers; V too
+//                                        below d = 128, else from LDS)
 //   P = exp2(S c - LSE2),  dS = P (dP - D)
-//   dV^T += dO^T P  and  dK^T += Q^T dS         (accumulated in registers)
-// so S is formed once for both gradients.  With one wave per SIMD the wave
-// has the register file to itself (K, V, dV, dK and two halves in flight),
-// and its own instruction stream overlaps elementwise work with products:
-// the exponentials of one half are interleaved with the products of the
-// other.
-constexpr int kKvWaves = 4;
+//   dV^T += dO^T P  and  dK^T += Q^T dS  (accumulated in registers)
+// so S is formed once for both gradients.  The two waves of a key block
+// (w, w + 4, which share a SIMD) hold partial sums over their halves and add
+// them once per unit, through LDS, in that order.  Each wave raises its issue
+// priority over its accumulating products, so that the two waves of a SIMD
+// drift apart and one's elementwise work overlaps the other's MFMAs.
+constexpr int kKvWaves = 8;
 constexpr int kKvThreads = 64 * kKvWaves;
-constexpr int kKN = 32 * kKvWaves;  // keys per workgroup
+constexpr int kKN = 128;  // keys per workgroup (32 per key block)
 static_assert(kKN == kKvKeys, "work units assume 128 keys per workgroup");
-constexpr int kQM = 64;             // query rows per step (two 32-row halves)
-
-// acc += A B with the accumulator held in AGPRs (issued as inline asm: the
-// compiler's own MFMA form moves a loop-carried accumulator between AGPRs and
-// VGPRs on every iteration once the VGPRs run out).  A and B are VGPRs whose
-// producers (LDS reads, waited on by the compiler, or VALU conversions issued
-// well before) are at least two wait states back.
-__device__ __forceinline__ void mfma_acc(f32x16 &acc, bf16x8 a, bf16x8 b) {
-  asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
-}
+constexpr int kQM = 64;   // query rows per step (two 32-row halves)
 
 template <int D>
 struct KvCfg {
-  static constexpr int DC = HeadDim<D>::DC;  // computed width (columns past D are zero)
-  static constexpr int LW = HeadDim<D>::LW;  // LDS row layout
-  static constexpr int TILE_BYTES = kQM * LW * 2;
-  static constexpr int AUX_BYTES = 1024;  // LSE2, then -D, of the step's 64 rows (first 512 B)
-  static constexpr int STAGE_BYTES = 2 * TILE_BYTES + AUX_BYTES;  // Q, dO, aux
+  static constexpr int DC = HeadDim<D>::DC;
+  static constexpr int LW = HeadDim<D>::LW;
+  static constexpr int TILE_BYTES = kQM * LW * 2;   // a step's Q or dO rows
+  static constexpr int KT_BYTES = kKN * LW * 2;     // the workgroup's V rows
+  static constexpr int AUX_BYTES = 1024;            // LSE2, then -D, of the step's rows
   static constexpr int NS = DC / 16;
   static constexpr int NE = DC / 32;
   static constexpr int CPR = LW / 8;
-  static constexpr int DMA_PER_WAVE = kQM * CPR / kKvThreads;  // 1 KB copies per tile
+  static constexpr int DMA_PER_WAVE = kQM * CPR / kKvThreads;     // 1 KB copies per tile
+  static constexpr int KV_DMA_PER_WAVE = kKN * CPR / kKvThreads;  // for the V tile
+  static constexpr bool V_REGS = D < 128;  // V of the wave's keys fits in registers
 };
 
-// `dvv` / `dkv` are the final dV / dK when there is one row chunk, else the
-// partial buffers of chunk 0 (local views), chunk ch being ch * chunk_elems
-// further.
 template <int D, bool SH>
 __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
     const RowView qv, const RowView kv, const RowView vv, const RowView dov,
@@ -170,19 +161,22 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
     float dk_scale) {
   using C = KvCfg<D>;
   using T = LdsTile<C::LW>;
-  // LDS: the Q tiles of the two ring stages, their dO tiles, their (LSE2,
-  // -D) blocks.  With one step body per stage, every operand address is a
-  // lane's fixed offset plus an instruction immediate.
-  constexpr int kKvStages = 2;
-  constexpr int kDoRegion = kKvStages * C::TILE_BYTES;
-  constexpr int kAuxRegion = 2 * kKvStages * C::TILE_BYTES;
-  __shared__ __attribute__((aligned(16))) unsigned char smem[kKvStages * C::STAGE_BYTES];
+  // LDS: Q tiles of the two ring stages, their dO tiles, their (LSE2, -D)
+  // blocks, then (d = 128) the V tile of the workgroup's keys.  After the
+  // last step the same bytes hold the second waves' partial sums: 1 KB per
+  // (key block, tensor, register group).
+  constexpr int kDoRegion = 2 * C::TILE_BYTES;
+  constexpr int kAuxRegion = 4 * C::TILE_BYTES;
+  constexpr int kKvRegion = kAuxRegion + 2 * C::AUX_BYTES;
+  constexpr int kPartBytes = kKvWaves / 2 * 2 * C::NE * 4 * 1024;
+  constexpr int kRingBytes = kKvRegion + (C::V_REGS ? 0 : C::KT_BYTES);
+  constexpr int kLdsBytes = kRingBytes > kPartBytes ? kRingBytes : kPartBytes;
+  __shared__ __attribute__((aligned(16))) unsigned char smem[kLdsBytes];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int kw = w & 3, h = w >> 2;  // key block, row half
   const int l32 = lane & 31, hh = lane >> 5;
-  // Work unit (key tile kt, row chunk ch) of sequence x kv head hb; the
-  // order of units is described with kv_unit.
   const int L = blockIdx.x;
   const int hb = L % kvheads_total;
   int kt, ch;
@@ -193,26 +187,41 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
   const int chunk_rows = chunk_tiles * kKvKeys;
   const int r_lo = max(k0, ch * chunk_rows), r_hi = min(S, (ch + 1) * chunk_rows);
   if (r_lo >= r_hi) return;
-  const int wk0 = k0 + 32 * w;
+  const int wk0 = k0 + 32 * kw;
   const int key = wk0 + l32;
 
   const uint32_t q_row_bytes = qv.row_elems * 2, kv_row_bytes = kv.row_elems * 2;
-  // K and V of this lane's key as B operands (B[e][j] = K[j][e], V[j][e]).
-  bf16x8 kf[C::NS], vf[C::NS];
+  const uint32_t smem_lds = lds_addr_of(smem);
+  // K of this lane's key as B operands in registers; V too below d = 128,
+  // where it fits, else the V tile of the workgroup's keys in LDS (rows past
+  // S arrive as zeros).
+  constexpr bool kVRegs = C::V_REGS;
+  bf16x8 kf[C::NS], vf[kVRegs ? C::NS : 1];
   {
     uint32_t left;
     const rsrc_t rk = make_rsrc(view_row<false, const uint16_t>(kv, beta, k0, kvh, D, left),
                                 left * kv_row_bytes);
-    const rsrc_t rv = make_rsrc(view_row<false, const uint16_t>(vv, beta, k0, kvh, D, left),
-                                left * kv_row_bytes);
+    const rsrc_t rvr = make_rsrc(view_row<false, const uint16_t>(vv, beta, k0, kvh, D, left),
+                                 left * kv_row_bytes);
 #pragma unroll
     for (int s = 0; s < C::NS; ++s) {
       const uint32_t off = (uint32_t)(key - k0) * kv_row_bytes + (2 * s + hh) * 16;
       kf[s] = 2 * s < D / 8 ? as_bf16x8(buf_load16(rk, off)) : bf16x8{};  // columns past D
-      vf[s] = 2 * s < D / 8 ? as_bf16x8(buf_load16(rv, off)) : bf16x8{};
+      if constexpr (kVRegs) vf[s] = 2 * s < D / 8 ? as_bf16x8(buf_load16(rvr, off)) : bf16x8{};
+    }
+    wait_vmcnt<0>();  // retire the tracked loads before untracked copies start
+    if constexpr (!kVRegs) {
+      const u32x4 rv = make_rsrc_words(
+          view_row<false, const uint16_t>(vv, beta, k0, kvh, D, left), left * kv_row_bytes);
+#pragma unroll
+      for (int i = 0; i < C::KV_DMA_PER_WAVE; ++i) {
+        const int pos = (w * C::KV_DMA_PER_WAVE + i) * 64 + lane;
+        const uint32_t off = dma_src_off<C::LW, D>(pos, kv_row_bytes);
+        buf_load16_lds_async(rv, off,
+                             smem_lds + kKvRegion + (w * C::KV_DMA_PER_WAVE + i) * 1024);
+      }
     }
   }
-  wait_vmcnt<0>();  // retire the tracked loads before untracked copies start
 
   f32x16 accv[C::NE], acck[C::NE];
 #pragma unroll
@@ -225,38 +234,41 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
 
   const int steps_per_head = (r_hi - r_lo + kQM - 1) / kQM;
   const int nsteps = steps_per_head * n_rep;
-  const uint32_t smem_lds = lds_addr_of(smem);
 
   uint32_t g_off[C::DMA_PER_WAVE];
 #pragma unroll
   for (int i = 0; i < C::DMA_PER_WAVE; ++i)
     g_off[i] = dma_src_off<C::LW, D>((w * C::DMA_PER_WAVE + i) * 64 + lane, q_row_bytes);
-  // A of S^T (Q) and dP^T (dO): row l32 (+32 for the second half), chunk 2s + hh.
-  int a_off[C::NS];
+  // A of S^T (Q) and dP^T (dO): row 32h + l32 of the step, chunk 2s + hh.
+  // B of dP^T from LDS (V, at d = 128): row 32kw + l32 of the V tile, same
+  // chunk.
+  int a_off[C::NS], b_off[C::NS];
 #pragma unroll
   for (int s = 0; s < C::NS; ++s) {
-    a_off[s] = T::off(l32, 2 * s + hh);
+    a_off[s] = T::off(32 * h + l32, 2 * s + hh);
     asm volatile("" : "+v"(a_off[s]));
+    b_off[s] = kKvRegion + T::off(32 * kw + l32, 2 * s + hh);
+    asm volatile("" : "+v"(b_off[s]));
   }
-  // Transposed A of dV^T / dK^T: rows 16*s2 + 4hh (+8), columns 32n + 16*((lane/16)&1).
+  // Transposed A of dV^T / dK^T: rows 32h + 16*s2 + 4hh (+8), columns 32n + 16*((lane/16)&1).
   int t_off[C::NE][2];
 #pragma unroll
   for (int n = 0; n < C::NE; ++n)
 #pragma unroll
     for (int x = 0; x < 2; ++x) {
-      t_off[n][x] = tr_piece_off<C::LW>(4 * hh + 8 * x, 32 * n + 16 * ((lane >> 4) & 1), lane);
+      t_off[n][x] =
+          tr_piece_off<C::LW>(32 * h + 4 * hh + 8 * x, 32 * n + 16 * ((lane >> 4) & 1), lane);
       asm volatile("" : "+v"(t_off[n][x]));
     }
-
-  // Byte offset of this lane's first (LSE2, -D) value in a stage's aux block
-  // (rows 4hh..), from the LDS base.
-  int aux_lane = kAuxRegion + 16 * hh;
+  // This lane's first (LSE2, -D) value of its half in a stage's aux block.
+  int aux_lane = kAuxRegion + 4 * 32 * h + 16 * hh;
   asm volatile("" : "+v"(aux_lane));
-  // Opaque to loop-invariant code motion: offset + stage constant stays one
-  // instruction's immediate instead of a hoisted register per stage.
   auto launder_offsets = [&]() __attribute__((always_inline)) {
 #pragma unroll
-    for (int s = 0; s < C::NS; ++s) asm volatile("" : "+v"(a_off[s]));
+    for (int s = 0; s < C::NS; ++s) {
+      asm volatile("" : "+v"(a_off[s]));
+      asm volatile("" : "+v"(b_off[s]));
+    }
 #pragma unroll
     for (int n = 0; n < C::NE; ++n) {
       asm volatile("" : "+v"(t_off[n][0]));
@@ -265,45 +277,31 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
     asm volatile("" : "+v"(aux_lane));
   };
 
-  // Within each head, the first nmask_ph row steps overlap some wave's keys
-  // and take the masked path; the rest need no mask in any wave.  The two
-  // kinds run in separate inner loops, so that each keeps one set of
-  // accumulator registers.
   const int nmask_ph = kv_masked_steps(k0, r_lo, steps_per_head, kQM);
-  // Copy state.  Steps are copied strictly in order (two ahead of use): the
-  // next one to copy is step ld_t of head ld_hr of the group, first row
-  // ld_i0, and rq, rd, ra are its resources (Q and dO rows from ld_i0 on,
-  // the head's (LSE2, D) pairs).  They advance by one step's rows at a time
-  // and are rebuilt per head, so a step costs a few scalar additions.
+  // Copy state, carried from step to step as in the one-wave kernel.
   int ld_hr = 0, ld_t = 0, ld_i0 = r_lo;
   u32x4 rq, rd, ra;
-  // Lanes 0-15 copy the step's 64 LSE2 values, lanes 16-31 its 64 -D
-  // values (the padded planes hold every row the steps reach); the other
-  // lanes read zeros.
   const uint32_t aux_lane_off = lane < 16   ? 16u * lane
                                 : lane < 32 ? plane_bytes + 16u * (lane - 16)
                                             : kZeroOffset;
   auto head_resources = [&]() __attribute__((always_inline)) {
-    const int h = kvh * n_rep + ld_hr;
-    uint32_t left;  // rows from r_lo to the sequence's end; rows past it read as zeros
-    rq = make_rsrc_words(view_row<false, const uint16_t>(qv, beta, r_lo, h, D, left),
+    const int hq = kvh * n_rep + ld_hr;
+    uint32_t left;
+    rq = make_rsrc_words(view_row<false, const uint16_t>(qv, beta, r_lo, hq, D, left),
                          left * q_row_bytes);
-    rd = make_rsrc_words(view_row<false, const uint16_t>(dov, beta, r_lo, h, D, left),
+    rd = make_rsrc_words(view_row<false, const uint16_t>(dov, beta, r_lo, hq, D, left),
                          left * q_row_bytes);
-    ra = make_rsrc_words(lp + ((size_t)beta * Hl + h) * Sp, plane_bytes + (uint32_t)Sp * 4);
+    ra = make_rsrc_words(lp + ((size_t)beta * Hl + hq) * Sp, plane_bytes + (uint32_t)Sp * 4);
   };
   auto advance = [&](u32x4 &r, uint32_t bytes) __attribute__((always_inline)) {
-    const uint64_t a = (((uint64_t)r[1] << 32) | r[0]) + bytes;  // 48-bit base, stride 0
+    const uint64_t a = (((uint64_t)r[1] << 32) | r[0]) + bytes;
     r[0] = (uint32_t)a;
     r[1] = (uint32_t)(a >> 32);
-    r[2] -= bytes;  // rows left from the new first row (at least one)
+    r[2] -= bytes;
   };
   head_resources();
-  // Copies of the next step (index st, ring stage st % 2): Q and dO tiles
-  // (every wave its share), the rows' LSE2 and -D (wave 0, 1 KB of which
-  // 512 B are used).
   auto load_step = [&](int st) __attribute__((always_inline)) {
-    const uint32_t sq = (uint32_t)st % kKvStages;
+    const uint32_t sq = (uint32_t)st & 1;
     const uint32_t stage = smem_lds + sq * C::TILE_BYTES;
 #pragma unroll
     for (int i = 0; i < C::DMA_PER_WAVE; ++i) {
@@ -314,7 +312,7 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
     if (w == 0)
       buf_load16_lds_async(ra, aux_lane_off + (uint32_t)ld_i0 * 4,
                            smem_lds + kAuxRegion + sq * C::AUX_BYTES);
-    if (++ld_t == steps_per_head) {  // wave-uniform
+    if (++ld_t == steps_per_head) {
       ld_t = 0;
       ld_i0 = r_lo;
       if (++ld_hr < n_rep) head_resources();
@@ -324,150 +322,81 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
       advance(rd, kQM * q_row_bytes);
     }
   };
-  // ---- the pieces of a step (half m of ring stage stg)
-  // The step's aux block holds LSE2 of its 64 rows, then their -D.  The 16
-  // rows of half m a lane's accumulator registers hold, 32m + 8g + 4hh +
-  // {0..3} for register 4g + {0..3}, are four 16-byte reads of either part.
-  auto aux_rows = [&](int stg, int part, int m) __attribute__((always_inline)) {
+  // 16 values (rows 32h + 8g + 4hh + {0..3} of the step) of part `part`
+  // (0: LSE2, 1: -D) of stage stg's aux block.
+  auto aux_rows = [&](int stg, int part) __attribute__((always_inline)) {
     const unsigned char *a = smem + aux_lane + stg * C::AUX_BYTES + 256 * part;
     f32x16 v;
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
-      const f32x4 x = *reinterpret_cast<const f32x4 *>(a + 4 * (32 * m + 8 * g));
+      const f32x4 x = *reinterpret_cast<const f32x4 *>(a + 4 * 8 * g);
 #pragma unroll
       for (int y = 0; y < 4; ++y) v[4 * g + y] = x[y];
     }
     return v;
   };
-  // S^T and dP^T of half m: 2 NS products, each with one 16-byte LDS read;
-  // dP^T starts from -D, so that it ends as dP - D.
-  auto scores = [&](int stg, int m, f32x16 &sacc, f32x16 &pacc) __attribute__((always_inline)) {
+  // One step's half for this wave.  lim: rows of the half whose offset is
+  // below lim precede the key (masked); 0 or less for none.
+  auto step = [&](int stg, int lim, auto mask_tag) __attribute__((always_inline)) {
+    constexpr bool MASK = decltype(mask_tag)::value;
     const unsigned char *Qs = smem + stg * C::TILE_BYTES, *dOs = Qs + kDoRegion;
-    const f32x16 negd = aux_rows(stg, 1, m);
+    f32x16 sacc, pacc;
+    {
+      const f32x16 negd = aux_rows(stg, 1);
 #pragma unroll
-    for (int s = 0; s < C::NS; ++s) {
-      const bf16x8 aq = *reinterpret_cast<const bf16x8 *>(Qs + a_off[s] + m * 32 * T::ROW_BYTES);
-      const bf16x8 ad = *reinterpret_cast<const bf16x8 *>(dOs + a_off[s] + m * 32 * T::ROW_BYTES);
-      sacc = mfma32x32x16(aq, kf[s], s == 0 ? f32x16{} : sacc);
-      pacc = mfma32x32x16(ad, vf[s], s == 0 ? negd : pacc);
+      for (int s = 0; s < C::NS; ++s) {
+        const bf16x8 aq = *reinterpret_cast<const bf16x8 *>(Qs + a_off[s]);
+        const bf16x8 ad = *reinterpret_cast<const bf16x8 *>(dOs + a_off[s]);
+        bf16x8 bv;
+        if constexpr (kVRegs) bv = vf[s];
+        else bv = *reinterpret_cast<const bf16x8 *>(smem + b_off[s]);
+        sacc = mfma32x32x16(aq, kf[s], s == 0 ? f32x16{} : sacc);
+        pacc = mfma32x32x16(ad, bv, s == 0 ? negd : pacc);
+      }
     }
-  };
-  // P and dS of half m as bf16 B operands along the rows: block s2 covers rows
-  // 32m + 16*s2 .. +15, slot t <-> register 8*s2 + t.  lim: rows of the half
-  // whose offset is below lim precede the key (masked); 0 for none.
-  auto elementwise = [&](int stg, int m, f32x16 &sacc, const f32x16 &pacc, int lim, bf16x8 *bp,
-                         bf16x8 *bds) __attribute__((always_inline)) {
-    const f32x16 lse2 = aux_rows(stg, 0, m);
-    float ds[16];
+    bf16x8 bp[2], bds[2];
+    {
+      const f32x16 lse2 = aux_rows(stg, 0);
+      float ds[16];
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      float p = fast_exp2(fmaf(sacc[r], c, -lse2[r]));
-      if (8 * (r >> 2) + (r & 3) < lim) p = 0.f;
-      sacc[r] = p;
-      ds[r] = p * pacc[r];
-    }
+      for (int r = 0; r < 16; ++r) {
+        float p = fast_exp2(fmaf(sacc[r], c, -lse2[r]));
+        if (MASK && 8 * (r >> 2) + (r & 3) < lim) p = 0.f;
+        sacc[r] = p;
+        ds[r] = p * pacc[r];
+      }
 #pragma unroll
-    for (int s2 = 0; s2 < 2; ++s2) {
-      const int b8 = 8 * s2;
-      bp[s2] = as_bf16x8(u32x4{pack_bf16x2(sacc[b8 + 0], sacc[b8 + 1]),
-                               pack_bf16x2(sacc[b8 + 2], sacc[b8 + 3]),
-                               pack_bf16x2(sacc[b8 + 4], sacc[b8 + 5]),
-                               pack_bf16x2(sacc[b8 + 6], sacc[b8 + 7])});
-      bds[s2] = as_bf16x8(u32x4{pack_bf16x2(ds[b8 + 0], ds[b8 + 1]), pack_bf16x2(ds[b8 + 2], ds[b8 + 3]),
-                                pack_bf16x2(ds[b8 + 4], ds[b8 + 5]), pack_bf16x2(ds[b8 + 6], ds[b8 + 7])});
+      for (int s2 = 0; s2 < 2; ++s2) {
+        const int b8 = 8 * s2;
+        bp[s2] = as_bf16x8(u32x4{pack_bf16x2(sacc[b8 + 0], sacc[b8 + 1]),
+                                 pack_bf16x2(sacc[b8 + 2], sacc[b8 + 3]),
+                                 pack_bf16x2(sacc[b8 + 4], sacc[b8 + 5]),
+                                 pack_bf16x2(sacc[b8 + 6], sacc[b8 + 7])});
+        bds[s2] = as_bf16x8(u32x4{pack_bf16x2(ds[b8 + 0], ds[b8 + 1]),
+                                  pack_bf16x2(ds[b8 + 2], ds[b8 + 3]),
+                                  pack_bf16x2(ds[b8 + 4], ds[b8 + 5]),
+                                  pack_bf16x2(ds[b8 + 6], ds[b8 + 7])});
+      }
     }
-  };
-  // dV^T += dO^T P and dK^T += Q^T dS over half m: 4 NE products, each with
-  // two transposed LDS reads.
-  auto accumulate = [&](int stg, int m, const bf16x8 *bp, const bf16x8 *bds)
-      __attribute__((always_inline)) {
-    const unsigned char *Qs = smem + stg * C::TILE_BYTES, *dOs = Qs + kDoRegion;
+    wave_priority<1>();
 #pragma unroll
     for (int n = 0; n < C::NE; ++n)
 #pragma unroll
       for (int s2 = 0; s2 < 2; ++s2) {
-        const int ro = (2 * m + s2) * 16 * T::ROW_BYTES;
+        const int ro = s2 * 16 * T::ROW_BYTES;
         const bf16x8 av = tr_operand(dOs, t_off[n][0] + ro, t_off[n][1] + ro);
-        mfma_acc(accv[n], av, bp[s2]);
+        accv[n] = mfma32x32x16(av, bp[s2], accv[n]);
         const bf16x8 ak = tr_operand(Qs, t_off[n][0] + ro, t_off[n][1] + ro);
-        mfma_acc(acck[n], ak, bds[s2]);
+        acck[n] = mfma32x32x16(ak, bds[s2], acck[n]);
       }
-  };
-  // One step clear of the diagonal as 4 blocks of 4 NE products (2 NS = 4 NE
-  // for every head dim taken), issued one product per slot:
-  //   A: S^T, dP^T of half 0       B: S^T, dP^T of half 1 + elementwise(0)
-  //   C: accumulate(0) + elementwise(1)                D: accumulate(1)
-  // Each slot reads the operand kPf products ahead and does its share of the
-  // elementwise work; scheduling barriers keep the slots in this order.  The
-  // elementwise work of a half starts kLag slots into its block, after the
-  // products it reads have finished.
-  constexpr int kPf = 3, kLag = 2;
-  auto unmasked_step = [&](int stg) __attribute__((always_inline)) {
-    constexpr int NB = 4 * C::NE;  // products per block
-    static_assert(2 * C::NS == NB, "score and accumulate blocks have equal length");
-    constexpr int NG = 4 * NB;
-    const unsigned char *Qs = smem + stg * C::TILE_BYTES, *dOs = Qs + kDoRegion;
-    bf16x8 opnd[NG];
-    auto load_opnd = [&](int g) __attribute__((always_inline)) {
-      const int blk = g / NB, j = g % NB;
-      if (blk < 2) {  // row operand of S^T (Q) or dP^T (dO), half blk, chunk pair j/2
-        opnd[g] = *reinterpret_cast<const bf16x8 *>(((j & 1) ? dOs : Qs) + a_off[j / 2] +
-                                                      blk * 32 * T::ROW_BYTES);
-      } else {  // transposed dO (for dV) or Q (for dK), half blk-2
-        const int n = j / 4, s2 = (j / 2) % 2;
-        const int ro = (2 * (blk - 2) + s2) * 16 * T::ROW_BYTES;
-        opnd[g] = tr_operand((j & 1) ? Qs : dOs, t_off[n][0] + ro, t_off[n][1] + ro);
-      }
-    };
-    f32x16 sc[2], pc[2];      // S^T and dP^T of each half
-    bf16x8 bp[2][2], bds[2][2];
-    float pv[16], dv[16];
-    f32x16 lse2, negd0, negd1;  // LSE2 of the half in elementwise work; -D of each half
-    auto element = [&](int me, int r) __attribute__((always_inline)) {
-      const float pr = fast_exp2(fmaf(sc[me][r], c, -lse2[r]));
-      pv[r] = pr;
-      dv[r] = pr * pc[me][r];  // dP^T started from -D
-      if (r & 1) {  // registers r-1, r -> dword (r % 8) / 2 of block r / 8
-        const int b = r / 8, dw = (r % 8) / 2;
-        reinterpret_cast<uint32_t *>(&bp[me][b])[dw] = pack_bf16x2(pv[r - 1], pv[r]);
-        reinterpret_cast<uint32_t *>(&bds[me][b])[dw] = pack_bf16x2(dv[r - 1], dv[r]);
-      }
-    };
-#pragma unroll
-    for (int g = 0; g < kPf; ++g) load_opnd(g);
-    negd0 = aux_rows(stg, 1, 0);  // for the first dP^T product, slot 1
+    sched_reads_ahead<4 * C::NE, 2, 4>();
     __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-    for (int g = 0; g < NG; ++g) {
-      const int blk = g / NB, j = g % NB;
-      if (g + kPf < NG) load_opnd(g + kPf);
-      if (blk == 0 && j == 2) negd1 = aux_rows(stg, 1, 1);
-      if (blk < 2) {
-        const int s = j / 2;
-        if (j & 1)
-          pc[blk] = mfma32x32x16(opnd[g], vf[s], s == 0 ? (blk == 0 ? negd0 : negd1) : pc[blk]);
-        else sc[blk] = mfma32x32x16(opnd[g], kf[s], s == 0 ? f32x16{} : sc[blk]);
-      } else {
-        const int n = j / 4, s2 = (j / 2) % 2, mh = blk - 2;
-        if (j & 1) mfma_acc(acck[n], opnd[g], bds[mh][s2]);
-        else mfma_acc(accv[n], opnd[g], bp[mh][s2]);
-      }
-      if (blk == 1 || blk == 2) {  // elementwise of half blk-1
-        const int me = blk - 1;
-        if (j == 0) lse2 = aux_rows(stg, 0, me);
-        if (j >= kLag) {
-#pragma unroll
-          for (int r = (j - kLag) * 16 / (NB - kLag); r < (j - kLag + 1) * 16 / (NB - kLag); ++r)
-            element(me, r);
-        }
-      }
-      __builtin_amdgcn_sched_barrier(0);
-    }
+    wave_priority<0>();
   };
 
   load_step(0);
-  // Two stages: step st's copies landed (the only ones in flight), then the
-  // barrier, after which stage (st+1) % 2, last read in step st-1, is free.
+  // Two stages: step st's copies (and, before step 0, the K/V tiles)
+  // landed, then the barrier, after which stage (st+1) % 2 is free.
   auto begin_step = [&](int st) __attribute__((always_inline)) {
     wait_vmcnt<0>();
     barrier_no_fence();
@@ -478,72 +407,70 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
     for (int t = 0; t < nmask_ph; ++t, ++st) {
       begin_step(st);
       const int i0 = r_lo + t * kQM;
-      const int stg = st % kKvStages;
-      // Halves in turn, masked; halves entirely before the keys skipped
-      // (wave-uniform).
-#pragma unroll
-      for (int m = 0; m < 2; ++m) {
-        if (i0 + 32 * m + 31 < wk0) continue;
-        f32x16 sacc, pacc;
-        bf16x8 bp[2], bds[2];
-        scores(stg, m, sacc, pacc);
-        sched_reads_ahead<2 * C::NS, 1, 4>();
-        __builtin_amdgcn_sched_barrier(0);
-        elementwise(stg, m, sacc, pacc, key - i0 - 32 * m - 4 * hh, bp, bds);
-        __builtin_amdgcn_sched_barrier(0);
-        asm volatile("s_nop 1");
-        accumulate(stg, m, bp, bds);
-        __builtin_amdgcn_sched_barrier(0);
-      }
+      if (i0 + 32 * h + 31 >= wk0)  // wave-uniform: some row of the half reaches a key
+        step(st & 1, key - i0 - 32 * h - 4 * hh, std::true_type{});
     }
-    // The accumulators may be moved between the loops: cover the latency of
-    // the last products before anything reads them.
-    asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
-    // Two steps per iteration, ring stages 0 and 1 (constant in each body);
-    // a step before and one after align the loop to even steps.
     int t = nmask_ph;
     if ((st & 1) && t < steps_per_head) {
       begin_step(st);
-      unmasked_step(1);
+      step(1, 0, std::false_type{});
       ++t;
       ++st;
     }
     for (; t + 1 < steps_per_head; t += 2, st += 2) {
       launder_offsets();
       begin_step(st);
-      unmasked_step(0);
+      step(0, 0, std::false_type{});
       begin_step(st + 1);
-      unmasked_step(1);
+      step(1, 0, std::false_type{});
     }
     if (t < steps_per_head) {
       begin_step(st);
-      unmasked_step(0);
+      step(0, 0, std::false_type{});
       ++st;
     }
-    asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
   }
 
-  // The last products' results are read below: cover their latency.
-  asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
-  // acc[n][r] = (dV or dK)^T[e = 32n + 8(r/4) + 4hh + r%4][key]
-  if (key < S) {
-    uint32_t left;
-    float *ov = view_row<true, float>(dvv, beta, k0, kvh, D, left) + (size_t)ch * chunk_elems +
-                (size_t)(key - k0) * dvv.row_elems;
-    float *ok = view_row<true, float>(dkv, beta, k0, kvh, D, left) + (size_t)ch * chunk_elems +
-                (size_t)(key - k0) * dkv.row_elems;
+  // The pair's partial sums: the second waves put theirs in LDS (every step
+  // is done: no copy in flight, nothing left to read), the first add them.
+  barrier_no_fence();
+  // Slot of (key block, tensor, register group n*4 + g): 1 KB, lane l's 16
+  // bytes at 16 l.
+  auto slot = [&](int tensor, int n, int g) __attribute__((always_inline)) {
+    return smem + (((kw * 2 + tensor) * C::NE + n) * 4 + g) * 1024 + 16 * lane;
+  };
+  if (h == 1) {
 #pragma unroll
     for (int n = 0; n < C::NE; ++n)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
-        if (32 * n + 8 * g >= D) continue;  // padding columns
-        *reinterpret_cast<f32x4 *>(ov + 32 * n + 8 * g + 4 * hh) =
+        *reinterpret_cast<f32x4 *>(slot(0, n, g)) =
             f32x4{accv[n][4 * g], accv[n][4 * g + 1], accv[n][4 * g + 2], accv[n][4 * g + 3]};
-        *reinterpret_cast<f32x4 *>(ok + 32 * n + 8 * g + 4 * hh) =
-            f32x4{acck[n][4 * g] * dk_scale, acck[n][4 * g + 1] * dk_scale,
-                  acck[n][4 * g + 2] * dk_scale, acck[n][4 * g + 3] * dk_scale};
+        *reinterpret_cast<f32x4 *>(slot(1, n, g)) =
+            f32x4{acck[n][4 * g], acck[n][4 * g + 1], acck[n][4 * g + 2], acck[n][4 * g + 3]};
       }
   }
+  __syncthreads();
+  if (h == 1 || key >= S) return;
+  uint32_t left;
+  float *ov = view_row<true, float>(dvv, beta, k0, kvh, D, left) + (size_t)ch * chunk_elems +
+              (size_t)(key - k0) * dvv.row_elems;
+  float *ok = view_row<true, float>(dkv, beta, k0, kvh, D, left) + (size_t)ch * chunk_elems +
+              (size_t)(key - k0) * dkv.row_elems;
+#pragma unroll
+  for (int n = 0; n < C::NE; ++n)
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      if (32 * n + 8 * g >= D) continue;  // padding columns
+      const f32x4 pv = *reinterpret_cast<const f32x4 *>(slot(0, n, g));
+      const f32x4 pk = *reinterpret_cast<const f32x4 *>(slot(1, n, g));
+      *reinterpret_cast<f32x4 *>(ov + 32 * n + 8 * g + 4 * hh) =
+          f32x4{accv[n][4 * g] + pv[0], accv[n][4 * g + 1] + pv[1], accv[n][4 * g + 2] + pv[2],
+                accv[n][4 * g + 3] + pv[3]};
+      *reinterpret_cast<f32x4 *>(ok + 32 * n + 8 * g + 4 * hh) =
+          f32x4{(acck[n][4 * g] + pk[0]) * dk_scale, (acck[n][4 * g + 1] + pk[1]) * dk_scale,
+                (acck[n][4 * g + 2] + pk[2]) * dk_scale, (acck[n][4 * g + 3] + pk[3]) * dk_scale};
+    }
 }
 
 // ---------------------------------------------------------------- bwd_reduce
