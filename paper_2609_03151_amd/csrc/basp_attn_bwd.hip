@@ -201,13 +201,19 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
     uint32_t left;
     const rsrc_t rk = make_rsrc(view_row<false, const uint16_t>(kv, beta, k0, kvh, D, left),
                                 left * kv_row_bytes);
-    const rsrc_t rvr = make_rsrc(view_row<false, const uint16_t>(vv, beta, k0, kvh, D, left),
-                                 left * kv_row_bytes);
 #pragma unroll
     for (int s = 0; s < C::NS; ++s) {
       const uint32_t off = (uint32_t)(key - k0) * kv_row_bytes + (2 * s + hh) * 16;
       kf[s] = 2 * s < D / 8 ? as_bf16x8(buf_load16(rk, off)) : bf16x8{};  // columns past D
-      if constexpr (kVRegs) vf[s] = 2 * s < D / 8 ? as_bf16x8(buf_load16(rvr, off)) : bf16x8{};
+    }
+    if constexpr (kVRegs) {
+      const rsrc_t rv = make_rsrc(view_row<false, const uint16_t>(vv, beta, k0, kvh, D, left),
+                                  left * kv_row_bytes);
+#pragma unroll
+      for (int s = 0; s < C::NS; ++s) {
+        const uint32_t off = (uint32_t)(key - k0) * kv_row_bytes + (2 * s + hh) * 16;
+        vf[s] = 2 * s < D / 8 ? as_bf16x8(buf_load16(rv, off)) : bf16x8{};
+      }
     }
     wait_vmcnt<0>();  // retire the tracked loads before untracked copies start
     if constexpr (!kVRegs) {
@@ -242,13 +248,15 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
   // A of S^T (Q) and dP^T (dO): row 32h + l32 of the step, chunk 2s + hh.
   // B of dP^T from LDS (V, at d = 128): row 32kw + l32 of the V tile, same
   // chunk.
-  int a_off[C::NS], b_off[C::NS];
+  int a_off[C::NS], b_off[kVRegs ? 1 : C::NS];
 #pragma unroll
   for (int s = 0; s < C::NS; ++s) {
     a_off[s] = T::off(32 * h + l32, 2 * s + hh);
     asm volatile("" : "+v"(a_off[s]));
-    b_off[s] = kKvRegion + T::off(32 * kw + l32, 2 * s + hh);
-    asm volatile("" : "+v"(b_off[s]));
+    if constexpr (!kVRegs) {
+      b_off[s] = kKvRegion + T::off(32 * kw + l32, 2 * s + hh);
+      asm volatile("" : "+v"(b_off[s]));
+    }
   }
   // Transposed A of dV^T / dK^T: rows 32h + 16*s2 + 4hh (+8), columns 32n + 16*((lane/16)&1).
   int t_off[C::NE][2];
@@ -267,7 +275,7 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
 #pragma unroll
     for (int s = 0; s < C::NS; ++s) {
       asm volatile("" : "+v"(a_off[s]));
-      asm volatile("" : "+v"(b_off[s]));
+      if constexpr (!kVRegs) asm volatile("" : "+v"(b_off[s]));
     }
 #pragma unroll
     for (int n = 0; n < C::NE; ++n) {
@@ -278,15 +286,22 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
   };
 
   const int nmask_ph = kv_masked_steps(k0, r_lo, steps_per_head, kQM);
-  // Copy state, carried from step to step as in the one-wave kernel.
+  // Copy state.  Steps are copied strictly in order, one ahead of use: the
+  // next one to copy is step ld_t of head ld_hr of the group, first row
+  // ld_i0, and rq, rd, ra are its resources (Q and dO rows from ld_i0 on,
+  // the head's (LSE2, -D) planes).  They advance by one step's rows at a
+  // time and are rebuilt per head, so a step costs a few scalar additions.
   int ld_hr = 0, ld_t = 0, ld_i0 = r_lo;
   u32x4 rq, rd, ra;
+  // Lanes 0-15 copy the step's 64 LSE2 values, lanes 16-31 its 64 -D values
+  // (the padded planes hold every row the steps reach); the other lanes
+  // read zeros.
   const uint32_t aux_lane_off = lane < 16   ? 16u * lane
                                 : lane < 32 ? plane_bytes + 16u * (lane - 16)
                                             : kZeroOffset;
   auto head_resources = [&]() __attribute__((always_inline)) {
     const int hq = kvh * n_rep + ld_hr;
-    uint32_t left;
+    uint32_t left;  // rows from r_lo to the sequence's end; rows past it read as zeros
     rq = make_rsrc_words(view_row<false, const uint16_t>(qv, beta, r_lo, hq, D, left),
                          left * q_row_bytes);
     rd = make_rsrc_words(view_row<false, const uint16_t>(dov, beta, r_lo, hq, D, left),
@@ -294,12 +309,14 @@ __global__ __launch_bounds__(kKvThreads, 1) void bwd_kv_kernel(
     ra = make_rsrc_words(lp + ((size_t)beta * Hl + hq) * Sp, plane_bytes + (uint32_t)Sp * 4);
   };
   auto advance = [&](u32x4 &r, uint32_t bytes) __attribute__((always_inline)) {
-    const uint64_t a = (((uint64_t)r[1] << 32) | r[0]) + bytes;
+    const uint64_t a = (((uint64_t)r[1] << 32) | r[0]) + bytes;  // 48-bit base, stride 0
     r[0] = (uint32_t)a;
     r[1] = (uint32_t)(a >> 32);
-    r[2] -= bytes;
+    r[2] -= bytes;  // rows left from the new first row (at least one)
   };
   head_resources();
+  // Copies of step st into ring stage st % 2: Q and dO rows (every wave its
+  // share), the rows' LSE2 and -D (wave 0, 1 KB of which 512 B are used).
   auto load_step = [&](int st) __attribute__((always_inline)) {
     const uint32_t sq = (uint32_t)st & 1;
     const uint32_t stage = smem_lds + sq * C::TILE_BYTES;
