@@ -1,7 +1,8 @@
 """GPU parity of basp_attn_fwd / basp_attn_bwd against the fp64 oracle.
 
 * small shapes (several tiles plus a ragged tail, GQA ratios 1, 4, 7): every
-  output element, O and LSE, dQ, dK, dV;
+  output element, O and LSE, dQ, dK, dV; and sequence lengths that end inside
+  and at the edges of the key pass's 32-row step halves;
 * the whole share of the tiny workload (pack -> fwd -> unpack, pack dO ->
   bwd -> unpack) against the oracle's composition;
 * exact cases: O_0 = V_0 bit for bit, K = 0 gives prefix means and
@@ -63,6 +64,27 @@ SMALL = [  # b, S, Hl, Hkl, d
     (2, 2112, 4, 2, 128),    # 2 chunks, the second one 64-row step; GQA 2, b = 2
     (1, 4160, 7, 1, 64),     # 3 chunks (4160 = 2*2048 + 64), GQA 7, d = 64
 ]
+
+
+# The key pass gives each of a workgroup's 8 waves 32 keys and one 32-row
+# half of every 64-row step.  These lengths end the sequence inside the first
+# half of a step, at its end, inside the second half and just past a step,
+# and cut the 128-key tile's four key blocks at each such point.
+HALVES = [(2, S, 2, 1, d) for S in (31, 32, 33, 63, 65, 95, 97, 129, 161, 191)
+          for d in (64, 128)]
+
+
+@pytest.mark.parametrize("b,S,Hl,Hkl,d", HALVES)
+def test_key_pass_step_halves(b, S, Hl, Hkl, d):
+    log(f"[attn halves] b={b} S={S} Hl={Hl} Hkl={Hkl} d={d}")
+    q, k, v, do = _rand_local(b, S, Hl, Hkl, d, seed=7 * S + d)
+    scale = 1.0 / math.sqrt(d)
+    o, lse, dq, dk, dv = _run(q.cuda(), k.cuda(), v.cuda(), do.cuda())
+    ro, rl = oracle.attn_fwd(q, k, v, scale)
+    rdq, rdk, rdv = oracle.attn_bwd(q, k, v, do, ro, rl, scale)
+    check_close("dQ", _f64(dq), rdq)
+    check_close("dK", _f64(dk), rdk)
+    check_close("dV", _f64(dv), rdv)
 
 
 @pytest.mark.parametrize("b,S,Hl,Hkl,d", SMALL)
