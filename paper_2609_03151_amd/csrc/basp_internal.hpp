@@ -45,13 +45,18 @@ struct FastDiv {
 // whose tile lies past S, or whose rows are empty, do nothing.  Longer chunks
 // mean fewer partial sums to write and add, shorter ones more, smaller units
 // to balance; a quarter of the sequence, between 2048 and 8192 rows,
-// measured best.  Host-callable for checking.
+// measured best.  Past S = 128K the cap grows with S so that there are at
+// most 16 chunks: the partial sums take (chunks x S) rows of workspace,
+// which would otherwise grow with S squared.  Host-callable for checking.
 constexpr int kKvKeys = 128;
+constexpr int kKvMaxChunks = 16;
 
 __host__ __device__ inline int kv_chunk_rows(int S) {
   int rows = (S / 4) / kKvKeys * kKvKeys;
   if (rows < 2048) rows = 2048;
-  if (rows > 8192) rows = 8192;
+  int cap = ((S + kKvMaxChunks - 1) / kKvMaxChunks + kKvKeys - 1) / kKvKeys * kKvKeys;
+  if (cap < 8192) cap = 8192;
+  if (rows > cap) rows = cap;
   return rows;
 }
 __host__ __device__ inline int kv_units(int nchunks, int T) {

@@ -32,12 +32,15 @@ static int fail(const char *what, int S, int a, int b) {
 int main() {
   std::vector<int> lengths = {1, 2, 63, 64, 65, 127, 128, 129, 255, 256, 300, 1000, 2047, 2048,
                               2049, 2500, 4095, 4096, 4097, 6000, 8192, 16384, 32768, 65536,
-                              131072};
+                              131072, 131073, 200000, 262144, 524289};
   for (int S = 64; S <= 40000; S += 997) lengths.push_back(S);
   const int step_rows = 64;
   int checked = 0;
   for (int S : lengths) {
+    if ((S + kv_chunk_rows(S) - 1) / kv_chunk_rows(S) > kKvMaxChunks)
+      return fail("more row chunks than the cap", S, kv_chunk_rows(S), 0);
     for (int C : {kv_chunk_rows(S), 2048, 4096, 8192, 128, 384}) {
+      if (S > 131072 && C != kv_chunk_rows(S)) continue;  // long ones: the library's chunk only
       if (C % kKvKeys != 0) return fail("chunk not a multiple of the key tile", S, C, 0);
       const int T = C / kKvKeys;
       const int nch = (S + C - 1) / C;

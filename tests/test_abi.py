@@ -276,3 +276,16 @@ def test_a2a_pack_bf16_rejects_before_any_hip_call():
     assert f(a, _fake(0x2001), 1, 64, 8, 64, 2, None) == ALIGN
     assert f(a, c, 1, 1 << 22, 32, 64, 2, None) == UNSUP
     assert f(None, None, 0, 64, 8, 64, 2, None) == OK    # empty
+
+
+@pytest.mark.parametrize("S", [32768, 131072, 262144, 1 << 20])
+def test_backward_workspace_grows_linearly_with_sequence(S):
+    """The key pass's row-chunk partial sums take (chunks x S) rows; with at
+    most 16 chunks the workspace stays linear in S: the two planes plus at
+    most 16 fp32 dV and dK partials of the rank's kv heads."""
+    L = basp.lib()
+    b, H, H_kv, d, G = 1, 8, 8, 128, 8   # one local query and kv head
+    planes = 2 * b * (H // G) * ((S + 63) // 64 * 64) * 4
+    bound = planes + 256 + 2 * 16 * b * (H_kv // G) * S * d * 4
+    need = L.basp_attn_bwd_workspace_bytes(b, S, H, H_kv, d, G)
+    assert planes < need <= bound

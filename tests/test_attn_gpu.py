@@ -275,6 +275,37 @@ def test_attention_full_size_keys_every_chunk(name):
     torch.cuda.empty_cache()
 
 
+def test_long_sequence_chunk_cap():
+    """S = 131200 (just past 128K), one query and one kv head, d = 64: past
+    S = 128K the key pass caps its row chunks at a sixteenth of S rounded up
+    to the key tile (here 16 chunks of 8320 rows, the last 6400), so the
+    workspace stays linear in S.  dK and dV of the keys in the last 6528 rows
+    (the tail of chunk 14, summing the partials of two chunks, and all of
+    chunk 15) and dQ, O, LSE of those rows against the oracle, and the
+    invariants over every key."""
+    b, S, Hl, Hkl, d = 1, 131200, 1, 1, 64
+    log(f"[attn long] b={b} S={S} Hl={Hl} Hkl={Hkl} d={d}")
+    q, k, v, do = _rand_local(b, S, Hl, Hkl, d, seed=2621)
+    scale = 1.0 / math.sqrt(d)
+    o, lse, dq, dk, dv = _run(q.cuda(), k.cuda(), v.cuda(), do.cuda())
+    log("  GPU done")
+    r0 = 15 * 8320 - 128
+    q64, k64, v64, do64 = (x.double().numpy() for x in (q, k, v, do))
+    to, tl = oracle.attn_fwd(q64, k64, v64, scale, r0, S)
+    tdq, tdk, tdv = oracle.attn_bwd(q64, k64, v64, do64, to, tl, scale, r0)
+    log("  oracle tail done")
+    check_close("O tail", _f64(o[:, r0:]), to)
+    check_close("LSE tail", _f64(lse[:, :, r0:]), tl, max_abs=LSE_MAX_ABS, mean_abs=LSE_MAX_ABS)
+    check_close("dQ tail", _f64(dq[:, r0:]), tdq)
+    check_close("dK tail", _f64(dk[:, r0:]), tdk)
+    check_close("dV tail", _f64(dv[:, r0:]), tdv)
+    dk_sum = dk.double().sum(dim=1)
+    assert float((dk_sum.abs() / dk.double().abs().sum(dim=1).clamp_min(1e-30)).max()) < 1e-3
+    do_sum = do.double().sum(dim=1).cuda()
+    rel = ((dv.double().sum(dim=1) - do_sum).abs().max() / do_sum.abs().max()).item()
+    assert rel < 1e-3
+
+
 @pytest.mark.parametrize("name", ["llama3_8b_s32k", "qwen25_7b_s64k", "ulysses_g8_b2_s64k",
                                   "basp_g4_b1_s64k", "llama3_70b_s128k"])
 def test_attention_full_size_kv_head_fp64(name):
