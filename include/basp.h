@@ -260,8 +260,10 @@ int basp_attn_fwd_sharded(const void *const *q_shards,
 /* Bytes of device workspace basp_attn_bwd (and basp_attn_bwd_sharded) needs
  * for this share of the Sec. II-A attention backward: the per-row pair
  * (LSE, D_i = dO_i . O_i) of every local query head, and, when S is longer
- * than one row chunk of the key pass (a quarter of S, 2048 to 8192 rows),
- * fp32 partial sums of dK and dV per chunk.  0 for an invalid shape, and
+ * than one row chunk of the key pass (a quarter of S, 2048 to 8192 rows;
+ * past S = 128K a sixteenth of S, so never more than 16 chunks and a
+ * workspace linear in S), fp32 partial sums of dK and dV per chunk.  0 for
+ * an invalid shape, and
  * for an empty one (b == 0 or S == 0), which needs none. */
 size_t basp_attn_bwd_workspace_bytes(int b, int S, int H, int H_kv, int d,
                                      int G);
